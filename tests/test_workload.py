@@ -1,0 +1,40 @@
+"""The shared seeded input generator: host and device backends agree bit for
+bit, and the draws have the intended shapes and moments."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2607_11185_amd import workload as WL
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_numpy_and_torch_backends_identical(dtype):
+    idx = np.arange(1000, 9000)
+    a = WL.normal_np(3, 1, idx, 0.02, dtype)
+    b = WL.normal_torch(3, 1, 1000, 8000, 0.02, dtype, device="cpu", chunk=3000)
+    assert np.array_equal(a, b.to(torch.float64).numpy())
+    ti = WL.uniform_int_np(3, 5, idx, 151936)
+    tt = WL.uniform_int_torch(3, 5, 1000, 8000, 151936, device="cpu")
+    assert np.array_equal(ti, tt.numpy())
+
+
+def test_moments_and_ranges():
+    z = WL.normal_np(0, 1, np.arange(200000), 1.0, "f32")
+    assert abs(z.mean()) < 0.01 and abs(z.var() - 1.0) < 0.01
+    t = WL.uniform_int_np(0, 5, np.arange(100000), 1024)
+    assert t.min() >= 0 and t.max() < 1024
+
+
+def test_large_index_counters_differ():
+    a = WL.normal_np(0, 1, np.array([5, (1 << 32) + 5]), 1.0, "f32")
+    assert a[0] != a[1]
+
+
+def test_spans_of_configs():
+    sp = WL.make_spans(WL.SEVEN_B)
+    assert sp.num_traj == 8 and sp.num_steps == 240
+    assert sp.text_len.min() >= 150 and sp.text_len.max() <= 400
+    assert (sp.action_len == 32).all() and (sp.img_len == 2691).all()
+    lg = WL.make_spans(WL.LONG)
+    T = np.diff(lg.step_offsets)
+    assert T.min() >= 10 and T.max() <= 50
