@@ -1,0 +1,231 @@
+/*
+ * seg.h - C ABI of libseg: the segmented training hot path of Visual Context
+ * Segmentation (ScaleCUA, Sec. 3.3 "Visual Context Segmentation for
+ * Long-Horizon Multimodal RL", App. D "Sliding-Window Details", Eq. (loss) of
+ * App. E) on AMD Instinct MI355X (gfx950).
+ *
+ * A trajectory is a system prompt followed by T turns; turn j carries one
+ * screenshot (an image-token block of img_len tokens) and one text block of
+ * text_len tokens whose last action_len tokens are the trained action tokens.
+ * Trajectories are cut into segments of at most L turns; inside a segment every
+ * earlier text token stays visible while a screenshot is visible only to the
+ * queries of the W turns starting at its own (the sliding window of W
+ * screenshots, Sec. 3.3).  The library builds the packed layout and a 128x128
+ * block-sparse tile map of it, runs masked GQA attention forward and backward
+ * over the packed segments, and computes the action-token log-probs with the
+ * clipped policy-ratio loss and its gradients.
+ *
+ * Conventions (all entry points):
+ *  - "host" pointers are host memory; every other pointer is device memory on
+ *    the current HIP device.  The caller owns all memory, including workspace;
+ *    the library allocates no device memory.
+ *  - Work is enqueued asynchronously on `stream`, except where a function says
+ *    otherwise.  Arguments are validated on the host before any launch; on a
+ *    non-OK status nothing has been enqueued unless the status is SEG_ERR_HIP.
+ *  - No exception crosses the ABI.  A non-OK status leaves a thread-local
+ *    message readable with seg_last_error().
+ *  - Reductions run in a fixed order: repeated calls on the same inputs give
+ *    bitwise-identical outputs.  Integer atomics are used only where their
+ *    result does not depend on order.
+ *  - Numeric kernels compute in bf16 with fp32 accumulation (MFMA).  SEG_F32
+ *    inputs are rounded to bf16 (nearest-even) when loaded; outputs are written
+ *    in the input dtype unless stated otherwise.
+ */
+#ifndef SEG_H
+#define SEG_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SEG_OK = 0,
+  SEG_ERR_ARG = 1,         /* invalid argument (null pointer, bad span, mismatched sizes) */
+  SEG_ERR_CAPACITY = 2,    /* a turn does not fit max_seg_tokens / buffer_tokens, or int32 overflow */
+  SEG_ERR_WORKSPACE = 3,   /* ws_bytes smaller than the required workspace */
+  SEG_ERR_UNSUPPORTED = 4, /* shape the kernels do not support (head_dim, tile, head ratio) */
+  SEG_ERR_HIP = 5          /* a HIP call failed; the message holds the HIP error string */
+} seg_status;
+
+typedef enum { SEG_BF16 = 0, SEG_F32 = 1 } seg_dtype;
+
+/* Token kinds, stored in tok_meta = turn << 2 | kind (the prompt has turn 0). */
+enum { SEG_KIND_PROMPT = 0, SEG_KIND_IMAGE = 1, SEG_KIND_TEXT = 2, SEG_KIND_PAD = 3 };
+/* Tile classes stored in the CSR maps (skipped tiles are not stored). */
+enum { SEG_TILE_PARTIAL = 1, SEG_TILE_FULL = 2 };
+/* Fields of one seg_info record. */
+enum {
+  SEG_INFO_TRAJ = 0, SEG_INFO_FIRST_TURN = 1, SEG_INFO_END_TURN = 2, SEG_INFO_START = 3,
+  SEG_INFO_LEN = 4, SEG_INFO_QTILE_BASE = 5, SEG_INFO_LOSS_BASE = 6, SEG_INFO_LOSS_COUNT = 7,
+  SEG_INFO_FIELDS = 8
+};
+
+/*
+ * A batch of trajectories (all arrays host memory, read during the call).
+ * Turns of trajectory i are steps [step_offsets[i], step_offsets[i+1]), numbered
+ * 1..T inside the trajectory.  prompt_len >= 1; img_len, text_len >= 0;
+ * 0 <= action_len <= text_len.  A trajectory with no turns yields no segment.
+ *
+ * Segmentation (Sec. 3.3, App. D; the segment length L plays the removal
+ * threshold Delta and W the kept-screenshot count K):
+ *   - turns are cut into runs [a, b) of at most seg_steps turns, closed early
+ *     when the next turn would push the segment past max_seg_tokens (0 = no cap);
+ *   - segment [a, b) holds the prompt, then for every turn j < b its screenshot
+ *     if j > a - W and its text (older screenshots are dropped, all text kept);
+ *   - with buffer_tokens > 0 segments are packed in order into buffers of that
+ *     many rows: a segment that does not fit the current buffer opens the next
+ *     one, and the tail of a buffer is padding (tok_src = -1, kind PAD).
+ * Visibility inside a segment: key k is visible to query q iff k is not after q
+ * and k is not a screenshot token of a turn <= turn(q) - W.
+ * tile: tile edge of the block-sparse map; 128 for the numeric kernels, any
+ * value >= 1 for layout-only use.
+ */
+typedef struct {
+  int32_t num_traj;
+  const int32_t *step_offsets; /* host [num_traj+1], step_offsets[0] = 0, non-decreasing */
+  const int32_t *prompt_len;   /* host [num_traj] */
+  const int32_t *img_len;      /* host [num_steps] screenshot tokens of each turn */
+  const int32_t *text_len;     /* host [num_steps] non-image tokens of each turn */
+  const int32_t *action_len;   /* host [num_steps] trained tokens = last action_len text tokens */
+  int32_t window;              /* W >= 1: screenshots visible to a turn, its own included */
+  int32_t seg_steps;           /* L >= 1: turns per segment (1 = step-wise decomposition) */
+  int32_t max_seg_tokens;      /* 0 = no cap */
+  int32_t buffer_tokens;       /* 0 = one contiguous packed buffer */
+  int32_t tile;                /* >= 1 */
+} seg_problem;
+
+typedef struct {
+  int32_t num_segments;
+  int32_t num_buffers;
+  int32_t loss_rows;      /* R: trained action tokens */
+  int32_t num_qtiles;     /* tiles over all segments (q-tiles = k-tiles) */
+  int32_t num_steps;
+  int32_t pad0;
+  int64_t packed_tokens;  /* rows of the packed buffer, padding included */
+  int64_t traj_tokens;    /* canonical tokens of the batch */
+  int64_t tile_nnz_max;   /* lower-triangular tile count: bound on non-skipped tiles */
+  size_t workspace_bytes; /* workspace needed by seg_build_layout */
+} seg_sizes;
+
+/*
+ * Device arrays of a layout, sized from seg_sizes (S segments, P packed rows,
+ * R loss rows, G q-tiles, Z = tile_nnz_max).  Filled by seg_build_layout, which
+ * also sets the scalars `window` and `tile`.
+ */
+typedef struct {
+  int32_t *seg_info;      /* [S*8] see SEG_INFO_*; turns are 1-based, segments in packed order */
+  int32_t *tok_src;       /* [P] canonical token index (trajectory-major canonical order), -1 = pad */
+  int32_t *tok_meta;      /* [P] turn << 2 | kind */
+  int32_t *loss_pred_row; /* [R] packed row predicting the action token (its position - 1) */
+  int32_t *loss_tgt_src;  /* [R] canonical index of the action token */
+  int32_t *loss_traj;     /* [R] trajectory of the row (selects the advantage) */
+  int32_t *tile_seg;      /* [G] segment of each tile */
+  int32_t *qt_ptr;        /* [G+1] CSR over q-tiles: non-skipped k-tiles, ascending */
+  int32_t *qt_col;        /* [Z] global tile index of the k-tile */
+  uint8_t *qt_cls;        /* [Z] SEG_TILE_PARTIAL or SEG_TILE_FULL */
+  int32_t *kt_ptr;        /* [G+1] transposed CSR over k-tiles: non-skipped q-tiles, ascending */
+  int32_t *kt_row;        /* [Z] */
+  uint8_t *kt_cls;        /* [Z] */
+  int64_t *seg_pairs;     /* [S] exact visible (query, key) pairs of each segment */
+  int64_t *tile_nnz;      /* [1] non-skipped tiles */
+  int32_t *work_order;    /* [G] tiles by decreasing CSR row length (ties: ascending index) */
+  int32_t window;         /* set by seg_build_layout */
+  int32_t tile;           /* set by seg_build_layout */
+} seg_layout;
+
+/* Sizes of the layout of `p` (host only, no HIP call).  Errors: SEG_ERR_ARG for
+ * invalid spans or parameters, SEG_ERR_CAPACITY when a single turn exceeds the
+ * cap or the buffer, or a count overflows int32. */
+seg_status seg_layout_query(const seg_problem *p, seg_sizes *out);
+
+/* Build every array of `out` for `p` (Sec. 3.3 / App. D segmentation, the
+ * sliding-window visibility and the tile map).  `sz` must be the result of
+ * seg_layout_query(p); `ws` >= sz->workspace_bytes.  The segment table is
+ * computed on the host and uploaded to `ws`; the call waits on `stream` once
+ * after that small upload, then enqueues the token, loss-row and tile kernels. */
+seg_status seg_build_layout(const seg_problem *p, const seg_sizes *sz, seg_layout *out,
+                            void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Workspace of seg_attn_fwd (bwd = 0) or seg_attn_bwd (bwd = 1). */
+size_t seg_attn_workspace_bytes(const seg_sizes *sz, seg_dtype dt, int32_t hq, int32_t hkv,
+                                int32_t d, int32_t bwd);
+
+/*
+ * Masked GQA attention forward over the packed segments (the attention of the
+ * policy forward pass on VCS training items, Sec. 3.3).  Query head h reads
+ * key/value head h / (hq / hkv).  Tiles classed as skipped are never touched;
+ * partial tiles apply the visibility rule per element.
+ *   q [P, hq, d], k/v [P, hkv, d] (dtype dt, row-major);
+ *   o [P, hq, d] (dtype dt); lse [hq, P] fp32, natural-log sum of exp of the
+ *   scaled scores of each row.  Padding rows of o and lse are not written.
+ * Supported: d in {64, 128}, hq % hkv == 0, layout tile == 128.
+ */
+seg_status seg_attn_fwd(const seg_layout *L, const seg_sizes *sz, seg_dtype dt, int32_t hq,
+                        int32_t hkv, int32_t d, float softmax_scale, const void *q,
+                        const void *k, const void *v, void *o, float *lse, void *ws,
+                        size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Backward of seg_attn_fwd: given dO, the gradients of sum(O * dO) w.r.t. q, k
+ * and v.  dk/dv of a kv head sum the contributions of all its query heads.
+ * dq [P, hq, d], dk/dv [P, hkv, d] in dtype dt; padding rows are not written.
+ * o and lse are the outputs of seg_attn_fwd on the same inputs.
+ */
+seg_status seg_attn_bwd(const seg_layout *L, const seg_sizes *sz, seg_dtype dt, int32_t hq,
+                        int32_t hkv, int32_t d, float softmax_scale, const void *q,
+                        const void *k, const void *v, const void *o, const float *lse,
+                        const void *d_o, void *dq, void *dk, void *dv, void *ws,
+                        size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Settings of the clipped policy-ratio objective (Eq. (loss), App. E):
+ * per row, rho = exp(logp - old_logp), A = adv[row_traj];
+ * objective = min(rho A, clip(rho, 1 - eps_low, 1 + eps_high) A), and when
+ * dual_clip_c > 0 and A < 0, objective = max(objective, dual_clip_c A);
+ * loss_tok = -objective; loss_sum = loss_scale * sum(loss_tok).  Logits are
+ * logit_scale * h W^T.  Clipping uses strict inequalities.
+ */
+typedef struct {
+  float eps_low;
+  float eps_high;
+  float dual_clip_c;  /* <= 0: off */
+  float loss_scale;
+  float logit_scale;
+  int32_t want_grad;  /* 0: forward only (dh and dw untouched, may be NULL) */
+} seg_loss_cfg;
+
+size_t seg_logprob_workspace_bytes(int32_t rows, int32_t hidden, int32_t vocab, seg_dtype dt);
+
+/*
+ * Fused action-token log-prob, clipped-ratio loss and gradients.
+ *   h [n_h, hidden] (dtype dt) hidden states; row_index [rows] selects the rows
+ *   of h to use (e.g. loss_pred_row), or NULL to use rows 0..rows-1;
+ *   w [vocab, hidden] (dtype dt) output projection; target [rows] token ids in
+ *   [0, vocab); old_logp [rows] fp32 rollout log-probs; adv [num_traj] fp32;
+ *   row_traj [rows] index into adv.
+ * Outputs: logp, loss_tok [rows] fp32; clipped [rows] (1 where the clipped
+ * branch is taken, so the row has no gradient); loss_sum [1] fp32;
+ * with want_grad: dh [rows, hidden] (dtype dt) and dw [vocab, hidden] fp32
+ * (overwritten), the gradients of loss_sum.
+ */
+seg_status seg_logprob_loss(int32_t rows, int32_t hidden, int32_t vocab, seg_dtype dt,
+                            const void *h, const int32_t *row_index, const void *w,
+                            const int32_t *target, const float *old_logp, const float *adv,
+                            const int32_t *row_traj, int32_t num_traj, const seg_loss_cfg *cfg,
+                            float *logp, float *loss_tok, uint8_t *clipped, float *loss_sum,
+                            void *dh, float *dw, void *ws, size_t ws_bytes,
+                            hipStream_t stream);
+
+/* Message of the last non-OK status on the calling thread ("" if none). */
+const char *seg_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SEG_H */

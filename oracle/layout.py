@@ -124,6 +124,34 @@ def visibility(seg: Segment, W: int) -> np.ndarray:
     return causal & ~expired
 
 
+def visibility_rows(seg: Segment, W: int, rows) -> np.ndarray:
+    """Rows ``rows`` of the dense mask of :func:`visibility`."""
+    rows = np.asarray(rows)
+    ki = np.arange(seg.length)[None, :]
+    causal = ki <= rows[:, None]
+    expired = (seg.kind[None, :] == KIND_IMAGE) & (seg.step[None, :] <= seg.step[rows][:, None] - W)
+    return causal & ~expired
+
+
+def segment_tiles(seg: Segment, W: int, tile: int):
+    """Class grid [nt, nt] of one segment (0 = skip, PARTIAL, FULL) and its
+    exact visible-pair count, read off the dense mask: a tile is skipped when
+    it holds no visible pair and FULL when it is tile x tile and every pair
+    is visible."""
+    mask = visibility(seg, W)
+    n = seg.length
+    nt = -(-n // tile)
+    cls = np.zeros((nt, nt), np.int64)
+    for i in range(nt):
+        for j in range(nt):
+            sub = mask[i * tile:(i + 1) * tile, j * tile:(j + 1) * tile]
+            if not sub.any():
+                continue
+            full = sub.shape == (tile, tile) and bool(sub.all())
+            cls[i, j] = CLS_FULL if full else CLS_PARTIAL
+    return cls, int(mask.sum())
+
+
 @dataclasses.dataclass
 class Layout:
     segments: List[Segment]
@@ -215,16 +243,8 @@ def build(spans, W, L, tile, cap=0, buffer_tokens=0, with_tiles=True) -> Layout:
         seg_info[si] = [sg.traj, sg.a, sg.b, sg.start, n, qbase, loss_base, seg_nloss[si]]
         loss_base += seg_nloss[si]
         if with_tiles:
-            mask = visibility(sg, W)
-            pairs.append(int(mask.sum()))
-            cls = np.zeros((nt, nt), np.int64)
-            for i in range(nt):
-                for j in range(nt):
-                    sub = mask[i * tile:(i + 1) * tile, j * tile:(j + 1) * tile]
-                    if not sub.any():
-                        continue
-                    full = sub.shape == (tile, tile) and bool(sub.all())
-                    cls[i, j] = CLS_FULL if full else CLS_PARTIAL
+            cls, npairs = segment_tiles(sg, W, tile)
+            pairs.append(npairs)
             for i in range(nt):
                 qt_rows.append([(qbase + j, int(cls[i, j])) for j in range(nt) if cls[i, j]])
             for j in range(nt):

@@ -1,0 +1,497 @@
+// Fused action-token log-prob and clipped policy-ratio loss with gradients
+// (Eq. (loss) of App. E: min(rho A, clip(rho, 1 - eps_l, 1 + eps_h) A) over the
+// trained action tokens, rho = pi_theta / pi_rollout), bf16 MFMA on gfx950.
+//
+// Only the R action rows are projected onto the vocabulary.  Pipeline:
+//   1. zT[v][r] = s * W[v] . h[r] (MFMA, fp32 out) with a fused epilogue that
+//      writes per-(row, 128-vocab tile) max / sum-exp partials and captures the
+//      target logit;
+//   2. per row: LSE from the partials (fixed order), logp, rho, loss, the
+//      clipped flag and g = d loss_sum / d logp;
+//   3. dz = g * (onehot(target) - softmax(z)) as bf16, written in both
+//      orientations (one pass over zT);
+//   4. dH = s * dz W and dW = s * dz^T h (MFMA).
+// All GEMMs use one "NT" kernel: C[m][n] = sum_k A[m][k] B[n][k] with both
+// operands k-contiguous, 128x128 block tiles, 4 waves of 64x64.
+#include <climits>
+#include <cmath>
+
+#include "common.h"
+
+namespace seg {
+namespace {
+
+constexpr int BM = 128, BN = 128, BK = 32;
+constexpr float LOG2E = 1.4426950408889634f;
+constexpr float LN2 = 0.6931471805599453f;
+
+__device__ __forceinline__ bf16x8 as_bf8(const u16x8 &v) { return __builtin_bit_cast(bf16x8, v); }
+
+// Epilogue of the logits GEMM (M = vocab, N = rows).
+struct EpiLogits {
+  float *zt;        // [M][ldz] fp32
+  long ldz;
+  float2 *stats;    // [M/BM tiles][N]: (max, sum exp(z - max)) in log2 units
+  int nrows;        // N
+  const int32_t *target;  // [N]
+  float *ztgt;      // [N]
+  float scale;
+};
+
+// Epilogue writing C (times scale) as dtype TO with leading dimension ldc.
+template <class TO>
+struct EpiStore {
+  TO *c;
+  long ldc;
+  float scale;
+};
+
+template <class Epi>
+__device__ __forceinline__ void epilogue(const Epi &, const f32x16 (&)[2][2], int, int, int, int,
+                                         int, int, int, int);
+
+template <class TO>
+__device__ __forceinline__ void epilogue_store(const EpiStore<TO> &ep, const f32x16 (&acc)[2][2],
+                                               int m0, int n0, int M, int N, int wm, int wn,
+                                               int col, int hh) {
+#pragma unroll
+  for (int bm = 0; bm < 2; ++bm)
+#pragma unroll
+    for (int bn = 0; bn < 2; ++bn) {
+      const int n = n0 + wn * 64 + bn * 32 + col;
+      if (n >= N) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = m0 + wm * 64 + bm * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+        if (m < M) store_val(ep.c, (long)m * ep.ldc + n, acc[bm][bn][r] * ep.scale);
+      }
+    }
+}
+
+// C[m][n] = sum_k A[m][k] * B[n][k]; K % 32 == 0 is not required but
+// lda/ldb/K must be multiples of 8 (16-byte chunks).  Rows beyond M / N and
+// chunks beyond K are read as zero.
+template <int EPI, class Epi>
+__global__ void __launch_bounds__(256, 2) k_gemm_nt(const unsigned short *__restrict__ A, long lda,
+                                                    const unsigned short *__restrict__ B, long ldb,
+                                                    int M, int N, int K, Epi ep) {
+  __shared__ unsigned short sA[2][BM * BK];
+  __shared__ unsigned short sB[2][BN * BK];
+  __shared__ float2 sStat[2][BN];
+  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int wm = wave >> 1, wn = wave & 1, col = lane & 31, hh = lane >> 5;
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+
+  auto load = [&](int kt, int buf) {
+#pragma unroll
+    for (int it = 0; it < 2; ++it) {
+      const int c = tid + it * 256;
+      const int row = c >> 2, ch = c & 3;
+      const int gk = kt * BK + ch * 8;
+      const int sw = (ch ^ ((row >> 2) & 3)) * 8;
+      u16x8 va = {0, 0, 0, 0, 0, 0, 0, 0}, vb = va;
+      if (m0 + row < M && gk < K) va = *reinterpret_cast<const u16x8 *>(A + (long)(m0 + row) * lda + gk);
+      if (n0 + row < N && gk < K) vb = *reinterpret_cast<const u16x8 *>(B + (long)(n0 + row) * ldb + gk);
+      *reinterpret_cast<u16x8 *>(&sA[buf][row * BK + sw]) = va;
+      *reinterpret_cast<u16x8 *>(&sB[buf][row * BK + sw]) = vb;
+    }
+  };
+
+  const int nk = (K + BK - 1) / BK;
+  load(0, 0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) load(kt + 1, buf ^ 1);
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const int ch = kk * 2 + hh;
+      bf16x8 a[2], b[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int ra = wm * 64 + i * 32 + col;
+        const int rb = wn * 64 + i * 32 + col;
+        a[i] = *reinterpret_cast<const bf16x8 *>(&sA[buf][ra * BK + ((ch ^ ((ra >> 2) & 3)) * 8)]);
+        b[i] = *reinterpret_cast<const bf16x8 *>(&sB[buf][rb * BK + ((ch ^ ((rb >> 2) & 3)) * 8)]);
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = mfma32(a[i], b[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+
+  if constexpr (EPI == 0) {
+    // logits: C[m = vocab][n = row]; accumulator lane holds one row n
+    const EpiLogits &e = ep;
+#pragma unroll
+    for (int bn = 0; bn < 2; ++bn) {
+      const int n = n0 + wn * 64 + bn * 32 + col;
+      const bool nok = n < N;
+      const int tgt = nok ? e.target[n] : -1;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int bm = 0; bm < 2; ++bm)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int m = m0 + wm * 64 + bm * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+          const float z = acc[bm][bn][r] * e.scale;
+          if (nok && m < M) {
+            e.zt[(long)m * e.ldz + n] = z;
+            if (m == tgt) e.ztgt[n] = z;
+            mx = fmaxf(mx, z * LOG2E);
+          }
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      float sm = 0.f;
+      if (mx != -INFINITY) {
+#pragma unroll
+        for (int bm = 0; bm < 2; ++bm)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int m = m0 + wm * 64 + bm * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+            if (m < M) sm += exp2f(acc[bm][bn][r] * e.scale * LOG2E - mx);
+          }
+      }
+      sm += __shfl_xor(sm, 32, 64);
+      if (hh == 0) sStat[wm][wn * 64 + bn * 32 + col] = make_float2(mx, sm);
+    }
+    __syncthreads();
+    if (tid < BN && n0 + tid < N) {
+      const float2 a = sStat[0][tid], b = sStat[1][tid];
+      const float mx = fmaxf(a.x, b.x);
+      float sm = 0.f;
+      if (mx != -INFINITY) {
+        if (a.x != -INFINITY) sm += a.y * exp2f(a.x - mx);
+        if (b.x != -INFINITY) sm += b.y * exp2f(b.x - mx);
+      }
+      e.stats[(long)blockIdx.y * e.nrows + n0 + tid] = make_float2(mx, sm);
+    }
+  } else {
+    epilogue_store(ep, acc, m0, n0, M, N, wm, wn, col, hh);
+  }
+}
+
+// Per row: LSE over the vocab-tile partials (fixed order), then the loss.
+__global__ void __launch_bounds__(256) k_row_loss(
+    const float2 *__restrict__ stats, int ntiles, int rows, const float *__restrict__ ztgt,
+    const float *__restrict__ old_logp, const float *__restrict__ adv,
+    const int32_t *__restrict__ row_traj, int num_traj, seg_loss_cfg cfg, float *__restrict__ logp,
+    float *__restrict__ loss_tok, uint8_t *__restrict__ clipped, float *__restrict__ lse_out,
+    float *__restrict__ g_out) {
+  __shared__ float2 red[256];
+  const int r = blockIdx.x, t = threadIdx.x;
+  float mx = -INFINITY, sm = 0.f;
+  for (int i = t; i < ntiles; i += 256) {
+    const float2 p = stats[(long)i * rows + r];
+    if (p.x == -INFINITY) continue;
+    if (p.x > mx) {
+      sm = sm * exp2f(mx - p.x) + p.y;
+      mx = p.x;
+    } else {
+      sm += p.y * exp2f(p.x - mx);
+    }
+  }
+  red[t] = make_float2(mx, sm);
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (t < o) {
+      const float2 a = red[t], b = red[t + o];
+      const float m2 = fmaxf(a.x, b.x);
+      float s2 = 0.f;
+      if (m2 != -INFINITY) {
+        if (a.x != -INFINITY) s2 += a.y * exp2f(a.x - m2);
+        if (b.x != -INFINITY) s2 += b.y * exp2f(b.x - m2);
+      }
+      red[t] = make_float2(m2, s2);
+    }
+    __syncthreads();
+  }
+  if (t == 0) {
+    const float lse = (red[0].x + log2f(red[0].y)) * LN2;
+    const float lp = ztgt[r] - lse;
+    // an out-of-range trajectory index yields NaN rather than a stray read
+    const int tj = row_traj[r];
+    const float A = (tj >= 0 && tj < num_traj) ? adv[tj] : __builtin_nanf("");
+    const float rho = expf(lp - old_logp[r]);
+    const float lo = 1.f - cfg.eps_low, hi = 1.f + cfg.eps_high;
+    const float unc = rho * A;
+    const float clp = fminf(fmaxf(rho, lo), hi) * A;
+    float obj = fminf(unc, clp);
+    bool cl = (A > 0.f && rho > hi) || (A < 0.f && rho < lo);
+    if (cfg.dual_clip_c > 0.f && A < 0.f) {
+      obj = fmaxf(obj, cfg.dual_clip_c * A);
+      cl = cl || rho > cfg.dual_clip_c;
+    }
+    logp[r] = lp;
+    loss_tok[r] = -obj;
+    clipped[r] = cl ? 1 : 0;
+    lse_out[r] = lse;
+    g_out[r] = cl ? 0.f : -cfg.loss_scale * rho * A;
+  }
+}
+
+// loss_sum = loss_scale * sum(loss_tok), fixed-order reduction in one block.
+__global__ void __launch_bounds__(256) k_loss_sum(const float *__restrict__ loss_tok, int rows,
+                                                  float scale, float *__restrict__ out) {
+  __shared__ double red[256];
+  const int t = threadIdx.x;
+  double s = 0.0;
+  for (int i = t; i < rows; i += 256) s += (double)loss_tok[i];
+  red[t] = s;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (t < o) red[t] += red[t + o];
+    __syncthreads();
+  }
+  if (t == 0) *out = (float)(red[0] * (double)scale);
+}
+
+// dz = g[r] * (onehot(target[r]) - exp(z - lse[r])), from zT [V][ldz] to
+// dz [Rp][Vp] and dzT [Vp][Rp] (bf16, zero in the padding).  64x64 tiles.
+__global__ void __launch_bounds__(256) k_dz(const float *__restrict__ zt, long ldz, int V, int R,
+                                            int Vp, int Rp, const float *__restrict__ lse,
+                                            const float *__restrict__ g,
+                                            const int32_t *__restrict__ target,
+                                            unsigned short *__restrict__ dz,
+                                            unsigned short *__restrict__ dzt) {
+  __shared__ unsigned short t[64][66];
+  const int v0 = blockIdx.y * 64, r0 = blockIdx.x * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  const int r = r0 + tx;
+  const bool rok = r < R;
+  const float lr = rok ? lse[r] : 0.f, gr = rok ? g[r] : 0.f;
+  const int tg = rok ? target[r] : -1;
+  for (int i = ty; i < 64; i += 4) {
+    const int v = v0 + i;
+    float val = 0.f;
+    if (rok && v < V) {
+      const float p = expf(zt[(long)v * ldz + r] - lr);
+      val = gr * ((v == tg ? 1.f : 0.f) - p);
+    }
+    const unsigned short b = f2bf_bits(val);
+    if (v < Vp && r < Rp) dzt[(long)v * Rp + r] = b;
+    t[i][tx] = b;
+  }
+  __syncthreads();
+  for (int i = ty; i < 64; i += 4) {
+    const int rr = r0 + i, v = v0 + tx;
+    if (rr < Rp && v < Vp) dz[(long)rr * Vp + v] = t[tx][i];
+  }
+}
+
+// y[c][r] = x[r][c] for a [rows][cols] matrix (ldx), output [cols][ldy]; x is
+// bf16 bits or fp32 (rounded); optional row gather; zero for r >= rows up to
+// pad_rows.
+template <class TI>
+__global__ void __launch_bounds__(256) k_transpose2d(const TI *__restrict__ x, long ldx,
+                                                     const int32_t *__restrict__ rowmap, int rows,
+                                                     int cols, int pad_rows,
+                                                     unsigned short *__restrict__ y, long ldy) {
+  __shared__ unsigned short t[64][66];
+  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int i = ty; i < 64; i += 4) {
+    const int r = r0 + i, c = c0 + tx;
+    unsigned short b = 0;
+    if (r < rows && c < cols) {
+      const long sr = rowmap ? rowmap[r] : r;
+      b = load_bf(x, sr * ldx + c);
+    }
+    t[i][tx] = b;
+  }
+  __syncthreads();
+  for (int i = ty; i < 64; i += 4) {
+    const int c = c0 + i, r = r0 + tx;
+    if (c < cols && r < pad_rows) y[(long)c * ldy + r] = t[tx][i];
+  }
+}
+
+// y[r][:] = x[rowmap[r]][:] as bf16 (rows < rows_pad are zero beyond rows).
+template <class TI>
+__global__ void k_gather_rows(const TI *__restrict__ x, long ldx, const int32_t *__restrict__ rowmap,
+                              int rows, int rows_pad, int cols, unsigned short *__restrict__ y) {
+  const long n = (long)rows_pad * cols;
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x) {
+    const int r = (int)(i / cols), c = (int)(i % cols);
+    unsigned short b = 0;
+    if (r < rows) b = load_bf(x, (long)(rowmap ? rowmap[r] : r) * ldx + c);
+    y[i] = b;
+  }
+}
+
+struct LpWs {
+  size_t hb, ht, wt, wb, zt, stats, ztgt, lse, g, dz, dzt, total;
+  int Rp, Vp, ntiles;
+};
+
+LpWs lp_ws(int rows, int hidden, int vocab, seg_dtype dt) {
+  LpWs w{};
+  w.Rp = (rows + 31) / 32 * 32;
+  w.Vp = (vocab + 31) / 32 * 32;
+  w.ntiles = (vocab + BM - 1) / BM;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off = align_up(off + std::max<size_t>(bytes, 1));
+    return o;
+  };
+  const size_t Rp = w.Rp, Vp = w.Vp, H = hidden;
+  w.hb = take(Rp * H * 2);
+  w.ht = take(H * Rp * 2);
+  w.wt = take(H * Vp * 2);
+  w.wb = dt == SEG_F32 ? take((size_t)vocab * H * 2) : 0;
+  w.zt = take((size_t)vocab * Rp * 4);
+  w.stats = take((size_t)w.ntiles * std::max(rows, 1) * sizeof(float2));
+  w.ztgt = take(Rp * 4);
+  w.lse = take(Rp * 4);
+  w.g = take(Rp * 4);
+  w.dz = take(Rp * Vp * 2);
+  w.dzt = take(Vp * Rp * 2);
+  w.total = off;
+  return w;
+}
+
+dim3 grid2(long cols, long rows, int t = 64) {
+  return dim3((unsigned)((cols + t - 1) / t), (unsigned)((rows + t - 1) / t));
+}
+
+template <class TI, class TO>
+void logprob_impl(int rows, int H, int V, const TI *h, const int32_t *row_index, const TI *w,
+                  const int32_t *target, const float *old_logp, const float *adv,
+                  const int32_t *row_traj, int num_traj, const seg_loss_cfg &cfg, float *logp,
+                  float *loss_tok,
+                  uint8_t *clipped, float *loss_sum, void *dh, float *dw, char *base,
+                  const LpWs &L, hipStream_t st) {
+  const int Rp = L.Rp, Vp = L.Vp;
+  unsigned short *hb = reinterpret_cast<unsigned short *>(base + L.hb);
+  unsigned short *ht = reinterpret_cast<unsigned short *>(base + L.ht);
+  unsigned short *wt = reinterpret_cast<unsigned short *>(base + L.wt);
+  float *zt = reinterpret_cast<float *>(base + L.zt);
+  float2 *stats = reinterpret_cast<float2 *>(base + L.stats);
+  float *ztgt = reinterpret_cast<float *>(base + L.ztgt);
+  float *lse = reinterpret_cast<float *>(base + L.lse);
+  float *g = reinterpret_cast<float *>(base + L.g);
+  unsigned short *dz = reinterpret_cast<unsigned short *>(base + L.dz);
+  unsigned short *dzt = reinterpret_cast<unsigned short *>(base + L.dzt);
+
+  // gathered action rows (bf16)
+  {
+    const long n = (long)Rp * H;
+    k_gather_rows<TI><<<(int)std::min<long>(65536, (n + 255) / 256), 256, 0, st>>>(
+        h, H, row_index, rows, Rp, H, hb);
+    SEG_LAUNCH_CHECK();
+  }
+  const unsigned short *wb;
+  if constexpr (sizeof(TI) == 4) {
+    unsigned short *w2 = reinterpret_cast<unsigned short *>(base + L.wb);
+    const long n = (long)V * H;
+    k_gather_rows<TI><<<(int)std::min<long>(65536, (n + 255) / 256), 256, 0, st>>>(
+        w, H, nullptr, V, V, H, w2);
+    SEG_LAUNCH_CHECK();
+    wb = w2;
+  } else {
+    wb = reinterpret_cast<const unsigned short *>(w);
+  }
+  // 1. logits zT = s * W h^T with partial softmax stats; the target logit
+  //    stays NaN for a target outside [0, vocab)
+  SEG_HIP(hipMemsetAsync(ztgt, 0xff, sizeof(float) * Rp, st));
+  {
+    EpiLogits e{zt, Rp, stats, rows, target, ztgt, cfg.logit_scale};
+    dim3 grid((rows + BN - 1) / BN, (V + BM - 1) / BM);
+    k_gemm_nt<0, EpiLogits><<<grid, 256, 0, st>>>(wb, H, hb, H, V, rows, H, e);
+    SEG_LAUNCH_CHECK();
+  }
+  // 2. per-row loss
+  k_row_loss<<<rows, 256, 0, st>>>(stats, L.ntiles, rows, ztgt, old_logp, adv, row_traj, num_traj,
+                                   cfg, logp, loss_tok, clipped, lse, g);
+  SEG_LAUNCH_CHECK();
+  k_loss_sum<<<1, 256, 0, st>>>(loss_tok, rows, cfg.loss_scale, loss_sum);
+  SEG_LAUNCH_CHECK();
+  if (!cfg.want_grad) return;
+  // 3. dz in both orientations
+  k_dz<<<grid2(Rp, Vp), 256, 0, st>>>(zt, Rp, V, rows, Vp, Rp, lse, g, target, dz, dzt);
+  SEG_LAUNCH_CHECK();
+  // transposed operands: hT [H][Rp], Wt [H][Vp]
+  k_transpose2d<unsigned short><<<grid2(H, Rp), 256, 0, st>>>(hb, H, nullptr, Rp, H, Rp, ht, Rp);
+  SEG_LAUNCH_CHECK();
+  k_transpose2d<unsigned short><<<grid2(H, Vp), 256, 0, st>>>(wb, H, nullptr, V, H, Vp, wt, Vp);
+  SEG_LAUNCH_CHECK();
+  // 4. dH = s * dz W  (M = rows, N = H, K = Vp)
+  {
+    EpiStore<TO> e{static_cast<TO *>(dh), H, cfg.logit_scale};
+    dim3 grid((H + BN - 1) / BN, (rows + BM - 1) / BM);
+    k_gemm_nt<1, EpiStore<TO>><<<grid, 256, 0, st>>>(dz, Vp, wt, Vp, rows, H, Vp, e);
+    SEG_LAUNCH_CHECK();
+  }
+  //    dW = s * dz^T h  (M = V, N = H, K = Rp)
+  {
+    EpiStore<float> e{dw, H, cfg.logit_scale};
+    dim3 grid((H + BN - 1) / BN, (V + BM - 1) / BM);
+    k_gemm_nt<1, EpiStore<float>><<<grid, 256, 0, st>>>(dzt, Rp, ht, Rp, V, H, Rp, e);
+    SEG_LAUNCH_CHECK();
+  }
+}
+
+}  // namespace
+}  // namespace seg
+
+using namespace seg;
+
+extern "C" size_t seg_logprob_workspace_bytes(int32_t rows, int32_t hidden, int32_t vocab,
+                                              seg_dtype dt) {
+  if (rows < 0 || hidden < 1 || vocab < 1) return 0;
+  return lp_ws(rows, hidden, vocab, dt).total;
+}
+
+extern "C" seg_status seg_logprob_loss(int32_t rows, int32_t hidden, int32_t vocab, seg_dtype dt,
+                                       const void *h, const int32_t *row_index, const void *w,
+                                       const int32_t *target, const float *old_logp,
+                                       const float *adv, const int32_t *row_traj,
+                                       int32_t num_traj, const seg_loss_cfg *cfg, float *logp,
+                                       float *loss_tok, uint8_t *clipped, float *loss_sum,
+                                       void *dh, float *dw, void *ws, size_t ws_bytes,
+                                       hipStream_t stream) {
+  return guarded([&] {
+    SEG_CHECK(cfg != nullptr, SEG_ERR_ARG, "cfg is NULL");
+    SEG_CHECK(dt == SEG_BF16 || dt == SEG_F32, SEG_ERR_ARG, "unknown dtype %d", (int)dt);
+    SEG_CHECK(rows >= 0 && hidden >= 1 && vocab >= 1 && num_traj >= 0, SEG_ERR_ARG,
+              "bad sizes rows=%d hidden=%d vocab=%d num_traj=%d", rows, hidden, vocab, num_traj);
+    SEG_CHECK(hidden % 8 == 0, SEG_ERR_UNSUPPORTED, "hidden %d must be a multiple of 8", hidden);
+    SEG_CHECK(std::isfinite(cfg->eps_low) && std::isfinite(cfg->eps_high) &&
+                  std::isfinite(cfg->loss_scale) && std::isfinite(cfg->logit_scale) &&
+                  std::isfinite(cfg->dual_clip_c),
+              SEG_ERR_ARG, "non-finite loss setting");
+    SEG_CHECK(cfg->eps_low >= 0.f && cfg->eps_high >= 0.f, SEG_ERR_ARG, "negative clip range");
+    const LpWs L = lp_ws(rows, hidden, vocab, dt);
+    SEG_CHECK(ws_bytes >= L.total, SEG_ERR_WORKSPACE, "workspace of %zu bytes < required %zu",
+              ws_bytes, L.total);
+    SEG_CHECK(loss_sum != nullptr, SEG_ERR_ARG, "loss_sum is NULL");
+    if (rows == 0) {
+      SEG_HIP(hipMemsetAsync(loss_sum, 0, sizeof(float), stream));
+      if (cfg->want_grad && dw) SEG_HIP(hipMemsetAsync(dw, 0, sizeof(float) * (size_t)vocab * hidden, stream));
+      return;
+    }
+    SEG_CHECK(h && w && target && old_logp && adv && row_traj && logp && loss_tok && clipped && ws,
+              SEG_ERR_ARG, "a tensor pointer is NULL");
+    SEG_CHECK(num_traj >= 1, SEG_ERR_ARG, "num_traj must be >= 1 when rows > 0");
+    if (cfg->want_grad) SEG_CHECK(dh && dw, SEG_ERR_ARG, "dh/dw is NULL with want_grad");
+    char *base = static_cast<char *>(ws);
+    if (dt == SEG_F32)
+      logprob_impl<float, float>(rows, hidden, vocab, static_cast<const float *>(h), row_index,
+                                 static_cast<const float *>(w), target, old_logp, adv, row_traj,
+                                 num_traj, *cfg, logp, loss_tok, clipped, loss_sum, dh, dw, base, L, stream);
+    else
+      logprob_impl<unsigned short, unsigned short>(
+          rows, hidden, vocab, static_cast<const unsigned short *>(h), row_index,
+          static_cast<const unsigned short *>(w), target, old_logp, adv, row_traj, num_traj, *cfg, logp,
+          loss_tok, clipped, loss_sum, dh, dw, base, L, stream);
+  });
+}

@@ -179,7 +179,19 @@ def _mul32(x, c: int):
 
 
 def hash32(x):
-    """lowbias32 integer hash (C. Wellons), a bijection on 32-bit words."""
+    """lowbias32 integer hash (C. Wellons), a bijection on 32-bit words.
+
+    NumPy uint32 arrays use native wrap-around multiplication; other arrays
+    (torch int64) use the split multiply of :func:`_mul32`.  Both compute the
+    same function.
+    """
+    if isinstance(x, np.ndarray) and x.dtype == np.uint32:
+        x = x ^ (x >> np.uint32(16))
+        x *= np.uint32(0x7FEB352D)
+        x ^= x >> np.uint32(15)
+        x *= np.uint32(0x846CA68B)
+        x ^= x >> np.uint32(16)
+        return x
     x = x ^ (x >> 16)
     x = _mul32(x, 0x7FEB352D)
     x = x ^ (x >> 15)
@@ -203,6 +215,10 @@ def _key(seed: int, stream: int, word: int) -> int:
 def _words(idx, seed, stream, word):
     """32-bit random word for every element index in ``idx`` (int64 array)."""
     k = _key(seed, stream, word)
+    if isinstance(idx, np.ndarray):
+        lo = (idx & M32).astype(np.uint32)
+        hi = (idx >> 32).astype(np.uint32)
+        return hash32(hash32(lo ^ np.uint32(k)) ^ hi).astype(np.int64)
     lo = idx & M32
     hi = idx >> 32
     return hash32(hash32(lo ^ k) ^ hi)
@@ -230,18 +246,60 @@ def bf16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
     return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
 
 
-def normal_np(seed, stream, idx, std=1.0, dtype="bf16"):
-    """Values of elements ``idx`` of a normal tensor, as float64 host array.
-
-    The returned float64 values are exactly the values stored in the tensor's
-    dtype (bf16 or f32).
-    """
-    idx = np.asarray(idx, np.int64)
+def _normal_np_chunk(seed, stream, idx, std, dtype):
     z = _normal_from_words(_words(idx, seed, stream, 0), _words(idx, seed, stream, 1), np)
     v32 = (z * std).astype(np.float32)
     if dtype == "bf16":
         return bf16_bits_to_f64(bf16_round_np(v32))
     return v32.astype(np.float64)
+
+
+def normal_np(seed, stream, idx, std=1.0, dtype="bf16", chunk=1 << 18):
+    """Values of elements ``idx`` of a normal tensor, as float64 host array.
+
+    The returned float64 values are exactly the values stored in the tensor's
+    dtype (bf16 or f32).  Large requests are split over threads.
+    """
+    idx = np.asarray(idx, np.int64)
+    if idx.size <= chunk:
+        return _normal_np_chunk(seed, stream, idx, std, dtype)
+    flat = idx.reshape(-1)
+    out = np.empty(flat.size, np.float64)
+
+    def work(c0):
+        c1 = min(flat.size, c0 + chunk)
+        out[c0:c1] = _normal_np_chunk(seed, stream, flat[c0:c1], std, dtype)
+
+    _parallel(work, range(0, flat.size, chunk))
+    return out.reshape(idx.shape)
+
+
+def normal_rows_np(seed, stream, rows, width, std=1.0, dtype="bf16", chunk=1 << 18):
+    """Rows ``rows`` of a [*, width] normal tensor (element r*width + c)."""
+    rows = np.asarray(rows, np.int64).reshape(-1)
+    out = np.empty((rows.size, width), np.float64)
+    per = max(1, chunk // width)
+    cols = np.arange(width, dtype=np.int64)[None, :]
+
+    def work(r0):
+        r1 = min(rows.size, r0 + per)
+        idx = rows[r0:r1, None] * width + cols
+        out[r0:r1] = _normal_np_chunk(seed, stream, idx, std, dtype)
+
+    _parallel(work, range(0, rows.size, per))
+    return out
+
+
+def _parallel(fn, starts):
+    import concurrent.futures as cf
+    import os
+    starts = list(starts)
+    if len(starts) <= 1:
+        for s0 in starts:
+            fn(s0)
+        return
+    with cf.ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
+        list(ex.map(fn, starts))
 
 
 def uniform_int_np(seed, stream, idx, n):
@@ -291,9 +349,7 @@ class Inputs:
 
     # ---- host (float64 values exactly as stored) ----
     def _rows_np(self, name, rows, width, std, dtype):
-        rows = np.asarray(rows, np.int64)
-        idx = rows[:, None] * width + np.arange(width, dtype=np.int64)[None, :]
-        return normal_np(self.seed, STREAM[name], idx, std, dtype)
+        return normal_rows_np(self.seed, STREAM[name], rows, width, std, dtype)
 
     def q_np(self, rows):
         c = self.cfg

@@ -1,0 +1,161 @@
+"""Host-side checks of libseg's C ABI (no GPU): the library loads and exports
+every symbol of include/seg.h; seg_layout_query agrees with the oracle's
+segmentation; argument validation rejects bad input before any HIP call."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import layout as OL
+from paper_2607_11185_amd import _lib
+from paper_2607_11185_amd import seg as S
+from paper_2607_11185_amd import workload as WL
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _lib_or_skip():
+    if not os.path.exists(_lib.LIB_PATH):
+        pytest.skip("libseg.so not built")
+    return _lib.lib()
+
+
+def test_exports_every_declared_symbol():
+    L = _lib_or_skip()
+    with open(os.path.join(ROOT, "include", "seg.h")) as f:
+        hdr = f.read()
+    declared = set(re.findall(r"^\s*(?:seg_status|size_t|const char \*)\s*(seg_\w+)\s*\(", hdr, re.M))
+    assert declared == set(_lib.EXPORTS)
+    for name in declared:
+        assert hasattr(L, name), name
+
+
+def _sizes_oracle(sp, W, L, tile, cap=0, buf=0):
+    lay = OL.build(sp, W, L, tile, cap=cap, buffer_tokens=buf, with_tiles=False)
+    G = sum(-(-sg.length // tile) for sg in lay.segments)
+    Z = sum((n := -(-sg.length // tile)) * (n + 1) // 2 for sg in lay.segments)
+    return dict(num_segments=len(lay.segments), num_buffers=lay.num_buffers,
+                loss_rows=len(lay.loss_pred_row), num_qtiles=G,
+                packed_tokens=lay.packed_tokens,
+                traj_tokens=int(sp.canon_offsets()[-1]), tile_nnz_max=Z)
+
+
+@pytest.mark.parametrize("cfg", [WL.TINY, WL.SMALL, WL.SEVEN_B, WL.STEPWISE_7B, WL.LONG],
+                         ids=lambda c: c.name)
+def test_query_matches_oracle(cfg):
+    _lib_or_skip()
+    sp = WL.make_spans(cfg)
+    pr = S.Problem.from_spans(sp, cfg.window, cfg.seg_steps, cfg.max_seg_tokens, cfg.buffer_tokens)
+    got = S.seg_layout_query(pr).as_dict()
+    want = _sizes_oracle(sp, cfg.window, cfg.seg_steps, 128, cfg.max_seg_tokens, cfg.buffer_tokens)
+    for k, v in want.items():
+        assert got[k] == v, (k, got[k], v)
+    assert got["workspace_bytes"] > 0
+
+
+def test_query_random_and_edge():
+    _lib_or_skip()
+    rng = np.random.default_rng(0)
+    for it in range(30):
+        n = int(rng.integers(0, 4))
+        T = rng.integers(0, 7, size=n)
+        ns = int(T.sum())
+        text = rng.integers(0, 9, size=ns)
+        sp = WL.explicit_spans(T, rng.integers(1, 9, size=n), rng.integers(0, 9, size=ns), text,
+                               [int(rng.integers(0, t + 1)) for t in text])
+        W, L, tile = int(rng.integers(1, 4)), int(rng.integers(1, 4)), int(rng.choice([1, 4, 128]))
+        pr = S.Problem.from_spans(sp, W, L, 0, 0, tile)
+        got = S.seg_layout_query(pr).as_dict()
+        want = _sizes_oracle(sp, W, L, tile)
+        for k, v in want.items():
+            assert got[k] == v, (it, k, got[k], v)
+
+
+def _prob(**kw):
+    sp = WL.explicit_spans([3], [4], [5, 5, 5], [3, 3, 3], [1, 1, 1])
+    d = dict(window=2, seg_steps=2, max_seg_tokens=0, buffer_tokens=0, tile=128)
+    d.update(kw)
+    return S.Problem.from_spans(sp, **d)
+
+
+@pytest.mark.parametrize("kw,status,text", [
+    (dict(window=0), _lib.SEG_ERR_ARG, "window"),
+    (dict(seg_steps=0), _lib.SEG_ERR_ARG, "seg_steps"),
+    (dict(tile=0), _lib.SEG_ERR_ARG, "tile"),
+    (dict(max_seg_tokens=10), _lib.SEG_ERR_CAPACITY, "max_seg_tokens"),
+    (dict(buffer_tokens=12), _lib.SEG_ERR_CAPACITY, "buffer_tokens"),
+])
+def test_query_errors(kw, status, text):
+    _lib_or_skip()
+    with pytest.raises(_lib.SegError) as ei:
+        S.seg_layout_query(_prob(**kw))
+    assert ei.value.status == status and text in str(ei.value)
+
+
+def test_bad_spans():
+    _lib_or_skip()
+    bad = [
+        WL.explicit_spans([2], [0], [1, 1], [2, 2], [1, 1]),        # empty prompt
+        WL.explicit_spans([2], [3], [1, -1], [2, 2], [1, 1]),       # negative screenshot
+        WL.explicit_spans([2], [3], [1, 1], [2, 2], [3, 1]),        # action longer than text
+    ]
+    for sp in bad:
+        with pytest.raises(_lib.SegError) as ei:
+            S.seg_layout_query(S.Problem.from_spans(sp, 1, 1))
+        assert ei.value.status == _lib.SEG_ERR_ARG
+    pr = _prob()
+    pr.step_offsets = np.array([1, 3], np.int32)
+    with pytest.raises(_lib.SegError):
+        S.seg_layout_query(pr)
+
+
+def test_null_problem_and_last_error():
+    L = _lib_or_skip()
+    sz = _lib.SegSizes()
+    assert L.seg_layout_query(None, ctypes.byref(sz)) == _lib.SEG_ERR_ARG
+    assert b"NULL" in L.seg_last_error()
+    assert L.seg_layout_query(ctypes.byref(_prob().c()), ctypes.byref(sz)) == _lib.SEG_OK
+    assert L.seg_last_error() == b""
+
+
+def test_build_and_compute_reject_bad_args_before_any_launch():
+    L = _lib_or_skip()
+    pr = _prob()
+    sz = S.seg_layout_query(pr)
+    lay = _lib.SegLayout()
+    # workspace too small
+    st = L.seg_build_layout(ctypes.byref(pr.c()), ctypes.byref(sz), ctypes.byref(lay), None, 0, None)
+    assert st == _lib.SEG_ERR_WORKSPACE
+    # sizes that do not belong to the problem
+    sz2 = _lib.SegSizes.from_buffer_copy(sz)
+    sz2.loss_rows += 1
+    st = L.seg_build_layout(ctypes.byref(pr.c()), ctypes.byref(sz2), ctypes.byref(lay), None,
+                            1 << 30, None)
+    assert st == _lib.SEG_ERR_ARG
+    # attention: unsupported head_dim / ratio / tile
+    lay.tile, lay.window = 128, 2
+    for hq, hkv, d, want in ((4, 1, 96, _lib.SEG_ERR_UNSUPPORTED), (4, 3, 64, _lib.SEG_ERR_UNSUPPORTED)):
+        st = L.seg_attn_fwd(ctypes.byref(lay), ctypes.byref(sz), 0, hq, hkv, d, 0.1, None, None,
+                            None, None, None, None, 1 << 40, None)
+        assert st == want, (hq, hkv, d, st)
+    lay.tile = 64
+    st = L.seg_attn_fwd(ctypes.byref(lay), ctypes.byref(sz), 0, 4, 1, 64, 0.1, None, None, None,
+                        None, None, None, 1 << 40, None)
+    assert st == _lib.SEG_ERR_UNSUPPORTED
+    lay.tile = 128
+    st = L.seg_attn_bwd(ctypes.byref(lay), ctypes.byref(sz), 0, 4, 1, 64, 0.1, None, None, None,
+                        None, None, None, None, None, None, None, 0, None)
+    assert st == _lib.SEG_ERR_WORKSPACE
+    # log-prob: hidden not a multiple of 8, workspace, null tensors
+    cfg = S.LossCfg().c()
+    args = [None] * 7
+    st = L.seg_logprob_loss(4, 12, 10, 0, *args, 1, ctypes.byref(cfg), *([None] * 6), None, 0, None)
+    assert st == _lib.SEG_ERR_UNSUPPORTED
+    st = L.seg_logprob_loss(4, 16, 10, 0, *args, 1, ctypes.byref(cfg), *([None] * 6), None, 0, None)
+    assert st == _lib.SEG_ERR_WORKSPACE
+    need = L.seg_logprob_workspace_bytes(4, 16, 10, 0)
+    st = L.seg_logprob_loss(4, 16, 10, 0, *args, 1, ctypes.byref(cfg), *([None] * 6), None, need,
+                            None)
+    assert st == _lib.SEG_ERR_ARG

@@ -1,0 +1,118 @@
+"""GPU layout (seg_build_layout through the C ABI) bit-exact against the oracle:
+tokens, loss rows, segment records, tile map (CSR and transposed CSR) and the
+exact visible-pair counts."""
+import json
+import os
+
+import numpy as np
+import pytest
+
+from oracle import layout as OL
+from paper_2607_11185_amd import seg as S
+from paper_2607_11185_amd import workload as WL
+from tests.gpu_helpers import say
+
+pytestmark = pytest.mark.gpu
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _gpu(sp, W, L, tile, cap=0, buf=0):
+    say(f"  layout W={W} L={L} tile={tile} cap={cap} buf={buf} traj={sp.num_traj}")
+    pr = S.Problem.from_spans(sp, W, L, cap, buf, tile)
+    return S.seg_build_layout(pr, device="cuda").host()
+
+
+def _check_all(got, ref):
+    for f in ("tok_src", "tok_meta", "loss_pred_row", "loss_tgt_src", "loss_traj", "tile_seg",
+              "qt_ptr", "qt_col", "qt_cls", "kt_ptr", "kt_row", "kt_cls", "seg_pairs"):
+        assert np.array_equal(got[f].astype(np.int64), getattr(ref, f).astype(np.int64)), f
+    assert np.array_equal(got["seg_info"].astype(np.int64), ref.seg_info), "seg_info"
+    assert int(got["tile_nnz"][0]) == len(ref.qt_col)
+    # work order: tiles by decreasing row length, ties by index
+    lens = np.diff(ref.qt_ptr)
+    want = sorted(range(len(lens)), key=lambda g: (-min(lens[g], 8191), g))
+    assert got["work_order"].tolist() == want
+
+
+@pytest.mark.parametrize("name", ["appA_example_a.json", "appA_example_b.json"])
+def test_hand_worked(name):
+    with open(os.path.join(GOLD, name)) as f:
+        d = json.load(f)
+    s = d["spans"]
+    sp = WL.explicit_spans(s["steps"], s["prompt"], s["img"], s["text"], s["action"])
+    got = _gpu(sp, d["window"], d["seg_steps"], d["tile"])
+    _check_all(got, OL.build(sp, d["window"], d["seg_steps"], d["tile"]))
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_spans(seed):
+    rng = np.random.default_rng(100 + seed)
+    n = int(rng.integers(1, 5))
+    T = rng.integers(0, 9, size=n)
+    ns = int(T.sum())
+    text = rng.integers(0, 40, size=ns)
+    sp = WL.explicit_spans(T, rng.integers(1, 50, size=n), rng.integers(0, 60, size=ns), text,
+                           [int(rng.integers(0, t + 1)) for t in text])
+    W, L = int(rng.integers(1, 5)), int(rng.integers(1, 5))
+    tile = int(rng.choice([1, 3, 4, 16, 128]))
+    buf = int(rng.choice([0, 0, 400]))
+    try:
+        ref = OL.build(sp, W, L, tile, buffer_tokens=buf)
+    except OL.CapacityError:
+        ref = OL.build(sp, W, L, tile)
+        buf = 0
+    _check_all(_gpu(sp, W, L, tile, buf=buf), ref)
+
+
+@pytest.mark.parametrize("cfg", [WL.TINY, WL.SMALL], ids=lambda c: c.name)
+def test_configs_full(cfg):
+    sp = WL.make_spans(cfg)
+    got = _gpu(sp, cfg.window, cfg.seg_steps, 128, cfg.max_seg_tokens, cfg.buffer_tokens)
+    _check_all(got, OL.build(sp, cfg.window, cfg.seg_steps, 128, cfg.max_seg_tokens,
+                             cfg.buffer_tokens))
+
+
+@pytest.mark.parametrize("cfg", [WL.SEVEN_B, WL.STEPWISE_7B, WL.LONG], ids=lambda c: c.name)
+def test_configs_large_sampled(cfg):
+    """Full-size layouts: every token, loss row and segment record exact; the
+    tile map and pair counts of sampled segments exact."""
+    sp = WL.make_spans(cfg)
+    got = _gpu(sp, cfg.window, cfg.seg_steps, 128, cfg.max_seg_tokens, cfg.buffer_tokens)
+    ref = OL.build(sp, cfg.window, cfg.seg_steps, 128, cfg.max_seg_tokens, cfg.buffer_tokens,
+                   with_tiles=False)
+    for f in ("tok_src", "tok_meta", "loss_pred_row", "loss_tgt_src", "loss_traj"):
+        assert np.array_equal(got[f].astype(np.int64), getattr(ref, f).astype(np.int64)), f
+    assert np.array_equal(got["seg_info"].astype(np.int64), ref.seg_info)
+    S_ = len(ref.segments)
+    lens = [sg.length for sg in ref.segments]
+    picks = sorted({0, S_ // 2, S_ - 1, int(np.argmax(lens))})
+    for si in picks:
+        sg = ref.segments[si]
+        say(f"  tiles of segment {si} ({sg.length} tokens)")
+        cls, pairs = OL.segment_tiles(sg, cfg.window, 128)
+        assert int(got["seg_pairs"][si]) == pairs
+        base = int(ref.seg_info[si][5])
+        nt = cls.shape[0]
+        for i in range(nt):
+            g = base + i
+            e0, e1 = got["qt_ptr"][g], got["qt_ptr"][g + 1]
+            cols = got["qt_col"][e0:e1] - base
+            want = np.nonzero(cls[i])[0]
+            assert np.array_equal(cols, want), (si, i)
+            assert np.array_equal(got["qt_cls"][e0:e1], cls[i][want]), (si, i)
+        for j in range(nt):
+            g = base + j
+            e0, e1 = got["kt_ptr"][g], got["kt_ptr"][g + 1]
+            rows = got["kt_row"][e0:e1] - base
+            want = np.nonzero(cls[:, j])[0]
+            assert np.array_equal(rows, want), (si, j)
+            assert np.array_equal(got["kt_cls"][e0:e1], cls[want, j]), (si, j)
+    # skipped tiles exist: expired screenshots are never visited
+    total_lower = sum((n := -(-l // 128)) * (n + 1) // 2 for l in lens)
+    assert int(got["tile_nnz"][0]) < total_lower
+
+
+def test_empty_batch():
+    sp = WL.explicit_spans([0, 0], [3, 3], [], [], [])
+    got = _gpu(sp, 2, 2, 128)
+    assert got["tok_src"].size == 0 and int(got["qt_ptr"][0]) == 0

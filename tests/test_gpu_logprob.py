@@ -1,0 +1,130 @@
+"""GPU fused log-prob + clipped-ratio loss (seg_logprob_loss through the C ABI)
+against the float64 oracle (Eq. loss): full parity on the tiny and small
+heads, the 7B-class head at full vocabulary and hidden size on a reduced row
+count, and the full 7B-class row count on sampled rows plus the identity
+sum_v dW[v] = 0 (each dz row sums to zero)."""
+import numpy as np
+import pytest
+
+from oracle import layout as OL
+from oracle import loss as OLS
+from paper_2607_11185_amd import seg as S
+from paper_2607_11185_amd import workload as WL
+from tests.gpu_helpers import TOL, GpuRun, as_model_dtype, rel, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _inputs(run, rows_idx=None):
+    """Oracle-side inputs of the loss rows (optionally a subset)."""
+    c = run.cfg
+    hst = run.host
+    R = len(hst["loss_pred_row"])
+    sel = np.arange(R) if rows_idx is None else np.asarray(rows_idx)
+    pred_canon = hst["tok_src"][hst["loss_pred_row"][sel]]
+    h = as_model_dtype(run.inp.h_np(pred_canon), c)
+    tgt = run.inp.tgt_np(hst["loss_tgt_src"][sel])
+    adv = run.inp.adv_np().astype(np.float32)
+    return sel, h, tgt, adv[hst["loss_traj"][sel]].astype(np.float64)
+
+
+def _run_gpu(run, old_logp, cfg_loss, w=None):
+    import torch
+    dev = run.dev
+    hst = run.host
+    src = torch.from_numpy(hst["tok_src"].astype(np.int64)).to(dev)
+    h = run.inp.h_torch(dev)[src].contiguous()
+    w = run.inp.w_torch(dev) if w is None else w
+    tgt = torch.from_numpy(run.inp.tgt_np(hst["loss_tgt_src"])).to(dev)
+    adv = torch.from_numpy(run.inp.adv_np().astype(np.float32)).to(dev)
+    out = S.seg_logprob_loss(h, run.lay.loss_pred_row, w, tgt,
+                             torch.from_numpy(old_logp.astype(np.float32)).to(dev), adv,
+                             run.lay.loss_traj, cfg_loss)
+    torch.cuda.synchronize()
+    return out
+
+
+def _full_case(cfg, dual=0.0, want_grad=True):
+    run = GpuRun(cfg)
+    R = run.lay.sizes.loss_rows
+    sel, h, tgt, adv = _inputs(run)
+    w = as_model_dtype(run.inp.w_np(), cfg)
+    logp_cur, _, _ = OLS.logprob(h, w, tgt)
+    old = (logp_cur + run.inp.old_noise_np(run.host["loss_tgt_src"])).astype(np.float32)
+    lc = S.LossCfg(cfg.eps_low, cfg.eps_high, dual, 1.0 / R, 1.0, want_grad)
+    ref = OLS.loss_and_grads(h, w, tgt, old.astype(np.float64), adv, cfg.eps_low, cfg.eps_high,
+                             loss_scale=1.0 / R, dual_clip_c=dual, want_grad=want_grad)
+    out = _run_gpu(run, old, lc)
+    return run, ref, out, old
+
+
+@pytest.mark.parametrize("cfg,dual", [(WL.TINY, 0.0), (WL.SMALL, 0.0), (WL.SMALL, 1.15)],
+                         ids=["tiny", "small", "small_dualclip"])
+def test_full_parity(cfg, dual):
+    say(f"logprob {cfg.name} dual={dual}")
+    run, ref, out, old = _full_case(cfg, dual)
+    R = run.lay.sizes.loss_rows
+    logp = out["logp"][:R].cpu().numpy()
+    assert np.abs(logp - ref["logp"]).max() < 2e-2 * max(1.0, np.abs(ref["logp"]).max())
+    assert rel(logp, ref["logp"]) < TOL
+    assert rel(out["loss_tok"][:R].cpu().numpy(), ref["loss_tok"]) < TOL
+    # clip decisions agree except where the ratio sits next to a clip bound
+    rho = np.exp(ref["logp"] - old)
+    near = (np.abs(np.log(rho) - np.log(1 - cfg.eps_low)) < 1e-2) | \
+           (np.abs(np.log(rho) - np.log(1 + cfg.eps_high)) < 1e-2)
+    if dual:
+        near |= np.abs(np.log(rho) - np.log(dual)) < 1e-2
+    cl = out["clipped"][:R].cpu().numpy().astype(bool)
+    assert (cl == ref["clipped"])[~near].all()
+    assert ref["clipped"].any() and (~ref["clipped"]).any()
+    assert abs(float(out["loss_sum"][0]) - ref["loss_sum"]) < TOL * max(1e-3, abs(ref["loss_sum"]))
+    e_dh = rel(out["dh"][:R].float().cpu().numpy(), ref["dh"])
+    e_dw = rel(out["dw"].cpu().numpy(), ref["dw"])
+    say(f"  dh {e_dh:.2e} dw {e_dw:.2e}")
+    assert e_dh < TOL and e_dw < TOL
+
+
+def test_forward_only():
+    run, ref, out, _ = _full_case(WL.TINY, want_grad=False)
+    R = run.lay.sizes.loss_rows
+    assert rel(out["logp"][:R].cpu().numpy(), ref["logp"]) < TOL
+
+
+def test_seven_b_head_reduced_rows():
+    """Full vocabulary and hidden size of the 7B-class head, 96 rows."""
+    cfg = WL.SEVEN_B.with_(num_traj=1, steps=(3, 3))
+    say("logprob 7B head, one trajectory of 3 turns")
+    run, ref, out, _ = _full_case(cfg)
+    R = run.lay.sizes.loss_rows
+    assert rel(out["logp"][:R].cpu().numpy(), ref["logp"]) < TOL
+    assert rel(out["dh"][:R].float().cpu().numpy(), ref["dh"]) < TOL
+    assert rel(out["dw"].cpu().numpy(), ref["dw"]) < TOL
+
+
+def test_seven_b_full_rows_sampled():
+    """All 7,680 action rows of the 7B-class batch; sampled rows against the
+    oracle and the dW column-sum identity."""
+    import torch
+    cfg = WL.SEVEN_B
+    say("logprob 7B full rows")
+    run = GpuRun(cfg)
+    R = run.lay.sizes.loss_rows
+    rng = np.random.default_rng(0)
+    sel = np.unique(rng.integers(0, R, 12))
+    _, h, tgt, adv = _inputs(run, sel)
+    w = run.inp.w_np()
+    logp_cur, _, _ = OLS.logprob(h, w, tgt)
+    # rollout log-probs: oracle value + noise on the sampled rows, a fixed
+    # offset elsewhere (any value is a valid input there)
+    old = np.full(R, -np.log(cfg.vocab), np.float64)
+    old += run.inp.old_noise_np(run.host["loss_tgt_src"])
+    old[sel] = logp_cur + run.inp.old_noise_np(run.host["loss_tgt_src"][sel])
+    lc = S.LossCfg(cfg.eps_low, cfg.eps_high, 0.0, 1.0 / R, 1.0, True)
+    out = _run_gpu(run, old, lc)
+    ref = OLS.loss_and_grads(h, w, tgt, old[sel].astype(np.float32).astype(np.float64), adv,
+                             cfg.eps_low, cfg.eps_high, loss_scale=1.0 / R)
+    assert rel(out["logp"][sel].cpu().numpy(), ref["logp"]) < TOL
+    assert rel(out["loss_tok"][sel].cpu().numpy(), ref["loss_tok"]) < TOL
+    assert rel(out["dh"][torch.from_numpy(sel).cuda()].float().cpu().numpy(), ref["dh"]) < TOL
+    dw = out["dw"].double()
+    assert float(dw.sum(0).norm()) < TOL * float(dw.norm())

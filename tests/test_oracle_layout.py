@@ -123,6 +123,15 @@ def test_invariants_random(seed):
     assert lay.seg_pairs.sum() == sum(int(OL.visibility(sg, W).sum()) for sg in lay.segments)
 
 
+def test_visibility_rows_are_rows_of_the_mask():
+    rng = np.random.default_rng(5)
+    sp = _random_spans(rng, 2, 6)
+    lay = OL.build(sp, 2, 3, 4)
+    for sg in lay.segments:
+        rows = np.arange(sg.length)[::2]
+        assert (OL.visibility_rows(sg, 2, rows) == OL.visibility(sg, 2)[rows]).all()
+
+
 def test_tile_one_is_the_mask():
     rng = np.random.default_rng(11)
     sp = _random_spans(rng, 2, 5)
