@@ -1,0 +1,287 @@
+#!/usr/bin/env python3
+"""Benchmark of the segmented training hot path on one MI355X.
+
+One step = the whole hot path over one batch: segmentation and packed layout
+with its tile map (seg_layout_query + seg_build_layout), masked GQA attention
+forward, the fused action-token log-prob / clipped-ratio loss with its
+gradients, and attention backward.  Inputs (packed q/k/v/dO, hidden states,
+projection, targets, advantages, rollout log-probs) are resident in HBM before
+the timed region.  The step-wise decomposition (every turn its own sample,
+same kernels) runs the same step for the comparison.
+
+Prints one JSON line.  `value` is the algorithmic attention forward+backward
+throughput (12*d FLOP per visible (query, key) pair per query head) over the
+device time of the two attention calls; `ms_per_step` and the trajectory
+token rates cover the whole step.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "segmented attn fwd+bwd TFLOP/s + trajectory tokens/sec vs step-wise (1 GPU)"
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+# algorithmic FLOP per visible pair per query head and per head-dim element
+KERNEL_FLOP_PER_PAIR_D = {"attn_fwd": 4, "attn_bwd_dkdv": 6, "attn_bwd_dq": 2}
+KERNELS = ["layout", "attn_prep", "attn_fwd", "attn_delta", "attn_bwd_dkdv", "attn_bwd_dq",
+           "lp_prep", "logits", "row_loss", "dz", "dh", "dw"]
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+class PathRun:
+    """All device buffers of one path (segmented or step-wise) and its step."""
+
+    def __init__(self, cfg, dev):
+        import numpy as np
+        import torch
+
+        from paper_2607_11185_amd import seg as S
+        from paper_2607_11185_amd import workload as WL
+        self.S, self.cfg, self.dev = S, cfg, dev
+        inp = WL.Inputs(cfg)
+        self.problem = S.Problem.from_spans(inp.spans, cfg.window, cfg.seg_steps,
+                                            cfg.max_seg_tokens, cfg.buffer_tokens, 128)
+        self.sizes = S.seg_layout_query(self.problem)
+        self.lay = S.seg_build_layout(self.problem, self.sizes, dev)
+        host = self.lay.host()
+        self.pairs = int(host["seg_pairs"].sum())
+        sz = self.sizes
+        P, R = sz.packed_tokens, sz.loss_rows
+        log(f"[{cfg.name}] segments={sz.num_segments} packed={P} traj_tokens={sz.traj_tokens} "
+            f"loss_rows={R} tiles={sz.num_qtiles} nnz={int(host['tile_nnz'][0])} pairs/head={self.pairs}")
+        src = torch.from_numpy(host["tok_src"].astype(np.int64)).to(dev)
+        self.q = inp.q_torch(dev)[src].contiguous()
+        self.k = inp.k_torch(dev)[src].contiguous()
+        self.v = inp.v_torch(dev)[src].contiguous()
+        torch.cuda.empty_cache()
+        self.dout = inp.dout_torch(P, dev)
+        self.h = inp.h_torch(dev)[src].contiguous()
+        torch.cuda.empty_cache()
+        self.w = inp.w_torch(dev)
+        self.tgt = torch.from_numpy(inp.tgt_np(host["loss_tgt_src"])).to(dev)
+        self.adv = torch.from_numpy(inp.adv_np().astype(np.float32)).to(dev)
+        self.scale = 1.0 / math.sqrt(cfg.head_dim)
+        dt = 0
+        self.ws_fwd = S.attn_workspace(self.lay, dt, cfg.hq, cfg.hkv, cfg.head_dim, False)
+        self.ws_bwd = S.attn_workspace(self.lay, dt, cfg.hq, cfg.hkv, cfg.head_dim, True)
+        self.ws_lp = S.logprob_workspace(R, cfg.hidden, cfg.vocab, dt, dev)
+        self.o = torch.empty_like(self.q)
+        self.lse = torch.empty((cfg.hq, P), dtype=torch.float32, device=dev)
+        self.dq = torch.empty_like(self.q)
+        self.dk = torch.empty_like(self.k)
+        self.dv = torch.empty_like(self.v)
+        self.lp_out = {
+            "logp": torch.empty(R, dtype=torch.float32, device=dev),
+            "loss_tok": torch.empty(R, dtype=torch.float32, device=dev),
+            "clipped": torch.empty(R, dtype=torch.uint8, device=dev),
+            "loss_sum": torch.empty(1, dtype=torch.float32, device=dev),
+            "dh": torch.empty((R, cfg.hidden), dtype=torch.bfloat16, device=dev),
+            "dw": torch.empty((cfg.vocab, cfg.hidden), dtype=torch.float32, device=dev),
+        }
+        # rollout log-probs: the current policy's log-probs (one forward-only
+        # call before timing) plus N(0, 0.1) noise, as the workload specifies
+        fwd_only = S.LossCfg(cfg.eps_low, cfg.eps_high, 0.0, 1.0 / R, 1.0, False)
+        zero = torch.zeros(R, dtype=torch.float32, device=dev)
+        S.seg_logprob_loss(self.h, self.lay.loss_pred_row, self.w, self.tgt, zero, self.adv,
+                           self.lay.loss_traj, fwd_only, out=dict(self.lp_out, dh=None, dw=None),
+                           ws=self.ws_lp)
+        noise = torch.from_numpy(inp.old_noise_np(host["loss_tgt_src"]).astype(np.float32)).to(dev)
+        self.old = (self.lp_out["logp"] + noise).contiguous()
+        self.loss_cfg = S.LossCfg(cfg.eps_low, cfg.eps_high, 0.0, 1.0 / R, 1.0, True)
+        torch.cuda.synchronize()
+
+    def step(self, ev=None):
+        S = self.S
+        rec = (lambda name: ev[name].record()) if ev is not None else (lambda name: None)
+        rec("t0")
+        sz = S.seg_layout_query(self.problem)
+        S.seg_build_layout(self.problem, sz, self.dev, out=self.lay)
+        rec("t1")
+        S.seg_attn_fwd(self.lay, self.q, self.k, self.v, self.scale, o=self.o, lse=self.lse,
+                       ws=self.ws_fwd)
+        rec("t2")
+        S.seg_logprob_loss(self.h, self.lay.loss_pred_row, self.w, self.tgt, self.old, self.adv,
+                           self.lay.loss_traj, self.loss_cfg, out=self.lp_out, ws=self.ws_lp)
+        rec("t3")
+        S.seg_attn_bwd(self.lay, self.q, self.k, self.v, self.o, self.lse, self.dout, self.scale,
+                       dq=self.dq, dk=self.dk, dv=self.dv, ws=self.ws_bwd)
+        rec("t4")
+
+    def attn_flop(self):
+        c = self.cfg
+        return 12.0 * c.head_dim * self.pairs * c.hq
+
+    def free(self):
+        for k in list(self.__dict__):
+            if k not in ("cfg", "sizes", "pairs", "S", "dev", "problem"):
+                delattr(self, k)
+
+
+def time_path(run, steps, warmup, profile=True):
+    import torch
+
+    from paper_2607_11185_amd import _lib
+    L = _lib.lib()
+    for _ in range(warmup):
+        run.step()
+    torch.cuda.synchronize()
+    names = ["t0", "t1", "t2", "t3", "t4"]
+    evs = [{n: torch.cuda.Event(enable_timing=True) for n in names} for _ in range(steps)]
+    L.seg_profile_reset()
+    L.seg_profile_enable(1 if profile else 0)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    for i in range(steps):
+        run.step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    L.seg_profile_enable(0)
+    ph = {"layout": 0.0, "attn_fwd": 0.0, "logprob_loss": 0.0, "attn_bwd": 0.0, "step": 0.0}
+    for e in evs:
+        ph["layout"] += e["t0"].elapsed_time(e["t1"])
+        ph["attn_fwd"] += e["t1"].elapsed_time(e["t2"])
+        ph["logprob_loss"] += e["t2"].elapsed_time(e["t3"])
+        ph["attn_bwd"] += e["t3"].elapsed_time(e["t4"])
+        ph["step"] += e["t0"].elapsed_time(e["t4"])
+    ph = {k: v / steps for k, v in ph.items()}
+    kern = {}
+    import ctypes
+    for name in KERNELS:
+        tot = ctypes.c_double()
+        n = ctypes.c_int64()
+        _lib.check(L.seg_profile_read(name.encode(), ctypes.byref(tot), ctypes.byref(n)))
+        if n.value:
+            kern[name] = {"ms_per_step": tot.value / steps, "launches_per_step": n.value / steps}
+    L.seg_profile_reset()
+    return ph, kern, wall / steps * 1e3
+
+
+def cpu_baseline(cfg, budget_note):
+    """The float64 oracle on a bounded sample: attention forward and backward
+    of the first segment for one query head and its kv head."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import attention as OA
+    from oracle import layout as OL
+    from paper_2607_11185_amd import workload as WL
+    inp = WL.Inputs(cfg)
+    ref = OL.build(inp.spans, cfg.window, cfg.seg_steps, 128, cfg.max_seg_tokens,
+                   cfg.buffer_tokens, with_tiles=False)
+    sg = ref.segments[0]
+    q = inp.q_np(sg.canon)[:, :1]
+    k = inp.k_np(sg.canon)[:, :1]
+    v = inp.v_np(sg.canon)[:, :1]
+    dout = inp.dout_np(np.arange(sg.start, sg.start + sg.length))[:, :1]
+    scale = 1.0 / math.sqrt(cfg.head_dim)
+    t0 = time.perf_counter()
+    mask = OL.visibility(sg, cfg.window)
+    OA.forward(q, k, v, mask, scale)
+    OA.backward(q, k, v, mask, scale, dout)
+    dt = time.perf_counter() - t0
+    pairs = int(mask.sum())
+    flop = 12.0 * cfg.head_dim * pairs
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    return {"value": flop / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": (f"attention fwd+bwd of segment 0 ({sg.length} tokens, {pairs} visible "
+                       f"pairs), 1 query head / 1 kv head, d={cfg.head_dim}, float64 NumPy; "
+                       f"{dt:.1f} s"),
+            "seconds": dt}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", default="7b", help="workload name (7b, small, long, tiny)")
+    ap.add_argument("--no-stepwise", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the segmented path runs on a single MI355X and this "
+              "build has no multi-GPU code (run with --gpus 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2607_11185_amd import workload as WL
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    cfg = WL.CONFIGS[args.config]
+
+    seg = PathRun(cfg, dev)
+    ph, kern, wall_ms = time_path(seg, args.steps, args.warmup)
+    attn_ms = ph["attn_fwd"] + ph["attn_bwd"]
+    value = seg.attn_flop() / (attn_ms * 1e-3) / 1e12
+    traj_tokens = seg.sizes.traj_tokens
+    # dominant attention kernel and its roofline from the live event timing
+    dom = max(KERNEL_FLOP_PER_PAIR_D, key=lambda n: kern.get(n, {}).get("ms_per_step", 0.0))
+    dom_ms = kern[dom]["ms_per_step"] / kern[dom]["launches_per_step"]
+    dom_flop = KERNEL_FLOP_PER_PAIR_D[dom] * cfg.head_dim * seg.pairs * cfg.hq
+    achieved = dom_flop / (dom_ms * 1e-3) / 1e12
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ph["step"], 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded counter-based generator; no datasets or weights)",
+        "config": {"workload": f"{cfg.name}-class segmented VCS step: {cfg.num_traj} trajectories "
+                               f"x {cfg.steps[0]}-{cfg.steps[1]} turns, prompt {cfg.prompt_len}, "
+                               f"{cfg.img_len} screenshot tokens, text {cfg.text_len[0]}-"
+                               f"{cfg.text_len[1]} (last {cfg.action_len} trained), W={cfg.window}, "
+                               f"L={cfg.seg_steps}, {cfg.hq}q/{cfg.hkv}kv heads, d={cfg.head_dim}, "
+                               f"hidden {cfg.hidden}, vocab {cfg.vocab}",
+                   "packed_tokens": seg.sizes.packed_tokens, "traj_tokens": traj_tokens,
+                   "segments": seg.sizes.num_segments, "visible_pairs_per_head": seg.pairs},
+        "traj_tokens_per_s": round(traj_tokens / (ph["step"] * 1e-3), 1),
+        "attn_ms": round(attn_ms, 3),
+        "phases_ms": {k: round(v, 3) for k, v in ph.items()},
+        "kernels_ms": {k: round(v["ms_per_step"], 3) for k, v in kern.items()},
+        "wall_ms_per_step": round(wall_ms, 3),
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "flop_per_launch": dom_flop, "ms_per_launch": round(dom_ms, 3)},
+    }
+    seg.free()
+    del seg
+    torch.cuda.empty_cache()
+
+    if not args.no_stepwise:
+        sw_cfg = cfg.with_(name=cfg.name + "_stepwise", seg_steps=1)
+        sw = PathRun(sw_cfg, dev)
+        ph2, kern2, _ = time_path(sw, args.steps, args.warmup)
+        attn2 = ph2["attn_fwd"] + ph2["attn_bwd"]
+        out["stepwise"] = {
+            "ms_per_step": round(ph2["step"], 3),
+            "traj_tokens_per_s": round(traj_tokens / (ph2["step"] * 1e-3), 1),
+            "attn_tflops": round(sw.attn_flop() / (attn2 * 1e-3) / 1e12, 2),
+            "attn_ms": round(attn2, 3), "packed_tokens": sw.sizes.packed_tokens,
+            "segments": sw.sizes.num_segments, "visible_pairs_per_head": sw.pairs,
+            "phases_ms": {k: round(v, 3) for k, v in ph2.items()},
+        }
+        out["speedup_vs_stepwise"] = round(ph2["step"] / ph["step"], 3)
+        sw.free()
+        del sw
+        torch.cuda.empty_cache()
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, "")
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -221,6 +221,19 @@ seg_status seg_logprob_loss(int32_t rows, int32_t hidden, int32_t vocab, seg_dty
                             void *dh, float *dw, void *ws, size_t ws_bytes,
                             hipStream_t stream);
 
+/*
+ * Kernel timing.  While enabled, every kernel the library launches is
+ * bracketed by HIP events recorded on its launch stream.  seg_profile_read sums
+ * the device time of all recorded launches of one kernel (names: "layout",
+ * "attn_prep", "attn_fwd", "attn_delta", "attn_bwd_dkdv", "attn_bwd_dq",
+ * "logits", "row_loss", "dz", "lp_prep", "dh", "dw"), waiting for them to
+ * finish; seg_profile_reset forgets the records.  Timing adds two event
+ * records per launch and is off by default.
+ */
+void seg_profile_enable(int32_t on);
+void seg_profile_reset(void);
+seg_status seg_profile_read(const char *name, double *total_ms, int64_t *launches);
+
 /* Message of the last non-OK status on the calling thread ("" if none). */
 const char *seg_last_error(void);
 

@@ -21,7 +21,8 @@ SEG_BF16, SEG_F32 = 0, 1
 
 # every symbol include/seg.h declares
 EXPORTS = ["seg_layout_query", "seg_build_layout", "seg_attn_workspace_bytes", "seg_attn_fwd",
-           "seg_attn_bwd", "seg_logprob_workspace_bytes", "seg_logprob_loss", "seg_last_error"]
+           "seg_attn_bwd", "seg_logprob_workspace_bytes", "seg_logprob_loss", "seg_profile_enable",
+           "seg_profile_reset", "seg_profile_read", "seg_last_error"]
 
 P32 = ctypes.POINTER(ctypes.c_int32)
 VP = ctypes.c_void_p
@@ -104,6 +105,13 @@ def lib() -> ctypes.CDLL:
                                        VP, VP, VP, VP, VP, VP, VP, ctypes.c_int32,
                                        ctypes.POINTER(SegLossCfg), VP, VP, VP, VP, VP, VP, VP,
                                        ctypes.c_size_t, VP]
+        L.seg_profile_enable.restype = None
+        L.seg_profile_enable.argtypes = [ctypes.c_int32]
+        L.seg_profile_reset.restype = None
+        L.seg_profile_reset.argtypes = []
+        L.seg_profile_read.restype = ctypes.c_int
+        L.seg_profile_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double),
+                                       ctypes.POINTER(ctypes.c_int64)]
         _lib = L
     return _lib
 

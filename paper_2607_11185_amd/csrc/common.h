@@ -58,6 +58,22 @@ inline seg_status guarded(F &&body) {
   }
 }
 
+// Brackets one kernel launch with HIP events when timing is enabled
+// (seg_profile_enable); a no-op otherwise.
+class ProfScope {
+ public:
+  ProfScope(const char *name, hipStream_t s);
+  ~ProfScope();
+  ProfScope(const ProfScope &) = delete;
+  ProfScope &operator=(const ProfScope &) = delete;
+
+ private:
+  const char *name_;
+  hipStream_t stream_;
+  hipEvent_t start_{}, stop_{};
+  bool active_ = false;
+};
+
 inline size_t align_up(size_t x, size_t a = 256) { return (x + a - 1) / a * a; }
 
 // Carves aligned sub-buffers out of a caller workspace.

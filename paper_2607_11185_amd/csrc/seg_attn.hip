@@ -640,6 +640,7 @@ void check_common(const seg_layout *L, const seg_sizes *sz, seg_dtype dt, int hq
 template <class TI, int D>
 void launch_transpose(const TI *x, int nh, const seg_layout *L, int G, unsigned short *out,
                       hipStream_t st) {
+  ProfScope prof("attn_prep", st);
   k_transpose_tiles<TI, D><<<G * nh, 256, 0, st>>>(x, nh, L->seg_info, L->tile_seg, out);
   SEG_LAUNCH_CHECK();
 }
@@ -653,6 +654,7 @@ void transpose_any(int d, const TI *x, int nh, const seg_layout *L, int G, unsig
 
 void to_bf16(const void *x, unsigned short *y, long n, hipStream_t st) {
   int grid = (int)std::min<long>(65536, (n + 255) / 256);
+  ProfScope prof("attn_prep", st);
   k_f32_to_bf16<<<std::max(1, grid), 256, 0, st>>>(static_cast<const float *>(x), y, n);
   SEG_LAUNCH_CHECK();
 }
@@ -662,6 +664,7 @@ void fwd_impl(const seg_layout *L, const seg_sizes *sz, int hq, int hkv, float s
               const unsigned short *q, const unsigned short *k, const unsigned short *vt, void *o,
               float *lse, hipStream_t st) {
   const int G = sz->num_qtiles;
+  ProfScope prof("attn_fwd", st);
   k_attn_fwd<D, TO><<<G * hq, 256, 0, st>>>(q, k, vt, L->seg_info, L->tile_seg, L->tok_meta,
                                             L->qt_ptr, L->qt_col, L->qt_cls, L->work_order, hq,
                                             hkv, L->window, scale * LOG2E, sz->packed_tokens,
@@ -679,17 +682,22 @@ void bwd_impl(const seg_layout *L, const seg_sizes *sz, int hq, int hkv, float s
   const long P = sz->packed_tokens;
   {
     const long threads = P * hq * (D / 8);
+    ProfScope prof("attn_delta", st);
     k_delta<TI, D><<<(int)((threads + 255) / 256), 256, 0, st>>>(o_raw, dout_raw, hq, P, delta);
     SEG_LAUNCH_CHECK();
   }
   launch_transpose<unsigned short, D>(k, hkv, L, G, kt, st);
   launch_transpose<unsigned short, D>(q, hq, L, G, qt, st);
   launch_transpose<unsigned short, D>(dout, hq, L, G, dot, st);
+  {
+  ProfScope prof("attn_bwd_dkdv", st);
   k_attn_bwd_dkdv<D, TO><<<G * hkv, 256, 0, st>>>(
       q, k, v, dout, qt, dot, lse, delta, L->seg_info, L->tile_seg, L->tok_meta, L->kt_ptr,
       L->kt_row, L->kt_cls, hq, hkv, L->window, scale * LOG2E, scale, P,
       static_cast<TO *>(dk), static_cast<TO *>(dv));
   SEG_LAUNCH_CHECK();
+  }
+  ProfScope prof("attn_bwd_dq", st);
   k_attn_bwd_dq<D, TO><<<G * hq, 256, 0, st>>>(
       q, k, v, dout, kt, lse, delta, L->seg_info, L->tile_seg, L->tok_meta, L->qt_ptr, L->qt_col,
       L->qt_cls, L->work_order, hq, hkv, L->window, scale * LOG2E, scale, P,

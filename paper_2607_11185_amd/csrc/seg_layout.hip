@@ -562,6 +562,7 @@ extern "C" seg_status seg_build_layout(const seg_problem *p, const seg_sizes *sz
     // the host tables are locals of this call: wait until they have been read
     SEG_HIP(hipStreamSynchronize(stream));
 
+    ProfScope prof("layout", stream);
     SEG_HIP(hipMemsetAsync(d_kcnt, 0, sizeof(int32_t) * G, stream));
     SEG_HIP(hipMemsetAsync(out->seg_pairs, 0, sizeof(int64_t) * S, stream));
     if (P > 0) {

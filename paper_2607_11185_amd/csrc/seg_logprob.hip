@@ -384,6 +384,7 @@ void logprob_impl(int rows, int H, int V, const TI *h, const int32_t *row_index,
 
   // gathered action rows (bf16)
   {
+    ProfScope prof("lp_prep", st);
     const long n = (long)Rp * H;
     k_gather_rows<TI><<<(int)std::min<long>(65536, (n + 255) / 256), 256, 0, st>>>(
         h, H, row_index, rows, Rp, H, hb);
@@ -393,6 +394,7 @@ void logprob_impl(int rows, int H, int V, const TI *h, const int32_t *row_index,
   if constexpr (sizeof(TI) == 4) {
     unsigned short *w2 = reinterpret_cast<unsigned short *>(base + L.wb);
     const long n = (long)V * H;
+    ProfScope prof("lp_prep", st);
     k_gather_rows<TI><<<(int)std::min<long>(65536, (n + 255) / 256), 256, 0, st>>>(
         w, H, nullptr, V, V, H, w2);
     SEG_LAUNCH_CHECK();
@@ -406,28 +408,39 @@ void logprob_impl(int rows, int H, int V, const TI *h, const int32_t *row_index,
   {
     EpiLogits e{zt, Rp, stats, rows, target, ztgt, cfg.logit_scale};
     dim3 grid((rows + BN - 1) / BN, (V + BM - 1) / BM);
+    ProfScope prof("logits", st);
     k_gemm_nt<0, EpiLogits><<<grid, 256, 0, st>>>(wb, H, hb, H, V, rows, H, e);
     SEG_LAUNCH_CHECK();
   }
   // 2. per-row loss
+  {
+  ProfScope prof("row_loss", st);
   k_row_loss<<<rows, 256, 0, st>>>(stats, L.ntiles, rows, ztgt, old_logp, adv, row_traj, num_traj,
                                    cfg, logp, loss_tok, clipped, lse, g);
   SEG_LAUNCH_CHECK();
   k_loss_sum<<<1, 256, 0, st>>>(loss_tok, rows, cfg.loss_scale, loss_sum);
   SEG_LAUNCH_CHECK();
+  }
   if (!cfg.want_grad) return;
   // 3. dz in both orientations
+  {
+  ProfScope prof("dz", st);
   k_dz<<<grid2(Rp, Vp), 256, 0, st>>>(zt, Rp, V, rows, Vp, Rp, lse, g, target, dz, dzt);
   SEG_LAUNCH_CHECK();
+  }
   // transposed operands: hT [H][Rp], Wt [H][Vp]
+  {
+  ProfScope prof("lp_prep", st);
   k_transpose2d<unsigned short><<<grid2(H, Rp), 256, 0, st>>>(hb, H, nullptr, Rp, H, Rp, ht, Rp);
   SEG_LAUNCH_CHECK();
   k_transpose2d<unsigned short><<<grid2(H, Vp), 256, 0, st>>>(wb, H, nullptr, V, H, Vp, wt, Vp);
   SEG_LAUNCH_CHECK();
+  }
   // 4. dH = s * dz W  (M = rows, N = H, K = Vp)
   {
     EpiStore<TO> e{static_cast<TO *>(dh), H, cfg.logit_scale};
     dim3 grid((H + BN - 1) / BN, (rows + BM - 1) / BM);
+    ProfScope prof("dh", st);
     k_gemm_nt<1, EpiStore<TO>><<<grid, 256, 0, st>>>(dz, Vp, wt, Vp, rows, H, Vp, e);
     SEG_LAUNCH_CHECK();
   }
@@ -435,6 +448,7 @@ void logprob_impl(int rows, int H, int V, const TI *h, const int32_t *row_index,
   {
     EpiStore<float> e{dw, H, cfg.logit_scale};
     dim3 grid((H + BN - 1) / BN, (V + BM - 1) / BM);
+    ProfScope prof("dw", st);
     k_gemm_nt<1, EpiStore<float>><<<grid, 256, 0, st>>>(dzt, Rp, ht, Rp, V, H, Rp, e);
     SEG_LAUNCH_CHECK();
   }

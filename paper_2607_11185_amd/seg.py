@@ -118,13 +118,22 @@ class Layout:
         return out
 
 
-def seg_build_layout(problem: Problem, sizes: Optional[SegSizes] = None, device="cuda") -> Layout:
-    """Build every layout array on the device (token, loss-row and tile kernels)."""
+def seg_build_layout(problem: Problem, sizes: Optional[SegSizes] = None, device="cuda",
+                     out: Optional[Layout] = None) -> Layout:
+    """Build every layout array on the device (token, loss-row and tile kernels).
+
+    ``out`` reuses the arrays of an earlier layout of the same sizes.
+    """
     import torch
     device = torch.device(device)
     if sizes is None:
         sizes = seg_layout_query(problem)
-    lay = Layout(sizes, device)
+    if out is not None:
+        if bytes(out.sizes) != bytes(sizes):
+            raise ValueError("out was built for different sizes")
+        lay = out
+    else:
+        lay = Layout(sizes, device)
     check(_lib.lib().seg_build_layout(ctypes.byref(problem.c()), ctypes.byref(sizes),
                                       ctypes.byref(lay.c), lay.ws.data_ptr(), lay.ws.numel(),
                                       _stream(device)))

@@ -26,7 +26,7 @@ def test_exports_every_declared_symbol():
     L = _lib_or_skip()
     with open(os.path.join(ROOT, "include", "seg.h")) as f:
         hdr = f.read()
-    declared = set(re.findall(r"^\s*(?:seg_status|size_t|const char \*)\s*(seg_\w+)\s*\(", hdr, re.M))
+    declared = set(re.findall(r"^\s*(?:seg_status|size_t|void|const char \*)\s*(seg_\w+)\s*\(", hdr, re.M))
     assert declared == set(_lib.EXPORTS)
     for name in declared:
         assert hasattr(L, name), name
