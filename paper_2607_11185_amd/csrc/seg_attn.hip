@@ -10,9 +10,9 @@
 // MFMA v_mfma_f32_32x32x16_bf16 lane layout used throughout (lane l, c = l%32,
 // h = l/32):  A[i][k]: i = c, k = 8h + 0..7;  B[k][j]: j = c, k = 8h + 0..7;
 // D[i][j] (16 regs r): j = c, i = 8*(r/4) + 4h + r%4.
-// Products that contract over the rows held in accumulator registers read the
-// other operand from "transposed tiles" T[tile][head][d][128] whose positions
-// follow kperm() inside each 16-row chunk (see common.h).
+// Products that contract over the rows held in accumulator registers take
+// their other operand from LDS through transpose reads in the same row order
+// (kperm() in common.h).
 #include <climits>
 #include <cmath>
 
@@ -72,38 +72,6 @@ __device__ __forceinline__ u16x8 load8_bf(const float *p) {
 
 // ------------------------------------------------------------- prep kernels
 
-// Transposed tiles: T[(g*nh + h)][d][p] = X[row of position p][h][d] (bf16),
-// zero beyond the tile's rows.
-template <class TI, int D>
-__global__ void __launch_bounds__(256) k_transpose_tiles(const TI *__restrict__ x, int nh,
-                                                         const int32_t *__restrict__ seg_info,
-                                                         const int32_t *__restrict__ tile_seg,
-                                                         unsigned short *__restrict__ out) {
-  constexpr int LD = D + 8;
-  __shared__ unsigned short t[TQ * LD];
-  const int g = blockIdx.x / nh, h = blockIdx.x % nh;
-  const TileRows tr = tile_rows(seg_info, tile_seg, g);
-  for (int c = threadIdx.x; c < TQ * D / 8; c += 256) {
-    const int row = c / (D / 8), ch = c % (D / 8);
-    u16x8 v = {0, 0, 0, 0, 0, 0, 0, 0};
-    if (row < tr.nrows)
-      v = load8_bf(x + ((long)(tr.start + tr.row0 + row) * nh + h) * D + ch * 8);
-    *reinterpret_cast<u16x8 *>(&t[row * LD + ch * 8]) = v;
-  }
-  __syncthreads();
-  unsigned short *o = out + ((long)g * nh + h) * D * TQ;
-  for (int c = threadIdx.x; c < D * TQ / 8; c += 256) {
-    const int d = c / (TQ / 8), pc = c % (TQ / 8);
-    u16x8 v;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int p = pc * 8 + j;
-      v[j] = t[((p & ~15) | kperm(p & 15)) * LD + d];
-    }
-    *reinterpret_cast<u16x8 *>(o + d * TQ + pc * 8) = v;
-  }
-}
-
 // fp32 -> bf16 copy (row-major, any shape)
 __global__ void k_f32_to_bf16(const float *__restrict__ x, unsigned short *__restrict__ y, long n) {
   for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x)
@@ -144,25 +112,127 @@ __global__ void __launch_bounds__(256) k_delta(const TI *__restrict__ o, const T
   }
 }
 
-// ------------------------------------------------------------- forward
+// ------------------------------------------------------------- pipelined kernels
+//
+// Tiles of 64 rows x d (row-major, bf16) are staged in LDS by direct 16-byte
+// global->LDS loads (each wave instruction fills 1 KB, lane-contiguous) into a
+// double buffer: the loads of the next unit are issued before the MFMA work of
+// the current one.  Rows are stored with a 16-byte-chunk swizzle that keeps
+// both 16-byte row reads (MFMA operands contracting over d) and 4x16 transpose
+// reads (ds_read_b64_tr_b16: operands contracting over the rows) free of bank
+// conflicts, so no transposed copy of any tensor is needed.
 
-// One block = one q-tile x one query head; 4 waves of 32 query rows.
-// S^T = K Q^T (keys on accumulator rows, queries on lanes), online softmax in
-// the exp2 domain, O^T += V^T P^T with V^T from transposed tiles.
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+
+template <int D>
+__device__ __forceinline__ int swz(int row) {
+  if constexpr (D == 128) return ((row & 7) << 1) | ((row >> 3) & 1);
+  else return (((row >> 1) & 3) << 1) | ((row >> 3) & 1);
+}
+
+template <int D>
+__device__ __forceinline__ int toff(int row, int col) {
+  return row * D + ((((col >> 3) ^ swz<D>(row))) << 3) + (col & 7);
+}
+
+// 8 consecutive columns (16-byte chunk `chunk`) of row `row`
+template <int D>
+__device__ __forceinline__ bf16x8 ld_row8(const unsigned short *t, int row, int chunk) {
+  return *reinterpret_cast<const bf16x8 *>(t + row * D + ((chunk ^ swz<D>(row)) << 3));
+}
+
+// Operand fragment contracting over tile rows: lane l receives column
+// n_base + l%32 of rows base + kperm(8h + j), j = 0..7 (h = l/32), i.e. the
+// MFMA k-order used by accumulator-held operands.
+template <int D>
+__device__ __forceinline__ bf16x8 ld_tr8(const unsigned short *t, int base, int n_base, int lane) {
+  const int l16 = lane & 15, g = lane >> 4, h = lane >> 5;
+  const int row = base + 4 * h + (l16 >> 2);
+  const int col = n_base + 16 * (g & 1) + 4 * (l16 & 3);
+  const v4i16 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)(t + toff<D>(row, col)));
+  const v4i16 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)(t + toff<D>(row + 8, col)));
+  bf16x8 r;
+  const bf16x4 a4 = __builtin_bit_cast(bf16x4, a), b4 = __builtin_bit_cast(bf16x4, b);
+  r[0] = a4[0]; r[1] = a4[1]; r[2] = a4[2]; r[3] = a4[3];
+  r[4] = b4[0]; r[5] = b4[1]; r[6] = b4[2]; r[7] = b4[3];
+  return r;
+}
+
+// Fill a 64-row swizzled tile: tile row r comes from `base + rowoff(r)` (d
+// contiguous bf16).  4 waves, each issuing D/32 1-KB instructions.
+template <int D, class RowOff>
+__device__ __forceinline__ void fill64(unsigned short *tile, const unsigned short *base,
+                                       RowOff rowoff, int wave, int lane) {
+  constexpr int CPR = D / 8, PER_WAVE = 64 * CPR / 256;
+#pragma unroll
+  for (int i = 0; i < PER_WAVE; ++i) {
+    const int s0 = (wave * PER_WAVE + i) * 64;
+    const int s = s0 + lane;
+    const int row = s / CPR, ch = (s % CPR) ^ swz<D>(row);
+    __builtin_amdgcn_global_load_lds(base + rowoff(row) + ch * 8,
+                                     (__attribute__((address_space(3))) void *)(tile + s0 * 8), 16, 0, 0);
+  }
+}
+
+// 64 consecutive 4-byte values (one per lane) into LDS
+__device__ __forceinline__ void fill64_dw(void *dst, const void *src_lane) {
+  __builtin_amdgcn_global_load_lds(src_lane, (__attribute__((address_space(3))) void *)dst, 4, 0, 0);
+}
+
+__device__ __forceinline__ void wait_all_and_sync() {
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+}
+
+// A unit of work: 64 rows (half of a 128-row tile) of the tile listed at CSR
+// entry e.
+struct Unit {
+  int e, half;
+  int r0;     // segment-relative first row of the unit
+  int vrows;  // valid rows (1..64)
+  bool partial;
+};
+
+__device__ __forceinline__ Unit make_unit(const int32_t *col_idx, const uint8_t *cls, int e,
+                                          int half, int qbase, int seg_len) {
+  Unit u;
+  u.e = e;
+  u.half = half;
+  const int t0 = (col_idx[e] - qbase) * TQ;
+  u.r0 = t0 + half * 64;
+  u.vrows = min(64, seg_len - u.r0);
+  u.partial = cls[e] == SEG_TILE_PARTIAL;
+  return u;
+}
+
+// next unit: the second half of the same tile when it has rows, else the next entry
+__device__ __forceinline__ bool next_unit(const Unit &u, int e1, const int32_t *col_idx,
+                                          const uint8_t *cls, int qbase, int seg_len, Unit &nu) {
+  if (u.half == 0 && u.r0 + 64 < seg_len) {
+    nu = make_unit(col_idx, cls, u.e, 1, qbase, seg_len);
+    return true;
+  }
+  if (u.e + 1 < e1) {
+    nu = make_unit(col_idx, cls, u.e + 1, 0, qbase, seg_len);
+    return true;
+  }
+  return false;
+}
+
+// Forward: one block = one q-tile x one query head, 4 waves of 32 query rows;
+// units are 64-key halves of the listed k-tiles.
 template <int D, class TO>
-__global__ void __launch_bounds__(256, 2) k_attn_fwd(
+__global__ void __launch_bounds__(256, 2) k_attn_fwd2(
     const unsigned short *__restrict__ q, const unsigned short *__restrict__ k,
-    const unsigned short *__restrict__ vt, const int32_t *__restrict__ seg_info,
+    const unsigned short *__restrict__ v, const int32_t *__restrict__ seg_info,
     const int32_t *__restrict__ tile_seg, const int32_t *__restrict__ tok_meta,
     const int32_t *__restrict__ qt_ptr, const int32_t *__restrict__ qt_col,
     const uint8_t *__restrict__ qt_cls, const int32_t *__restrict__ work_order, int hq, int hkv,
     int W, float scale_log2, long P, TO *__restrict__ o, float *__restrict__ lse) {
-  constexpr int KK = D / 16;   // k-steps over the head dim
-  constexpr int CPR = D / 8;   // 16-byte chunks per K row
-  constexpr int DB = D / 32;   // 32-row blocks of the head dim
-  __shared__ unsigned short sK[TQ * D];
-  __shared__ unsigned short sV[D * TQ];
-  __shared__ int sKexp[TQ];
+  constexpr int KK = D / 16, DB = D / 32, T64 = 64 * D;
+  __shared__ __attribute__((aligned(16))) unsigned short smem[4 * T64];  // K[2], V[2]
+  __shared__ __attribute__((aligned(16))) int sMeta[2][64];
 
   const int g = work_order[blockIdx.x / hq];
   const int h = blockIdx.x % hq;
@@ -172,108 +242,98 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd(
   const int col = lane & 31, hh = lane >> 5;
   const int qloc = wave * 32 + col;
   const bool qvalid = qloc < tr.nrows;
-  const int qr = tr.row0 + qloc;  // segment-relative query row
-  const int qstep = qvalid ? (tok_meta[tr.start + qr] >> 2) : 0;
+  const int qr = tr.row0 + (qvalid ? qloc : 0);
+  const int qstep = tok_meta[tr.start + qr] >> 2;
 
   bf16x8 qf[KK];
   {
-    const unsigned short *qrow = q + ((long)(tr.start + (qvalid ? qr : tr.row0)) * hq + h) * D;
+    const unsigned short *qrow = q + ((long)(tr.start + qr) * hq + h) * D;
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      qf[kk] = lds8(qrow + kk * 16 + hh * 8);
-      if (!qvalid) qf[kk] = bf16x8{};
-    }
+    for (int kk = 0; kk < KK; ++kk) qf[kk] = lds8(qrow + kk * 16 + hh * 8);
   }
   f32x16 oacc[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) oacc[db] = f32x16{};
   float m_run = -INFINITY, l_run = 0.f;
 
-  const int e0 = qt_ptr[g], e1 = qt_ptr[g + 1];
-  for (int e = e0; e < e1; ++e) {
-    const int gk = qt_col[e];
-    const bool partial = qt_cls[e] == SEG_TILE_PARTIAL;
-    const int k0 = (gk - tr.qbase) * TQ;
-    const int krows = min(TQ, tr.len - k0);
-    __syncthreads();
-    for (int c = threadIdx.x; c < TQ * CPR; c += 256) {
-      const int row = c / CPR, ch = c % CPR;
-      u16x8 val = {0, 0, 0, 0, 0, 0, 0, 0};
-      if (row < krows) val = load8_bf(k + ((long)(tr.start + k0 + row) * hkv + hk) * D + ch * 8);
-      *reinterpret_cast<u16x8 *>(&sK[row * D + ((ch ^ (row & (CPR - 1))) * 8)]) = val;
-    }
-    {
-      const unsigned short *vsrc = vt + ((long)gk * hkv + hk) * D * TQ;
-      for (int c = threadIdx.x; c < D * 16; c += 256) {
-        const int row = c >> 4, ch = c & 15;
-        *reinterpret_cast<u16x8 *>(&sV[row * TQ + ((ch ^ (row & 15)) * 8)]) =
-            load8_bf(vsrc + row * TQ + ch * 8);
-      }
-    }
-    if (threadIdx.x < TQ) {
-      const int kr = threadIdx.x;
-      sKexp[kr] = kr < krows ? key_expiry(tok_meta[tr.start + k0 + kr], W) : INT_MIN;
-    }
-    __syncthreads();
+  const long kv_stride = (long)hkv * D;
+  const unsigned short *kbase = k + (long)hk * D + (long)tr.start * kv_stride;
+  const unsigned short *vbase = v + (long)hk * D + (long)tr.start * kv_stride;
+  auto issue = [&](const Unit &u, int b) {
+    auto rowoff = [&](int r) { return (long)(u.r0 + min(r, u.vrows - 1)) * kv_stride; };
+    fill64<D>(smem + b * T64, kbase, rowoff, wave, lane);
+    fill64<D>(smem + (2 + b) * T64, vbase, rowoff, wave, lane);
+    if (wave == 0) fill64_dw(&sMeta[b][0], tok_meta + tr.start + u.r0 + min(lane, u.vrows - 1));
+  };
 
-    f32x16 sacc[4];
+  const int e0 = qt_ptr[g], e1 = qt_ptr[g + 1];
+  Unit u = make_unit(qt_col, qt_cls, e0, 0, tr.qbase, tr.len);
+  issue(u, 0);
+  wait_all_and_sync();
+  int b = 0;
+  for (;;) {
+    Unit nu;
+    const bool more = next_unit(u, e1, qt_col, qt_cls, tr.qbase, tr.len, nu);
+    if (more) issue(nu, b ^ 1);
+    const unsigned short *sK = smem + b * T64, *sV = smem + (2 + b) * T64;
+    f32x16 sacc[2];
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
+    for (int kb = 0; kb < 2; ++kb) {
+      bf16x8 ak[KK];
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) ak[kk] = ld_row8<D>(sK, kb * 32 + col, kk * 2 + hh);
       sacc[kb] = f32x16{};
-      const int key = kb * 32 + col;
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
-        const int ch = kk * 2 + hh;
-        sacc[kb] = mfma32(lds8(&sK[key * D + ((ch ^ (key & (CPR - 1))) * 8)]), qf[kk], sacc[kb]);
-      }
+      for (int kk = 0; kk < KK; ++kk) sacc[kb] = mfma32(ak[kk], qf[kk], sacc[kb]);
     }
     float mloc = -INFINITY;
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         float sv = sacc[kb][r] * scale_log2;
-        if (partial) {
+        if (u.partial) {
           const int key = kb * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-          const bool vis = qvalid && (k0 + key <= qr) && (qstep < sKexp[key]);
+          const bool vis = qvalid && key < u.vrows && (u.r0 + key <= qr) &&
+                           (qstep < key_expiry(sMeta[b][key], W));
           sv = vis ? sv : -INFINITY;
         }
         sacc[kb][r] = sv;
         mloc = fmaxf(mloc, sv);
       }
-    }
     mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
     const float m_new = fmaxf(m_run, mloc);
     const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
     const float alpha = exp2f(m_run - m_use);
     float rsum = 0.f;
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const float pv = exp2f(sacc[kb][r] - m_use);
         sacc[kb][r] = pv;
         rsum += pv;
       }
-    }
     rsum += __shfl_xor(rsum, 32, 64);
     l_run = l_run * alpha + rsum;
     m_run = m_new;
 #pragma unroll
     for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int c2 = 0; c2 < 2; ++c2) {
-        const bf16x8 pf = pack8(sacc[kb], c2 * 8);
-        const int chunk = kb * 4 + c2 * 2 + hh;
+        bf16x8 av[DB];
 #pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const int dd = db * 32 + col;
-          oacc[db] = mfma32(lds8(&sV[dd * TQ + ((chunk ^ (dd & 15)) * 8)]), pf, oacc[db]);
-        }
+        for (int db = 0; db < DB; ++db) av[db] = ld_tr8<D>(sV, kb * 32 + c2 * 16, db * 32, lane);
+        const bf16x8 pf = pack8(sacc[kb], c2 * 8);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) oacc[db] = mfma32(av[db], pf, oacc[db]);
       }
-    }
+    wait_all_and_sync();
+    if (!more) break;
+    u = nu;
+    b ^= 1;
   }
 
   if (qvalid) {
@@ -281,70 +341,55 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd(
     const long row = tr.start + qr;
     TO *orow = o + (row * hq + h) * D;
 #pragma unroll
-    for (int db = 0; db < DB; ++db) {
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int r4 = 0; r4 < 4; ++r4) {
         const int d0 = db * 32 + 8 * r4 + 4 * hh;
 #pragma unroll
         for (int j = 0; j < 4; ++j) store_val(orow, d0 + j, oacc[db][r4 * 4 + j] * inv);
       }
-    }
     if (hh == 0) lse[(long)h * P + row] = (m_run + log2f(l_run)) * LN2;
   }
 }
 
-// ------------------------------------------------------------- backward
-
-// dK/dV: one block = one k-tile x one kv head; wave w owns keys 32w..32w+31.
-// Loops over the q-tiles of the transposed CSR column and over the query heads
-// of the group, in 64-row halves.  S = Q K^T has queries on accumulator rows
-// and keys on lanes, so P and dS feed dV += P^T dO and dK += dS^T Q directly,
-// with dO^T and Q^T from transposed tiles.
+// dK/dV: one block = one k-tile x one kv head; wave w owns keys 32w..32w+31
+// (K and V fragments stay in registers).  Units are 64-row halves of the
+// listed q-tiles, for every query head of the group.
 template <int D, class TO>
-__global__ void __launch_bounds__(256, 1) k_attn_bwd_dkdv(
+__global__ void __launch_bounds__(256, 1) k_attn_bwd_dkdv2(
     const unsigned short *__restrict__ q, const unsigned short *__restrict__ k,
     const unsigned short *__restrict__ v, const unsigned short *__restrict__ dout,
-    const unsigned short *__restrict__ qt, const unsigned short *__restrict__ dot,
     const float *__restrict__ lse, const float *__restrict__ delta,
     const int32_t *__restrict__ seg_info, const int32_t *__restrict__ tile_seg,
     const int32_t *__restrict__ tok_meta, const int32_t *__restrict__ kt_ptr,
     const int32_t *__restrict__ kt_row, const uint8_t *__restrict__ kt_cls, int hq, int hkv,
     int W, float scale_log2, float scale, long P, TO *__restrict__ dk, TO *__restrict__ dv) {
-  constexpr int KK = D / 16, CPR = D / 8, DB = D / 32;
-  constexpr int HQ = 64;  // query rows per half
-  __shared__ unsigned short sQ[HQ * D];
-  __shared__ unsigned short sdO[HQ * D];
-  __shared__ unsigned short sQt[D * HQ];
-  __shared__ unsigned short sdOt[D * HQ];
-  __shared__ float sLse[HQ], sDelta[HQ];
-  __shared__ int sQstep[HQ], sQrow[HQ];
+  constexpr int KK = D / 16, DB = D / 32, T64 = 64 * D;
+  __shared__ __attribute__((aligned(16))) unsigned short smem[4 * T64];  // Q[2], dO[2]
+  __shared__ __attribute__((aligned(16))) float sLse[2][64];
+  __shared__ __attribute__((aligned(16))) float sDel[2][64];
+  __shared__ __attribute__((aligned(16))) int sMeta[2][64];
 
-  // k-tiles in natural order: within a segment the earliest k-tiles have the
-  // longest transposed-CSR columns, so they start first.
   const int g = blockIdx.x / hkv;
   const int hk = blockIdx.x % hkv;
   const int grp = hq / hkv;
-  const TileRows tr = tile_rows(seg_info, tile_seg, g);  // this k-tile
+  const TileRows tr = tile_rows(seg_info, tile_seg, g);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int col = lane & 31, hh = lane >> 5;
   const int kloc = wave * 32 + col;
   const bool kvalid = kloc < tr.nrows;
-  const int kr = tr.row0 + kloc;  // segment-relative key row
-  const int kexp = kvalid ? key_expiry(tok_meta[tr.start + kr], W) : INT_MIN;
+  const int kr = tr.row0 + (kvalid ? kloc : 0);
+  const int kexp = key_expiry(tok_meta[tr.start + kr], W);
 
   bf16x8 kf[KK], vf[KK];
   {
-    const long row = tr.start + (kvalid ? kr : tr.row0);
+    const long row = tr.start + kr;
     const unsigned short *krow = k + (row * hkv + hk) * D;
     const unsigned short *vrow = v + (row * hkv + hk) * D;
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       kf[kk] = lds8(krow + kk * 16 + hh * 8);
       vf[kk] = lds8(vrow + kk * 16 + hh * 8);
-      if (!kvalid) {
-        kf[kk] = bf16x8{};
-        vf[kk] = bf16x8{};
-      }
     }
   }
   f32x16 dkacc[DB], dvacc[DB];
@@ -354,125 +399,151 @@ __global__ void __launch_bounds__(256, 1) k_attn_bwd_dkdv(
     dvacc[db] = f32x16{};
   }
 
+  const long q_stride = (long)hq * D;
   const int e0 = kt_ptr[g], e1 = kt_ptr[g + 1];
-  for (int e = e0; e < e1; ++e) {
-    const int gq = kt_row[e];
-    const bool partial = kt_cls[e] == SEG_TILE_PARTIAL;
-    const int q0 = (gq - tr.qbase) * TQ;
-    const int qrows = min(TQ, tr.len - q0);
-    for (int hi = 0; hi < grp; ++hi) {
-      const int h = hk * grp + hi;
-      for (int half = 0; half < 2; ++half) {
-        const int hq0 = half * HQ;  // first row of this half inside the q-tile
-        if (hq0 >= qrows) break;
-        __syncthreads();
-        for (int c = threadIdx.x; c < HQ * CPR; c += 256) {
-          const int row = c / CPR, ch = c % CPR;
-          u16x8 a = {0, 0, 0, 0, 0, 0, 0, 0}, b = a;
-          if (hq0 + row < qrows) {
-            const long off = ((long)(tr.start + q0 + hq0 + row) * hq + h) * D + ch * 8;
-            a = load8_bf(q + off);
-            b = load8_bf(dout + off);
-          }
-          const int sw = (ch ^ (row & (CPR - 1))) * 8;
-          *reinterpret_cast<u16x8 *>(&sQ[row * D + sw]) = a;
-          *reinterpret_cast<u16x8 *>(&sdO[row * D + sw]) = b;
-        }
-        {
-          const long tb = ((long)gq * hq + h) * D * TQ + hq0;
-          for (int c = threadIdx.x; c < D * (HQ / 8); c += 256) {
-            const int row = c / (HQ / 8), ch = c % (HQ / 8);
-            const int sw = (ch ^ (row & 7)) * 8;
-            *reinterpret_cast<u16x8 *>(&sQt[row * HQ + sw]) = load8_bf(qt + tb + row * TQ + ch * 8);
-            *reinterpret_cast<u16x8 *>(&sdOt[row * HQ + sw]) = load8_bf(dot + tb + row * TQ + ch * 8);
-          }
-        }
-        if (threadIdx.x < HQ) {
-          const int r = threadIdx.x;
-          const bool ok = hq0 + r < qrows;
-          const long row = tr.start + q0 + hq0 + r;
-          sLse[r] = ok ? lse[(long)h * P + row] * LOG2E : INFINITY;
-          sDelta[r] = ok ? delta[(long)h * P + row] : 0.f;
-          sQstep[r] = ok ? (tok_meta[row] >> 2) : INT_MAX;
-          sQrow[r] = ok ? (q0 + hq0 + r) : -1;
-        }
-        __syncthreads();
+  // unit = (entry e, head index hi, half); heads vary fastest after halves
+  auto issue = [&](const Unit &u, int hi, int b) {
+    const int h = hk * grp + hi;
+    const unsigned short *qb = q + (long)h * D + (long)tr.start * q_stride;
+    const unsigned short *db_ = dout + (long)h * D + (long)tr.start * q_stride;
+    auto rowoff = [&](int r) { return (long)(u.r0 + min(r, u.vrows - 1)) * q_stride; };
+    fill64<D>(smem + b * T64, qb, rowoff, wave, lane);
+    fill64<D>(smem + (2 + b) * T64, db_, rowoff, wave, lane);
+    const long lrow = tr.start + u.r0 + min(lane, u.vrows - 1);
+    if (wave == 0) fill64_dw(&sLse[b][0], lse + (long)h * P + lrow);
+    if (wave == 1) fill64_dw(&sDel[b][0], delta + (long)h * P + lrow);
+    if (wave == 2) fill64_dw(&sMeta[b][0], tok_meta + lrow);
+  };
 
+  if (e0 < e1) {
+    Unit u = make_unit(kt_row, kt_cls, e0, 0, tr.qbase, tr.len);
+    int hi = 0;
+    issue(u, hi, 0);
+    wait_all_and_sync();
+    int b = 0;
+    for (;;) {
+      // next unit: other half of this tile, else next head, else next entry
+      Unit nu = u;
+      int nhi = hi;
+      bool more = true;
+      if (u.half == 0 && u.r0 + 64 < tr.len) {
+        nu = make_unit(kt_row, kt_cls, u.e, 1, tr.qbase, tr.len);
+      } else if (hi + 1 < grp) {
+        nu = make_unit(kt_row, kt_cls, u.e, 0, tr.qbase, tr.len);
+        nhi = hi + 1;
+      } else if (u.e + 1 < e1) {
+        nu = make_unit(kt_row, kt_cls, u.e + 1, 0, tr.qbase, tr.len);
+        nhi = 0;
+      } else {
+        more = false;
+      }
+      if (more) issue(nu, nhi, b ^ 1);
+
+      const unsigned short *sQ = smem + b * T64, *sdO = smem + (2 + b) * T64;
 #pragma unroll
-        for (int qb = 0; qb < HQ / 32; ++qb) {
-          f32x16 s = f32x16{}, dp = f32x16{};
-          const int qrow = qb * 32 + col;
+      for (int qb = 0; qb < 2; ++qb) {
+        if (qb * 32 >= u.vrows) break;
+        bf16x8 aq[KK], ad[KK];
 #pragma unroll
-          for (int kk = 0; kk < KK; ++kk) {
-            const int ch = kk * 2 + hh;
-            const int sw = (ch ^ (qrow & (CPR - 1))) * 8;
-            s = mfma32(lds8(&sQ[qrow * D + sw]), kf[kk], s);
-            dp = mfma32(lds8(&sdO[qrow * D + sw]), vf[kk], dp);
-          }
-          // P and dS; accumulator row r holds query qb*32 + 8*(r/4) + 4*hh + r%4
+        for (int kk = 0; kk < KK; ++kk) {
+          aq[kk] = ld_row8<D>(sQ, qb * 32 + col, kk * 2 + hh);
+          ad[kk] = ld_row8<D>(sdO, qb * 32 + col, kk * 2 + hh);
+        }
+        f32x16 s = f32x16{}, dp = f32x16{};
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int ql = qb * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-            float pv = exp2f(s[r] * scale_log2 - sLse[ql]);
-            bool vis = kvalid && sQrow[ql] >= 0;
-            if (partial) vis = vis && (kr <= sQrow[ql]) && (sQstep[ql] < kexp);
+        for (int kk = 0; kk < KK; ++kk) {
+          s = mfma32(aq[kk], kf[kk], s);
+          dp = mfma32(ad[kk], vf[kk], dp);
+        }
+#pragma unroll
+        for (int rg = 0; rg < 4; ++rg) {
+          const int base = qb * 32 + 8 * rg + 4 * hh;
+          const f32x4 L4 = *reinterpret_cast<const f32x4 *>(&sLse[b][base]);
+          const f32x4 D4 = *reinterpret_cast<const f32x4 *>(&sDel[b][base]);
+          typedef int i32x4 __attribute__((ext_vector_type(4)));
+          const i32x4 M4 = *reinterpret_cast<const i32x4 *>(&sMeta[b][base]);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int r = rg * 4 + j, ql = base + j;
+            float pv = exp2f(s[r] * scale_log2 - L4[j] * LOG2E);
+            bool vis = kvalid && ql < u.vrows;
+            if (u.partial) vis = vis && (kr <= u.r0 + ql) && ((M4[j] >> 2) < kexp);
             pv = vis ? pv : 0.f;
             s[r] = pv;
-            dp[r] = pv * (dp[r] - sDelta[ql]);
+            dp[r] = pv * (dp[r] - D4[j]);
           }
+        }
 #pragma unroll
-          for (int c2 = 0; c2 < 2; ++c2) {
-            const bf16x8 pa = pack8(s, c2 * 8);
-            const bf16x8 dsa = pack8(dp, c2 * 8);
-            const int chunk = qb * 4 + c2 * 2 + hh;  // 16-byte chunk of the transposed row
+        for (int c2 = 0; c2 < 2; ++c2) {
+          bf16x8 bo[DB], bq[DB];
 #pragma unroll
-            for (int db = 0; db < DB; ++db) {
-              const int dd = db * 32 + col;
-              const int sw = (chunk ^ (dd & 7)) * 8;
-              dvacc[db] = mfma32(pa, lds8(&sdOt[dd * HQ + sw]), dvacc[db]);
-              dkacc[db] = mfma32(dsa, lds8(&sQt[dd * HQ + sw]), dkacc[db]);
-            }
+          for (int db = 0; db < DB; ++db) {
+            bo[db] = ld_tr8<D>(sdO, qb * 32 + c2 * 16, db * 32, lane);
+            bq[db] = ld_tr8<D>(sQ, qb * 32 + c2 * 16, db * 32, lane);
+          }
+          const bf16x8 pa = pack8(s, c2 * 8);
+          const bf16x8 dsa = pack8(dp, c2 * 8);
+#pragma unroll
+          for (int db = 0; db < DB; ++db) {
+            dvacc[db] = mfma32(pa, bo[db], dvacc[db]);
+            dkacc[db] = mfma32(dsa, bq[db], dkacc[db]);
           }
         }
       }
+      wait_all_and_sync();
+      if (!more) break;
+      u = nu;
+      hi = nhi;
+      b ^= 1;
     }
   }
 
-  // accumulator D[i = key][j = d]: lane holds d = db*32 + col, rows are keys
+  // stage through LDS for coalesced stores; accumulator D[i = key][j = d]
+  TO *st = reinterpret_cast<TO *>(smem);  // [128][D] of TO (fits: 4 * 64 * D * 2 bytes)
+  constexpr int CH = 16 / sizeof(TO);     // elements per 16-byte chunk
 #pragma unroll
-  for (int db = 0; db < DB; ++db) {
-    const int dd = db * 32 + col;
+  for (int which = 0; which < 2; ++which) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int kl = wave * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int kl = wave * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+        const float val = which == 0 ? dkacc[db][r] * scale : dvacc[db][r];
+        if constexpr (sizeof(TO) == 2)
+          st[kl * D + db * 32 + col] = f2bf_bits(val);
+        else
+          st[kl * D + db * 32 + col] = val;
+      }
+    __syncthreads();
+    TO *dst = which == 0 ? dk : dv;
+    for (int c = threadIdx.x; c < TQ * D / CH; c += 256) {
+      const int kl = c / (D / CH), ch = c % (D / CH);
       if (kl < tr.nrows) {
         const long row = tr.start + tr.row0 + kl;
-        store_val(dk, (row * hkv + hk) * D + dd, dkacc[db][r] * scale);
-        store_val(dv, (row * hkv + hk) * D + dd, dvacc[db][r]);
+        *reinterpret_cast<u16x8 *>(dst + (row * hkv + hk) * D + ch * CH) =
+            *reinterpret_cast<const u16x8 *>(st + kl * D + ch * CH);
       }
     }
+    __syncthreads();
   }
 }
 
-// dQ: one block = one q-tile x one query head; 4 waves of 32 query rows.
-// Recomputes S^T = K Q^T and dP^T = V dO^T per 64-key half of each listed
-// k-tile, then dQ^T += K^T dS^T with K^T from transposed tiles.
+// dQ: one block = one q-tile x one query head, 4 waves of 32 query rows;
+// units are 64-key halves of the listed k-tiles.  dQ^T += K^T dS^T with K^T
+// read transposed from the row-major K tile.
 template <int D, class TO>
-__global__ void __launch_bounds__(256, 2) k_attn_bwd_dq(
+__global__ void __launch_bounds__(256, 2) k_attn_bwd_dq2(
     const unsigned short *__restrict__ q, const unsigned short *__restrict__ k,
     const unsigned short *__restrict__ v, const unsigned short *__restrict__ dout,
-    const unsigned short *__restrict__ kt, const float *__restrict__ lse,
-    const float *__restrict__ delta, const int32_t *__restrict__ seg_info,
-    const int32_t *__restrict__ tile_seg, const int32_t *__restrict__ tok_meta,
-    const int32_t *__restrict__ qt_ptr, const int32_t *__restrict__ qt_col,
-    const uint8_t *__restrict__ qt_cls, const int32_t *__restrict__ work_order, int hq, int hkv,
-    int W, float scale_log2, float scale, long P, TO *__restrict__ dq) {
-  constexpr int KK = D / 16, CPR = D / 8, DB = D / 32;
-  constexpr int HK = 64;  // keys per half
-  __shared__ unsigned short sK[HK * D];
-  __shared__ unsigned short sV[HK * D];
-  __shared__ unsigned short sKt[D * HK];
-  __shared__ int sKexp[HK];
+    const float *__restrict__ lse, const float *__restrict__ delta,
+    const int32_t *__restrict__ seg_info, const int32_t *__restrict__ tile_seg,
+    const int32_t *__restrict__ tok_meta, const int32_t *__restrict__ qt_ptr,
+    const int32_t *__restrict__ qt_col, const uint8_t *__restrict__ qt_cls,
+    const int32_t *__restrict__ work_order, int hq, int hkv, int W, float scale_log2,
+    float scale, long P, TO *__restrict__ dq) {
+  constexpr int KK = D / 16, DB = D / 32, T64 = 64 * D;
+  __shared__ __attribute__((aligned(16))) unsigned short smem[4 * T64];  // K[2], V[2]
+  __shared__ __attribute__((aligned(16))) int sMeta[2][64];
 
   const int g = work_order[blockIdx.x / hq];
   const int h = blockIdx.x % hq;
@@ -482,11 +553,11 @@ __global__ void __launch_bounds__(256, 2) k_attn_bwd_dq(
   const int col = lane & 31, hh = lane >> 5;
   const int qloc = wave * 32 + col;
   const bool qvalid = qloc < tr.nrows;
-  const int qr = tr.row0 + qloc;
-  const long qrow_abs = tr.start + (qvalid ? qr : tr.row0);
-  const int qstep = qvalid ? (tok_meta[tr.start + qr] >> 2) : 0;
-  const float lse2 = qvalid ? lse[(long)h * P + qrow_abs] * LOG2E : INFINITY;
-  const float dlt = qvalid ? delta[(long)h * P + qrow_abs] : 0.f;
+  const int qr = tr.row0 + (qvalid ? qloc : 0);
+  const long qrow_abs = tr.start + qr;
+  const int qstep = tok_meta[qrow_abs] >> 2;
+  const float lse2 = lse[(long)h * P + qrow_abs] * LOG2E;
+  const float dlt = delta[(long)h * P + qrow_abs];
 
   bf16x8 qf[KK], df[KK];
   {
@@ -496,104 +567,89 @@ __global__ void __launch_bounds__(256, 2) k_attn_bwd_dq(
     for (int kk = 0; kk < KK; ++kk) {
       qf[kk] = lds8(qp + kk * 16 + hh * 8);
       df[kk] = lds8(dp + kk * 16 + hh * 8);
-      if (!qvalid) {
-        qf[kk] = bf16x8{};
-        df[kk] = bf16x8{};
-      }
     }
   }
   f32x16 dqacc[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) dqacc[db] = f32x16{};
 
-  const int e0 = qt_ptr[g], e1 = qt_ptr[g + 1];
-  for (int e = e0; e < e1; ++e) {
-    const int gk = qt_col[e];
-    const bool partial = qt_cls[e] == SEG_TILE_PARTIAL;
-    const int k0 = (gk - tr.qbase) * TQ;
-    const int krows = min(TQ, tr.len - k0);
-    for (int half = 0; half < 2; ++half) {
-      const int hk0 = half * HK;
-      if (hk0 >= krows) break;
-      __syncthreads();
-      for (int c = threadIdx.x; c < HK * CPR; c += 256) {
-        const int row = c / CPR, ch = c % CPR;
-        u16x8 a = {0, 0, 0, 0, 0, 0, 0, 0}, b = a;
-        if (hk0 + row < krows) {
-          const long off = ((long)(tr.start + k0 + hk0 + row) * hkv + hk) * D + ch * 8;
-          a = load8_bf(k + off);
-          b = load8_bf(v + off);
-        }
-        const int sw = (ch ^ (row & (CPR - 1))) * 8;
-        *reinterpret_cast<u16x8 *>(&sK[row * D + sw]) = a;
-        *reinterpret_cast<u16x8 *>(&sV[row * D + sw]) = b;
-      }
-      {
-        const long tb = ((long)gk * hkv + hk) * D * TQ + hk0;
-        for (int c = threadIdx.x; c < D * (HK / 8); c += 256) {
-          const int row = c / (HK / 8), ch = c % (HK / 8);
-          *reinterpret_cast<u16x8 *>(&sKt[row * HK + ((ch ^ (row & 7)) * 8)]) =
-              load8_bf(kt + tb + row * TQ + ch * 8);
-        }
-      }
-      if (threadIdx.x < HK) {
-        const int r = threadIdx.x;
-        sKexp[r] = hk0 + r < krows ? key_expiry(tok_meta[tr.start + k0 + hk0 + r], W) : INT_MIN;
-      }
-      __syncthreads();
+  const long kv_stride = (long)hkv * D;
+  const unsigned short *kbase = k + (long)hk * D + (long)tr.start * kv_stride;
+  const unsigned short *vbase = v + (long)hk * D + (long)tr.start * kv_stride;
+  auto issue = [&](const Unit &u, int b) {
+    auto rowoff = [&](int r) { return (long)(u.r0 + min(r, u.vrows - 1)) * kv_stride; };
+    fill64<D>(smem + b * T64, kbase, rowoff, wave, lane);
+    fill64<D>(smem + (2 + b) * T64, vbase, rowoff, wave, lane);
+    if (wave == 0) fill64_dw(&sMeta[b][0], tok_meta + tr.start + u.r0 + min(lane, u.vrows - 1));
+  };
 
+  const int e0 = qt_ptr[g], e1 = qt_ptr[g + 1];
+  Unit u = make_unit(qt_col, qt_cls, e0, 0, tr.qbase, tr.len);
+  issue(u, 0);
+  wait_all_and_sync();
+  int b = 0;
+  for (;;) {
+    Unit nu;
+    const bool more = next_unit(u, e1, qt_col, qt_cls, tr.qbase, tr.len, nu);
+    if (more) issue(nu, b ^ 1);
+    const unsigned short *sK = smem + b * T64, *sV = smem + (2 + b) * T64;
 #pragma unroll
-      for (int kb = 0; kb < HK / 32; ++kb) {
-        f32x16 s = f32x16{}, dp = f32x16{};
-        const int key = kb * 32 + col;
+    for (int kb = 0; kb < 2; ++kb) {
+      if (kb * 32 >= u.vrows) break;
+      bf16x8 ak[KK], av[KK];
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-          const int ch = kk * 2 + hh;
-          const int sw = (ch ^ (key & (CPR - 1))) * 8;
-          s = mfma32(lds8(&sK[key * D + sw]), qf[kk], s);
-          dp = mfma32(lds8(&sV[key * D + sw]), df[kk], dp);
-        }
+      for (int kk = 0; kk < KK; ++kk) {
+        ak[kk] = ld_row8<D>(sK, kb * 32 + col, kk * 2 + hh);
+        av[kk] = ld_row8<D>(sV, kb * 32 + col, kk * 2 + hh);
+      }
+      f32x16 s = f32x16{}, dp = f32x16{};
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int kl = kb * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-          float pv = exp2f(s[r] * scale_log2 - lse2);
-          bool vis = qvalid && (sKexp[kl] != INT_MIN);
-          if (partial) vis = vis && (k0 + hk0 + kl <= qr) && (qstep < sKexp[kl]);
-          pv = vis ? pv : 0.f;
-          s[r] = pv * (dp[r] - dlt);  // dS^T
-        }
+      for (int kk = 0; kk < KK; ++kk) {
+        s = mfma32(ak[kk], qf[kk], s);
+        dp = mfma32(av[kk], df[kk], dp);
+      }
 #pragma unroll
-        for (int c2 = 0; c2 < 2; ++c2) {
-          const bf16x8 dsb = pack8(s, c2 * 8);
-          const int chunk = kb * 4 + c2 * 2 + hh;
+      for (int r = 0; r < 16; ++r) {
+        const int kl = kb * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+        float pv = exp2f(s[r] * scale_log2 - lse2);
+        bool vis = qvalid && kl < u.vrows;
+        if (u.partial) vis = vis && (u.r0 + kl <= qr) && (qstep < key_expiry(sMeta[b][kl], W));
+        pv = vis ? pv : 0.f;
+        s[r] = pv * (dp[r] - dlt);
+      }
 #pragma unroll
-          for (int db = 0; db < DB; ++db) {
-            const int dd = db * 32 + col;
-            dqacc[db] = mfma32(lds8(&sKt[dd * HK + ((chunk ^ (dd & 7)) * 8)]), dsb, dqacc[db]);
-          }
-        }
+      for (int c2 = 0; c2 < 2; ++c2) {
+        bf16x8 kt[DB];
+#pragma unroll
+        for (int db = 0; db < DB; ++db) kt[db] = ld_tr8<D>(sK, kb * 32 + c2 * 16, db * 32, lane);
+        const bf16x8 dsb = pack8(s, c2 * 8);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) dqacc[db] = mfma32(kt[db], dsb, dqacc[db]);
       }
     }
+    wait_all_and_sync();
+    if (!more) break;
+    u = nu;
+    b ^= 1;
   }
 
   if (qvalid) {
     TO *qrowp = dq + (qrow_abs * hq + h) * D;
 #pragma unroll
-    for (int db = 0; db < DB; ++db) {
+    for (int db = 0; db < DB; ++db)
 #pragma unroll
       for (int r4 = 0; r4 < 4; ++r4) {
         const int d0 = db * 32 + 8 * r4 + 4 * hh;
 #pragma unroll
         for (int j = 0; j < 4; ++j) store_val(qrowp, d0 + j, dqacc[db][r4 * 4 + j] * scale);
       }
-    }
   }
 }
 
 // ------------------------------------------------------------- host side
 
 struct AttnWs {
-  size_t vt, kt, qt, dot, delta, qb, kb, vb, ob, dob, total;
+  size_t delta, qb, kb, vb, dob, total;
 };
 
 AttnWs attn_ws(const seg_sizes &sz, seg_dtype dt, int hq, int hkv, int d, int bwd) {
@@ -604,24 +660,15 @@ AttnWs attn_ws(const seg_sizes &sz, seg_dtype dt, int hq, int hkv, int d, int bw
     off = align_up(off + bytes);
     return o;
   };
-  const size_t G = (size_t)std::max(1, sz.num_qtiles);
   const size_t P = (size_t)std::max<int64_t>(1, sz.packed_tokens);
-  const size_t tkv = G * hkv * d * TQ * 2, tq = G * hq * d * TQ * 2;
-  if (!bwd) {
-    w.vt = take(tkv);
-  } else {
-    w.kt = take(tkv);
-    w.qt = take(tq);
-    w.dot = take(tq);
-    w.delta = take(P * hq * sizeof(float));
-  }
+  if (bwd) w.delta = take(P * hq * sizeof(float));
   if (dt == SEG_F32) {
     w.qb = take(P * hq * d * 2);
     w.kb = take(P * hkv * d * 2);
     w.vb = take(P * hkv * d * 2);
     if (bwd) w.dob = take(P * hq * d * 2);
   }
-  w.total = off;
+  w.total = std::max<size_t>(off, 256);
   return w;
 }
 
@@ -637,21 +684,6 @@ void check_common(const seg_layout *L, const seg_sizes *sz, seg_dtype dt, int hq
   SEG_CHECK((long)sz->packed_tokens * hq * d < (1L << 40), SEG_ERR_CAPACITY, "tensor too large");
 }
 
-template <class TI, int D>
-void launch_transpose(const TI *x, int nh, const seg_layout *L, int G, unsigned short *out,
-                      hipStream_t st) {
-  ProfScope prof("attn_prep", st);
-  k_transpose_tiles<TI, D><<<G * nh, 256, 0, st>>>(x, nh, L->seg_info, L->tile_seg, out);
-  SEG_LAUNCH_CHECK();
-}
-
-template <class TI>
-void transpose_any(int d, const TI *x, int nh, const seg_layout *L, int G, unsigned short *out,
-                   hipStream_t st) {
-  if (d == 128) launch_transpose<TI, 128>(x, nh, L, G, out, st);
-  else launch_transpose<TI, 64>(x, nh, L, G, out, st);
-}
-
 void to_bf16(const void *x, unsigned short *y, long n, hipStream_t st) {
   int grid = (int)std::min<long>(65536, (n + 255) / 256);
   ProfScope prof("attn_prep", st);
@@ -661,14 +693,14 @@ void to_bf16(const void *x, unsigned short *y, long n, hipStream_t st) {
 
 template <int D, class TO>
 void fwd_impl(const seg_layout *L, const seg_sizes *sz, int hq, int hkv, float scale,
-              const unsigned short *q, const unsigned short *k, const unsigned short *vt, void *o,
+              const unsigned short *q, const unsigned short *k, const unsigned short *v, void *o,
               float *lse, hipStream_t st) {
   const int G = sz->num_qtiles;
   ProfScope prof("attn_fwd", st);
-  k_attn_fwd<D, TO><<<G * hq, 256, 0, st>>>(q, k, vt, L->seg_info, L->tile_seg, L->tok_meta,
-                                            L->qt_ptr, L->qt_col, L->qt_cls, L->work_order, hq,
-                                            hkv, L->window, scale * LOG2E, sz->packed_tokens,
-                                            static_cast<TO *>(o), lse);
+  k_attn_fwd2<D, TO><<<G * hq, 256, 0, st>>>(q, k, v, L->seg_info, L->tile_seg, L->tok_meta,
+                                             L->qt_ptr, L->qt_col, L->qt_cls, L->work_order, hq,
+                                             hkv, L->window, scale * LOG2E, sz->packed_tokens,
+                                             static_cast<TO *>(o), lse);
   SEG_LAUNCH_CHECK();
 }
 
@@ -676,8 +708,7 @@ template <int D, class TO, class TI>
 void bwd_impl(const seg_layout *L, const seg_sizes *sz, int hq, int hkv, float scale,
               const unsigned short *q, const unsigned short *k, const unsigned short *v,
               const unsigned short *dout, const TI *o_raw, const TI *dout_raw,
-              const float *lse, unsigned short *kt, unsigned short *qt, unsigned short *dot,
-              float *delta, void *dq, void *dk, void *dv, hipStream_t st) {
+              const float *lse, float *delta, void *dq, void *dk, void *dv, hipStream_t st) {
   const int G = sz->num_qtiles;
   const long P = sz->packed_tokens;
   {
@@ -686,20 +717,17 @@ void bwd_impl(const seg_layout *L, const seg_sizes *sz, int hq, int hkv, float s
     k_delta<TI, D><<<(int)((threads + 255) / 256), 256, 0, st>>>(o_raw, dout_raw, hq, P, delta);
     SEG_LAUNCH_CHECK();
   }
-  launch_transpose<unsigned short, D>(k, hkv, L, G, kt, st);
-  launch_transpose<unsigned short, D>(q, hq, L, G, qt, st);
-  launch_transpose<unsigned short, D>(dout, hq, L, G, dot, st);
   {
-  ProfScope prof("attn_bwd_dkdv", st);
-  k_attn_bwd_dkdv<D, TO><<<G * hkv, 256, 0, st>>>(
-      q, k, v, dout, qt, dot, lse, delta, L->seg_info, L->tile_seg, L->tok_meta, L->kt_ptr,
-      L->kt_row, L->kt_cls, hq, hkv, L->window, scale * LOG2E, scale, P,
-      static_cast<TO *>(dk), static_cast<TO *>(dv));
-  SEG_LAUNCH_CHECK();
+    ProfScope prof("attn_bwd_dkdv", st);
+    k_attn_bwd_dkdv2<D, TO><<<G * hkv, 256, 0, st>>>(
+        q, k, v, dout, lse, delta, L->seg_info, L->tile_seg, L->tok_meta, L->kt_ptr, L->kt_row,
+        L->kt_cls, hq, hkv, L->window, scale * LOG2E, scale, P, static_cast<TO *>(dk),
+        static_cast<TO *>(dv));
+    SEG_LAUNCH_CHECK();
   }
   ProfScope prof("attn_bwd_dq", st);
-  k_attn_bwd_dq<D, TO><<<G * hq, 256, 0, st>>>(
-      q, k, v, dout, kt, lse, delta, L->seg_info, L->tile_seg, L->tok_meta, L->qt_ptr, L->qt_col,
+  k_attn_bwd_dq2<D, TO><<<G * hq, 256, 0, st>>>(
+      q, k, v, dout, lse, delta, L->seg_info, L->tile_seg, L->tok_meta, L->qt_ptr, L->qt_col,
       L->qt_cls, L->work_order, hq, hkv, L->window, scale * LOG2E, scale, P,
       static_cast<TO *>(dq));
   SEG_LAUNCH_CHECK();
@@ -729,29 +757,29 @@ extern "C" seg_status seg_attn_fwd(const seg_layout *L, const seg_sizes *sz, seg
     SEG_CHECK(q && k && v && o && lse && ws, SEG_ERR_ARG, "a tensor pointer is NULL");
     SEG_CHECK(std::isfinite(softmax_scale), SEG_ERR_ARG, "softmax_scale is not finite");
     char *base = static_cast<char *>(ws);
-    const int G = sz->num_qtiles;
     const long P = sz->packed_tokens;
-    unsigned short *vt = reinterpret_cast<unsigned short *>(base + w.vt);
-    const unsigned short *qb, *kb;
+    const unsigned short *qb, *kb, *vb;
     if (dt == SEG_F32) {
       unsigned short *q2 = reinterpret_cast<unsigned short *>(base + w.qb);
       unsigned short *k2 = reinterpret_cast<unsigned short *>(base + w.kb);
+      unsigned short *v2 = reinterpret_cast<unsigned short *>(base + w.vb);
       to_bf16(q, q2, P * hq * d, stream);
       to_bf16(k, k2, P * hkv * d, stream);
-      transpose_any(d, static_cast<const float *>(v), hkv, L, G, vt, stream);
+      to_bf16(v, v2, P * hkv * d, stream);
       qb = q2;
       kb = k2;
+      vb = v2;
     } else {
-      transpose_any(d, static_cast<const unsigned short *>(v), hkv, L, G, vt, stream);
       qb = static_cast<const unsigned short *>(q);
       kb = static_cast<const unsigned short *>(k);
+      vb = static_cast<const unsigned short *>(v);
     }
     if (d == 128) {
-      if (dt == SEG_F32) fwd_impl<128, float>(L, sz, hq, hkv, softmax_scale, qb, kb, vt, o, lse, stream);
-      else fwd_impl<128, unsigned short>(L, sz, hq, hkv, softmax_scale, qb, kb, vt, o, lse, stream);
+      if (dt == SEG_F32) fwd_impl<128, float>(L, sz, hq, hkv, softmax_scale, qb, kb, vb, o, lse, stream);
+      else fwd_impl<128, unsigned short>(L, sz, hq, hkv, softmax_scale, qb, kb, vb, o, lse, stream);
     } else {
-      if (dt == SEG_F32) fwd_impl<64, float>(L, sz, hq, hkv, softmax_scale, qb, kb, vt, o, lse, stream);
-      else fwd_impl<64, unsigned short>(L, sz, hq, hkv, softmax_scale, qb, kb, vt, o, lse, stream);
+      if (dt == SEG_F32) fwd_impl<64, float>(L, sz, hq, hkv, softmax_scale, qb, kb, vb, o, lse, stream);
+      else fwd_impl<64, unsigned short>(L, sz, hq, hkv, softmax_scale, qb, kb, vb, o, lse, stream);
     }
   });
 }
@@ -772,11 +800,7 @@ extern "C" seg_status seg_attn_bwd(const seg_layout *L, const seg_sizes *sz, seg
     SEG_CHECK(std::isfinite(softmax_scale), SEG_ERR_ARG, "softmax_scale is not finite");
     char *base = static_cast<char *>(ws);
     const long P = sz->packed_tokens;
-    unsigned short *kt = reinterpret_cast<unsigned short *>(base + w.kt);
-    unsigned short *qt = reinterpret_cast<unsigned short *>(base + w.qt);
-    unsigned short *dot = reinterpret_cast<unsigned short *>(base + w.dot);
     float *delta = reinterpret_cast<float *>(base + w.delta);
-    const unsigned short *qb, *kb, *vb, *dob;
     if (dt == SEG_F32) {
       unsigned short *q2 = reinterpret_cast<unsigned short *>(base + w.qb);
       unsigned short *k2 = reinterpret_cast<unsigned short *>(base + w.kb);
@@ -786,28 +810,27 @@ extern "C" seg_status seg_attn_bwd(const seg_layout *L, const seg_sizes *sz, seg
       to_bf16(k, k2, P * hkv * d, stream);
       to_bf16(v, v2, P * hkv * d, stream);
       to_bf16(d_o, do2, P * hq * d, stream);
-      qb = q2; kb = k2; vb = v2; dob = do2;
       const float *o32 = static_cast<const float *>(o), *do32 = static_cast<const float *>(d_o);
       if (d == 128)
-        bwd_impl<128, float, float>(L, sz, hq, hkv, softmax_scale, qb, kb, vb, dob, o32, do32,
-                                    lse, kt, qt, dot, delta, dq, dk, dv, stream);
+        bwd_impl<128, float, float>(L, sz, hq, hkv, softmax_scale, q2, k2, v2, do2, o32, do32,
+                                    lse, delta, dq, dk, dv, stream);
       else
-        bwd_impl<64, float, float>(L, sz, hq, hkv, softmax_scale, qb, kb, vb, dob, o32, do32, lse,
-                                   kt, qt, dot, delta, dq, dk, dv, stream);
+        bwd_impl<64, float, float>(L, sz, hq, hkv, softmax_scale, q2, k2, v2, do2, o32, do32, lse,
+                                   delta, dq, dk, dv, stream);
     } else {
-      qb = static_cast<const unsigned short *>(q);
-      kb = static_cast<const unsigned short *>(k);
-      vb = static_cast<const unsigned short *>(v);
-      dob = static_cast<const unsigned short *>(d_o);
+      const unsigned short *qb = static_cast<const unsigned short *>(q);
+      const unsigned short *kb = static_cast<const unsigned short *>(k);
+      const unsigned short *vb = static_cast<const unsigned short *>(v);
+      const unsigned short *dob = static_cast<const unsigned short *>(d_o);
       const unsigned short *o16 = static_cast<const unsigned short *>(o);
       if (d == 128)
         bwd_impl<128, unsigned short, unsigned short>(L, sz, hq, hkv, softmax_scale, qb, kb, vb,
-                                                      dob, o16, dob, lse, kt, qt, dot, delta, dq,
-                                                      dk, dv, stream);
+                                                      dob, o16, dob, lse, delta, dq, dk, dv,
+                                                      stream);
       else
         bwd_impl<64, unsigned short, unsigned short>(L, sz, hq, hkv, softmax_scale, qb, kb, vb,
-                                                     dob, o16, dob, lse, kt, qt, dot, delta, dq,
-                                                     dk, dv, stream);
+                                                     dob, o16, dob, lse, delta, dq, dk, dv,
+                                                     stream);
     }
   });
 }
