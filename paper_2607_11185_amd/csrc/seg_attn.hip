@@ -14,6 +14,7 @@
 // their other operand from LDS through transpose reads in the same row order
 // (kperm() in common.h).
 #include <climits>
+#include <type_traits>
 #include <cmath>
 
 #include "common.h"
@@ -78,10 +79,12 @@ __global__ void k_f32_to_bf16(const float *__restrict__ x, unsigned short *__res
     y[i] = f2bf_bits(x[i]);
 }
 
-// Delta[h][row] = sum_d dO[row][h][d] * O[row][h][d]  (D/8 lanes per (row, head))
+// Delta[h][row] = sum_d dO[row][h][d] * O[row][h][d]  (D/8 lanes per (row, head)),
+// and the row's log-sum-exp in log2 units for the backward kernels.
 template <class TI, int D>
 __global__ void __launch_bounds__(256) k_delta(const TI *__restrict__ o, const TI *__restrict__ dout,
-                                               int hq, long P, float *__restrict__ delta) {
+                                               const float *__restrict__ lse, int hq, long P,
+                                               float *__restrict__ delta, float *__restrict__ lse2) {
   constexpr int LPR = D / 8;  // lanes per (row, head)
   const long gid = (long)blockIdx.x * 256 + threadIdx.x;
   const long pair = gid / LPR;
@@ -109,6 +112,7 @@ __global__ void __launch_bounds__(256) k_delta(const TI *__restrict__ o, const T
     const long row = pair / hq;
     const int h = (int)(pair % hq);
     delta[(long)h * P + row] = acc;
+    lse2[(long)h * P + row] = lse[(long)h * P + row] * LOG2E;
   }
 }
 
@@ -120,10 +124,14 @@ __global__ void __launch_bounds__(256) k_delta(const TI *__restrict__ o, const T
 // the current one.  Rows are stored with a 16-byte-chunk swizzle that keeps
 // both 16-byte row reads (MFMA operands contracting over d) and 4x16 transpose
 // reads (ds_read_b64_tr_b16: operands contracting over the rows) free of bank
-// conflicts, so no transposed copy of any tensor is needed.
+// conflicts, so no transposed copy of any tensor is needed.  Every lane's
+// swizzled offsets are computed once; inside the loops a read is a register
+// offset plus an immediate (row block and buffer are compile-time).
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 
 template <int D>
 __device__ __forceinline__ int swz(int row) {
@@ -131,58 +139,103 @@ __device__ __forceinline__ int swz(int row) {
   else return (((row >> 1) & 3) << 1) | ((row >> 3) & 1);
 }
 
+// element offset of (row, col) in a swizzled row-major tile of d columns
 template <int D>
 __device__ __forceinline__ int toff(int row, int col) {
-  return row * D + ((((col >> 3) ^ swz<D>(row))) << 3) + (col & 7);
+  return row * D + (((col >> 3) ^ swz<D>(row)) << 3) + (col & 7);
 }
 
-// 8 consecutive columns (16-byte chunk `chunk`) of row `row`
+// Per-lane byte offsets into a 64-row tile, valid for any row block R that is
+// a multiple of 16 (the swizzle depends on row % 16 only).
 template <int D>
-__device__ __forceinline__ bf16x8 ld_row8(const unsigned short *t, int row, int chunk) {
-  return *reinterpret_cast<const bf16x8 *>(t + row * D + ((chunk ^ swz<D>(row)) << 3));
+struct LaneOffsets {
+  static constexpr int KK = D / 16, DB = D / 32;
+  int row[KK];     // 16-byte read of row R + lane%32, chunk 2*kk + lane/32
+  int tra[DB];     // transpose reads: rows R + 4h + (lane%16)/4 (+8 for trb),
+  int trb[DB];     // columns nb0 + 32*db + 16*((lane/16)%2) + 4*(lane%4)
+  __device__ __forceinline__ void init(int lane, int nb0) {
+    const int col = lane & 31, hh = lane >> 5, l16 = lane & 15, g = lane >> 4;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) row[kk] = toff<D>(col, (kk * 2 + hh) * 8) * 2;
+    const int r = 4 * hh + (l16 >> 2);
+#pragma unroll
+    for (int db = 0; db < DB; ++db) {
+      const int c = nb0 + db * 32 + 16 * (g & 1) + 4 * (l16 & 3);
+      tra[db] = toff<D>(r, c) * 2;
+      trb[db] = toff<D>(r + 8, c) * 2;
+    }
+  }
+};
+
+template <int D>
+__device__ __forceinline__ bf16x8 frag_row(const char *tile, int R, int off) {
+  return *reinterpret_cast<const bf16x8 *>(tile + R * D * 2 + off);
 }
 
 // Operand fragment contracting over tile rows: lane l receives column
-// n_base + l%32 of rows base + kperm(8h + j), j = 0..7 (h = l/32), i.e. the
-// MFMA k-order used by accumulator-held operands.
+// n(l) of rows R + kperm(8h + j), j = 0..7 (h = l/32), the MFMA k-order of
+// accumulator-held operands.
 template <int D>
-__device__ __forceinline__ bf16x8 ld_tr8(const unsigned short *t, int base, int n_base, int lane) {
-  const int l16 = lane & 15, g = lane >> 4, h = lane >> 5;
-  const int row = base + 4 * h + (l16 >> 2);
-  const int col = n_base + 16 * (g & 1) + 4 * (l16 & 3);
-  const v4i16 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)(t + toff<D>(row, col)));
-  const v4i16 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)(t + toff<D>(row + 8, col)));
-  bf16x8 r;
+__device__ __forceinline__ bf16x8 frag_tr(const char *tile, int R, int offa, int offb) {
+  const v4i16 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)(tile + R * D * 2 + offa));
+  const v4i16 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)(tile + R * D * 2 + offb));
   const bf16x4 a4 = __builtin_bit_cast(bf16x4, a), b4 = __builtin_bit_cast(bf16x4, b);
+  bf16x8 r;
   r[0] = a4[0]; r[1] = a4[1]; r[2] = a4[2]; r[3] = a4[3];
   r[4] = b4[0]; r[5] = b4[1]; r[6] = b4[2]; r[7] = b4[3];
   return r;
 }
 
-// Fill a 64-row swizzled tile: tile row r comes from `base + rowoff(r)` (d
-// contiguous bf16).  4 waves, each issuing D/32 1-KB instructions.
-template <int D, class RowOff>
-__device__ __forceinline__ void fill64(unsigned short *tile, const unsigned short *base,
-                                       RowOff rowoff, int wave, int lane) {
-  constexpr int CPR = D / 8, PER_WAVE = 64 * CPR / 256;
+// Lane coordinates of a 64-row tile fill by NW waves (PW 1-KB loads each).
+template <int D, int NW>
+struct FillPlan {
+  static constexpr int CPR = D / 8, PW = 64 * CPR / (64 * NW);
+  static_assert(PW >= 1, "tile too small for the wave count");
+  int row[PW], chunk[PW];  // tile row and element offset of the lane's 16 bytes
+  __device__ __forceinline__ void init(int wave, int lane) {
 #pragma unroll
-  for (int i = 0; i < PER_WAVE; ++i) {
-    const int s0 = (wave * PER_WAVE + i) * 64;
-    const int s = s0 + lane;
-    const int row = s / CPR, ch = (s % CPR) ^ swz<D>(row);
-    __builtin_amdgcn_global_load_lds(base + rowoff(row) + ch * 8,
-                                     (__attribute__((address_space(3))) void *)(tile + s0 * 8), 16, 0, 0);
+    for (int i = 0; i < PW; ++i) {
+      const int s = (wave * PW + i) * 64 + lane;
+      row[i] = s / CPR;
+      chunk[i] = ((s % CPR) ^ swz<D>(row[i])) * 8;
+    }
   }
-}
+  // rows r0 + min(row, vrows - 1) of `base` (stride elements per row)
+  __device__ __forceinline__ void issue(unsigned short *tile, const unsigned short *base, long stride,
+                                        int r0, int vrows, int wave) const {
+    // device pass only: the host pass of clang drops the launch stub of a
+    // kernel that reaches this address-space cast
+#if defined(__HIP_DEVICE_COMPILE__)
+#pragma unroll
+    for (int i = 0; i < PW; ++i) {
+      const long r = r0 + min(row[i], vrows - 1);
+      __builtin_amdgcn_global_load_lds(
+          base + r * stride + chunk[i],
+          (__attribute__((address_space(3))) void *)(tile + (wave * PW + i) * 64 * 8), 16, 0, 0);
+    }
+#endif
+  }
+};
 
 // 64 consecutive 4-byte values (one per lane) into LDS
 __device__ __forceinline__ void fill64_dw(void *dst, const void *src_lane) {
+#if defined(__HIP_DEVICE_COMPILE__)
   __builtin_amdgcn_global_load_lds(src_lane, (__attribute__((address_space(3))) void *)dst, 4, 0, 0);
+#endif
 }
 
 __device__ __forceinline__ void wait_all_and_sync() {
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
+}
+
+// sum of 8 bf16 values (fp32 accumulation)
+__device__ __forceinline__ float sum8(const bf16x8 &v, float acc) {
+  const bf16x2 one = {(__bf16)1.f, (__bf16)1.f};
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    acc = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{v[2 * i], v[2 * i + 1]}, one, acc, false);
+  return acc;
 }
 
 // A unit of work: 64 rows (half of a 128-row tile) of the tile listed at CSR
@@ -221,9 +274,11 @@ __device__ __forceinline__ bool next_unit(const Unit &u, int e1, const int32_t *
 }
 
 // Forward: one block = one q-tile x one query head, 4 waves of 32 query rows;
-// units are 64-key halves of the listed k-tiles.
+// units are 64-key halves of the listed k-tiles.  S^T = K Q^T keeps one query
+// per lane, so the online softmax is in-lane (plus one exchange with the
+// other half-wave); O^T += V^T P^T with V^T by transpose reads.
 template <int D, class TO>
-__global__ void __launch_bounds__(256, 2) k_attn_fwd2(
+__global__ void __launch_bounds__(256, 2) k_attn_fwd(
     const unsigned short *__restrict__ q, const unsigned short *__restrict__ k,
     const unsigned short *__restrict__ v, const int32_t *__restrict__ seg_info,
     const int32_t *__restrict__ tile_seg, const int32_t *__restrict__ tok_meta,
@@ -256,84 +311,111 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd2(
   for (int db = 0; db < DB; ++db) oacc[db] = f32x16{};
   float m_run = -INFINITY, l_run = 0.f;
 
+  LaneOffsets<D> lo;
+  lo.init(lane, 0);
+  FillPlan<D, 4> fp;
+  fp.init(wave, lane);
   const long kv_stride = (long)hkv * D;
   const unsigned short *kbase = k + (long)hk * D + (long)tr.start * kv_stride;
   const unsigned short *vbase = v + (long)hk * D + (long)tr.start * kv_stride;
-  auto issue = [&](const Unit &u, int b) {
-    auto rowoff = [&](int r) { return (long)(u.r0 + min(r, u.vrows - 1)) * kv_stride; };
-    fill64<D>(smem + b * T64, kbase, rowoff, wave, lane);
-    fill64<D>(smem + (2 + b) * T64, vbase, rowoff, wave, lane);
+  const char *sbase = reinterpret_cast<const char *>(smem);
+
+  auto issue = [&](const Unit &u, const int b) __attribute__((always_inline)) {
+    fp.issue(smem + b * T64, kbase, kv_stride, u.r0, u.vrows, wave);
+    fp.issue(smem + (2 + b) * T64, vbase, kv_stride, u.r0, u.vrows, wave);
     if (wave == 0) fill64_dw(&sMeta[b][0], tok_meta + tr.start + u.r0 + min(lane, u.vrows - 1));
   };
-
-  const int e0 = qt_ptr[g], e1 = qt_ptr[g + 1];
-  Unit u = make_unit(qt_col, qt_cls, e0, 0, tr.qbase, tr.len);
-  issue(u, 0);
-  wait_all_and_sync();
-  int b = 0;
-  for (;;) {
-    Unit nu;
-    const bool more = next_unit(u, e1, qt_col, qt_cls, tr.qbase, tr.len, nu);
-    if (more) issue(nu, b ^ 1);
-    const unsigned short *sK = smem + b * T64, *sV = smem + (2 + b) * T64;
+  auto compute = [&](const Unit &u, const int b) __attribute__((always_inline)) {
+    const char *sK = sbase + b * T64 * 2, *sV = sbase + (2 + b) * T64 * 2;
     f32x16 sacc[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       bf16x8 ak[KK];
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) ak[kk] = ld_row8<D>(sK, kb * 32 + col, kk * 2 + hh);
+      for (int kk = 0; kk < KK; ++kk) ak[kk] = frag_row<D>(sK, kb * 32, lo.row[kk]);
       sacc[kb] = f32x16{};
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) sacc[kb] = mfma32(ak[kk], qf[kk], sacc[kb]);
+    }
+    // raw scores; masked entries -inf (scale > 0 keeps the order)
+    if (u.partial) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int rg = 0; rg < 4; ++rg) {
+          const int kb0 = kb * 32 + 8 * rg + 4 * hh;
+          const i32x4 M4 = *reinterpret_cast<const i32x4 *>(&sMeta[b][kb0]);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int key = kb0 + j;
+            const bool vis = qvalid && key < u.vrows && (u.r0 + key <= qr) &&
+                             (qstep < key_expiry(M4[j], W));
+            sacc[kb][rg * 4 + j] = vis ? sacc[kb][rg * 4 + j] : -INFINITY;
+          }
+        }
     }
     float mloc = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float sv = sacc[kb][r] * scale_log2;
-        if (u.partial) {
-          const int key = kb * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-          const bool vis = qvalid && key < u.vrows && (u.r0 + key <= qr) &&
-                           (qstep < key_expiry(sMeta[b][key], W));
-          sv = vis ? sv : -INFINITY;
-        }
-        sacc[kb][r] = sv;
-        mloc = fmaxf(mloc, sv);
-      }
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-    const float m_new = fmaxf(m_run, mloc);
-    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    const float alpha = exp2f(m_run - m_use);
+      for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, sacc[kb][r]);
+    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64)) * scale_log2;
+    // Lazy rescaling: the running max (log2 units) only moves when a row's
+    // tile max exceeds it by more than 8, so unnormalised P stays below 2^8.
+    const bool grow = mloc > m_run + 8.f;
+    if (__any(grow)) {
+      const float m_new = grow ? mloc : m_run;
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
+      m_run = m_new;
+    }
+    const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
+    bf16x8 pf[2][2];
     float rsum = 0.f;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float pv = exp2f(sacc[kb][r] - m_use);
-        sacc[kb][r] = pv;
-        rsum += pv;
-      }
+      for (int r = 0; r < 16; ++r)
+        sacc[kb][r] = __builtin_amdgcn_exp2f(fmaf(sacc[kb][r], scale_log2, -m_use));
+      pf[kb][0] = pack8(sacc[kb], 0);
+      pf[kb][1] = pack8(sacc[kb], 8);
+      rsum = sum8(pf[kb][0], rsum);
+      rsum = sum8(pf[kb][1], rsum);
+    }
     rsum += __shfl_xor(rsum, 32, 64);
-    l_run = l_run * alpha + rsum;
-    m_run = m_new;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
+    l_run += rsum;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int c2 = 0; c2 < 2; ++c2) {
         bf16x8 av[DB];
 #pragma unroll
-        for (int db = 0; db < DB; ++db) av[db] = ld_tr8<D>(sV, kb * 32 + c2 * 16, db * 32, lane);
-        const bf16x8 pf = pack8(sacc[kb], c2 * 8);
+        for (int db = 0; db < DB; ++db)
+          av[db] = frag_tr<D>(sV, kb * 32 + c2 * 16, lo.tra[db], lo.trb[db]);
 #pragma unroll
-        for (int db = 0; db < DB; ++db) oacc[db] = mfma32(av[db], pf, oacc[db]);
+        for (int db = 0; db < DB; ++db) oacc[db] = mfma32(av[db], pf[kb][c2], oacc[db]);
       }
+  };
+
+  const int e0 = qt_ptr[g], e1 = qt_ptr[g + 1];
+  Unit u = make_unit(qt_col, qt_cls, e0, 0, tr.qbase, tr.len), nu;
+  issue(u, 0);
+  wait_all_and_sync();
+  for (;;) {
+    bool more = next_unit(u, e1, qt_col, qt_cls, tr.qbase, tr.len, nu);
+    if (more) issue(nu, 1);
+    compute(u, 0);
     wait_all_and_sync();
     if (!more) break;
     u = nu;
-    b ^= 1;
+    more = next_unit(u, e1, qt_col, qt_cls, tr.qbase, tr.len, nu);
+    if (more) issue(nu, 0);
+    compute(u, 1);
+    wait_all_and_sync();
+    if (!more) break;
+    u = nu;
   }
 
   if (qvalid) {
@@ -352,23 +434,31 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd2(
   }
 }
 
-// dK/dV: one block = one k-tile x one kv head; wave w owns keys 32w..32w+31
-// (K and V fragments stay in registers).  Units are 64-row halves of the
-// listed q-tiles, for every query head of the group.
+// dK/dV with the head dimension split over wave pairs: one block = one
+// k-tile x one kv head, 8 waves (two per SIMD).  Wave w serves keys
+// 32*(w%4)..+31; waves 0-3 hold K fragments and compute S and P, waves 4-7
+// hold V fragments and compute dP and dS; P and dS are exchanged through LDS
+// and each wave accumulates dK and dV for one half of the head dimension.
+// S = Q K^T keeps queries on accumulator rows, so P and dS feed
+// dV += P^T dO and dK += dS^T Q directly (dO^T, Q^T by transpose reads).
+// Units are 64-row halves of the listed q-tiles, for every query head of the
+// group; no atomics.
 template <int D, class TO>
-__global__ void __launch_bounds__(256, 1) k_attn_bwd_dkdv2(
+__global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
     const unsigned short *__restrict__ q, const unsigned short *__restrict__ k,
     const unsigned short *__restrict__ v, const unsigned short *__restrict__ dout,
-    const float *__restrict__ lse, const float *__restrict__ delta,
+    const float *__restrict__ lse2, const float *__restrict__ delta,
     const int32_t *__restrict__ seg_info, const int32_t *__restrict__ tile_seg,
     const int32_t *__restrict__ tok_meta, const int32_t *__restrict__ kt_ptr,
     const int32_t *__restrict__ kt_row, const uint8_t *__restrict__ kt_cls, int hq, int hkv,
     int W, float scale_log2, float scale, long P, TO *__restrict__ dk, TO *__restrict__ dv) {
-  constexpr int KK = D / 16, DB = D / 32, T64 = 64 * D;
+  constexpr int KK = D / 16, T64 = 64 * D, DH = D / 2, DBH = DH / 32;
   __shared__ __attribute__((aligned(16))) unsigned short smem[4 * T64];  // Q[2], dO[2]
   __shared__ __attribute__((aligned(16))) float sLse[2][64];
   __shared__ __attribute__((aligned(16))) float sDel[2][64];
   __shared__ __attribute__((aligned(16))) int sMeta[2][64];
+  __shared__ __attribute__((aligned(16))) f32x4 xP[2][4][4][64];     // [qb][key group][quarter][lane]
+  __shared__ __attribute__((aligned(16))) bf16x8 xdS[2][4][2][64];   // [qb][key group][c][lane]
 
   const int g = blockIdx.x / hkv;
   const int hk = blockIdx.x % hkv;
@@ -376,147 +466,186 @@ __global__ void __launch_bounds__(256, 1) k_attn_bwd_dkdv2(
   const TileRows tr = tile_rows(seg_info, tile_seg, g);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int col = lane & 31, hh = lane >> 5;
-  const int kloc = wave * 32 + col;
+  const int kg = wave & 3, role = wave >> 2;
+  const int kloc = kg * 32 + col;
   const bool kvalid = kloc < tr.nrows;
   const int kr = tr.row0 + (kvalid ? kloc : 0);
   const int kexp = key_expiry(tok_meta[tr.start + kr], W);
 
-  bf16x8 kf[KK], vf[KK];
+  bf16x8 kv_f[KK];  // K fragments (role 0) or V fragments (role 1)
   {
     const long row = tr.start + kr;
-    const unsigned short *krow = k + (row * hkv + hk) * D;
-    const unsigned short *vrow = v + (row * hkv + hk) * D;
+    const unsigned short *src = (role == 0 ? k : v) + (row * hkv + hk) * D;
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      kf[kk] = lds8(krow + kk * 16 + hh * 8);
-      vf[kk] = lds8(vrow + kk * 16 + hh * 8);
-    }
+    for (int kk = 0; kk < KK; ++kk) kv_f[kk] = lds8(src + kk * 16 + hh * 8);
   }
-  f32x16 dkacc[DB], dvacc[DB];
+  f32x16 dkacc[DBH], dvacc[DBH];
 #pragma unroll
-  for (int db = 0; db < DB; ++db) {
+  for (int db = 0; db < DBH; ++db) {
     dkacc[db] = f32x16{};
     dvacc[db] = f32x16{};
   }
 
+  LaneOffsets<D> lo;
+  lo.init(lane, role * DH);
+  FillPlan<D, 8> fp;
+  fp.init(wave, lane);
   const long q_stride = (long)hq * D;
+  const char *sbase = reinterpret_cast<const char *>(smem);
   const int e0 = kt_ptr[g], e1 = kt_ptr[g + 1];
-  // unit = (entry e, head index hi, half); heads vary fastest after halves
-  auto issue = [&](const Unit &u, int hi, int b) {
+
+  auto issue = [&](const Unit &u, int hi, const int b) __attribute__((always_inline)) {
     const int h = hk * grp + hi;
-    const unsigned short *qb = q + (long)h * D + (long)tr.start * q_stride;
-    const unsigned short *db_ = dout + (long)h * D + (long)tr.start * q_stride;
-    auto rowoff = [&](int r) { return (long)(u.r0 + min(r, u.vrows - 1)) * q_stride; };
-    fill64<D>(smem + b * T64, qb, rowoff, wave, lane);
-    fill64<D>(smem + (2 + b) * T64, db_, rowoff, wave, lane);
+    fp.issue(smem + b * T64, q + (long)h * D + (long)tr.start * q_stride, q_stride, u.r0, u.vrows,
+             wave);
+    fp.issue(smem + (2 + b) * T64, dout + (long)h * D + (long)tr.start * q_stride, q_stride, u.r0,
+             u.vrows, wave);
     const long lrow = tr.start + u.r0 + min(lane, u.vrows - 1);
-    if (wave == 0) fill64_dw(&sLse[b][0], lse + (long)h * P + lrow);
+    if (wave == 0) fill64_dw(&sLse[b][0], lse2 + (long)h * P + lrow);
     if (wave == 1) fill64_dw(&sDel[b][0], delta + (long)h * P + lrow);
     if (wave == 2) fill64_dw(&sMeta[b][0], tok_meta + lrow);
   };
-
-  if (e0 < e1) {
-    Unit u = make_unit(kt_row, kt_cls, e0, 0, tr.qbase, tr.len);
-    int hi = 0;
-    issue(u, hi, 0);
-    wait_all_and_sync();
-    int b = 0;
-    for (;;) {
-      // next unit: other half of this tile, else next head, else next entry
-      Unit nu = u;
-      int nhi = hi;
-      bool more = true;
-      if (u.half == 0 && u.r0 + 64 < tr.len) {
-        nu = make_unit(kt_row, kt_cls, u.e, 1, tr.qbase, tr.len);
-      } else if (hi + 1 < grp) {
-        nu = make_unit(kt_row, kt_cls, u.e, 0, tr.qbase, tr.len);
-        nhi = hi + 1;
-      } else if (u.e + 1 < e1) {
-        nu = make_unit(kt_row, kt_cls, u.e + 1, 0, tr.qbase, tr.len);
-        nhi = 0;
-      } else {
-        more = false;
-      }
-      if (more) issue(nu, nhi, b ^ 1);
-
-      const unsigned short *sQ = smem + b * T64, *sdO = smem + (2 + b) * T64;
+  auto compute = [&](const Unit &u, const int b) __attribute__((always_inline)) {
+    const char *sQ = sbase + b * T64 * 2, *sdO = sbase + (2 + b) * T64 * 2;
+    const char *sA = role == 0 ? sQ : sdO;  // S-role reads Q, dP-role reads dO
+    const int nqb = (u.vrows + 31) >> 5;
 #pragma unroll
-      for (int qb = 0; qb < 2; ++qb) {
-        if (qb * 32 >= u.vrows) break;
-        bf16x8 aq[KK], ad[KK];
+    for (int qb = 0; qb < 2; ++qb) {
+      if (qb >= nqb) break;
+      // phase 1: S (role 0) or dP (role 1), queries on accumulator rows
+      bf16x8 af[KK];
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-          aq[kk] = ld_row8<D>(sQ, qb * 32 + col, kk * 2 + hh);
-          ad[kk] = ld_row8<D>(sdO, qb * 32 + col, kk * 2 + hh);
-        }
-        f32x16 s = f32x16{}, dp = f32x16{};
+      for (int kk = 0; kk < KK; ++kk) af[kk] = frag_row<D>(sA, qb * 32, lo.row[kk]);
+      f32x16 acc = f32x16{};
 #pragma unroll
-        for (int kk = 0; kk < KK; ++kk) {
-          s = mfma32(aq[kk], kf[kk], s);
-          dp = mfma32(ad[kk], vf[kk], dp);
-        }
+      for (int kk = 0; kk < KK; ++kk) acc = mfma32(af[kk], kv_f[kk], acc);
+      bf16x8 pa[2], dsa[2];
+      if (role == 0) {
 #pragma unroll
         for (int rg = 0; rg < 4; ++rg) {
           const int base = qb * 32 + 8 * rg + 4 * hh;
           const f32x4 L4 = *reinterpret_cast<const f32x4 *>(&sLse[b][base]);
-          const f32x4 D4 = *reinterpret_cast<const f32x4 *>(&sDel[b][base]);
-          typedef int i32x4 __attribute__((ext_vector_type(4)));
           const i32x4 M4 = *reinterpret_cast<const i32x4 *>(&sMeta[b][base]);
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const int r = rg * 4 + j, ql = base + j;
-            float pv = exp2f(s[r] * scale_log2 - L4[j] * LOG2E);
+            const float pv = __builtin_amdgcn_exp2f(fmaf(acc[r], scale_log2, -L4[j]));
             bool vis = kvalid && ql < u.vrows;
             if (u.partial) vis = vis && (kr <= u.r0 + ql) && ((M4[j] >> 2) < kexp);
-            pv = vis ? pv : 0.f;
-            s[r] = pv;
-            dp[r] = pv * (dp[r] - D4[j]);
+            acc[r] = vis ? pv : 0.f;
           }
+          xP[qb][kg][rg][lane] = f32x4{acc[rg * 4], acc[rg * 4 + 1], acc[rg * 4 + 2], acc[rg * 4 + 3]};
         }
-#pragma unroll
-        for (int c2 = 0; c2 < 2; ++c2) {
-          bf16x8 bo[DB], bq[DB];
-#pragma unroll
-          for (int db = 0; db < DB; ++db) {
-            bo[db] = ld_tr8<D>(sdO, qb * 32 + c2 * 16, db * 32, lane);
-            bq[db] = ld_tr8<D>(sQ, qb * 32 + c2 * 16, db * 32, lane);
-          }
-          const bf16x8 pa = pack8(s, c2 * 8);
-          const bf16x8 dsa = pack8(dp, c2 * 8);
-#pragma unroll
-          for (int db = 0; db < DB; ++db) {
-            dvacc[db] = mfma32(pa, bo[db], dvacc[db]);
-            dkacc[db] = mfma32(dsa, bq[db], dkacc[db]);
-          }
-        }
+        pa[0] = pack8(acc, 0);
+        pa[1] = pack8(acc, 8);
       }
+      __syncthreads();
+      if (role == 1) {
+        f32x16 pv;
+#pragma unroll
+        for (int rg = 0; rg < 4; ++rg) {
+          const f32x4 p4 = xP[qb][kg][rg][lane];
+          const f32x4 D4 = *reinterpret_cast<const f32x4 *>(&sDel[b][qb * 32 + 8 * rg + 4 * hh]);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            pv[rg * 4 + j] = p4[j];
+            acc[rg * 4 + j] = p4[j] * (acc[rg * 4 + j] - D4[j]);
+          }
+        }
+        pa[0] = pack8(pv, 0);
+        pa[1] = pack8(pv, 8);
+        dsa[0] = pack8(acc, 0);
+        dsa[1] = pack8(acc, 8);
+        xdS[qb][kg][0][lane] = dsa[0];
+        xdS[qb][kg][1][lane] = dsa[1];
+      }
+      // dV half += P^T dO[:, half]  (role 0 while role 1 forms dS)
+#pragma unroll
+      for (int c2 = 0; c2 < 2; ++c2) {
+        bf16x8 bo[DBH];
+#pragma unroll
+        for (int db = 0; db < DBH; ++db)
+          bo[db] = frag_tr<D>(sdO, qb * 32 + c2 * 16, lo.tra[db], lo.trb[db]);
+#pragma unroll
+        for (int db = 0; db < DBH; ++db) dvacc[db] = mfma32(pa[c2], bo[db], dvacc[db]);
+      }
+      __syncthreads();
+      if (role == 0) {
+        dsa[0] = xdS[qb][kg][0][lane];
+        dsa[1] = xdS[qb][kg][1][lane];
+      }
+      // dK half += dS^T Q[:, half]
+#pragma unroll
+      for (int c2 = 0; c2 < 2; ++c2) {
+        bf16x8 bq[DBH];
+#pragma unroll
+        for (int db = 0; db < DBH; ++db)
+          bq[db] = frag_tr<D>(sQ, qb * 32 + c2 * 16, lo.tra[db], lo.trb[db]);
+#pragma unroll
+        for (int db = 0; db < DBH; ++db) dkacc[db] = mfma32(dsa[c2], bq[db], dkacc[db]);
+      }
+    }
+  };
+
+  if (e0 < e1) {
+    Unit u = make_unit(kt_row, kt_cls, e0, 0, tr.qbase, tr.len), nu;
+    int hi = 0, nhi = 0;
+    // next unit: other half of this tile, else next head, else next entry
+    auto advance = [&](const Unit &cu, int chi, Unit &n, int &nh) __attribute__((always_inline)) -> bool {
+      if (cu.half == 0 && cu.r0 + 64 < tr.len) {
+        n = make_unit(kt_row, kt_cls, cu.e, 1, tr.qbase, tr.len);
+        nh = chi;
+      } else if (chi + 1 < grp) {
+        n = make_unit(kt_row, kt_cls, cu.e, 0, tr.qbase, tr.len);
+        nh = chi + 1;
+      } else if (cu.e + 1 < e1) {
+        n = make_unit(kt_row, kt_cls, cu.e + 1, 0, tr.qbase, tr.len);
+        nh = 0;
+      } else {
+        return false;
+      }
+      return true;
+    };
+    issue(u, hi, 0);
+    wait_all_and_sync();
+    for (;;) {
+      bool more = advance(u, hi, nu, nhi);
+      if (more) issue(nu, nhi, 1);
+      compute(u, 0);
       wait_all_and_sync();
       if (!more) break;
       u = nu;
       hi = nhi;
-      b ^= 1;
+      more = advance(u, hi, nu, nhi);
+      if (more) issue(nu, nhi, 0);
+      compute(u, 1);
+      wait_all_and_sync();
+      if (!more) break;
+      u = nu;
+      hi = nhi;
     }
   }
 
   // stage through LDS for coalesced stores; accumulator D[i = key][j = d]
-  TO *st = reinterpret_cast<TO *>(smem);  // [128][D] of TO (fits: 4 * 64 * D * 2 bytes)
-  constexpr int CH = 16 / sizeof(TO);     // elements per 16-byte chunk
+  TO *st = reinterpret_cast<TO *>(smem);  // [128][D] of TO
+  constexpr int CH = 16 / sizeof(TO);
 #pragma unroll
   for (int which = 0; which < 2; ++which) {
 #pragma unroll
-    for (int db = 0; db < DB; ++db)
+    for (int db = 0; db < DBH; ++db)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int kl = wave * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+        const int kl = kg * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
         const float val = which == 0 ? dkacc[db][r] * scale : dvacc[db][r];
+        const int dd = role * DH + db * 32 + col;
         if constexpr (sizeof(TO) == 2)
-          st[kl * D + db * 32 + col] = f2bf_bits(val);
+          st[kl * D + dd] = f2bf_bits(val);
         else
-          st[kl * D + db * 32 + col] = val;
+          st[kl * D + dd] = val;
       }
     __syncthreads();
     TO *dst = which == 0 ? dk : dv;
-    for (int c = threadIdx.x; c < TQ * D / CH; c += 256) {
+    for (int c = threadIdx.x; c < TQ * D / CH; c += 512) {
       const int kl = c / (D / CH), ch = c % (D / CH);
       if (kl < tr.nrows) {
         const long row = tr.start + tr.row0 + kl;
@@ -529,13 +658,13 @@ __global__ void __launch_bounds__(256, 1) k_attn_bwd_dkdv2(
 }
 
 // dQ: one block = one q-tile x one query head, 4 waves of 32 query rows;
-// units are 64-key halves of the listed k-tiles.  dQ^T += K^T dS^T with K^T
-// read transposed from the row-major K tile.
+// units are 64-key halves of the listed k-tiles.  Recomputes S^T and dP^T per
+// unit; dQ^T += K^T dS^T with K^T by transpose reads.
 template <int D, class TO>
-__global__ void __launch_bounds__(256, 2) k_attn_bwd_dq2(
+__global__ void __launch_bounds__(256, 2) k_attn_bwd_dq(
     const unsigned short *__restrict__ q, const unsigned short *__restrict__ k,
     const unsigned short *__restrict__ v, const unsigned short *__restrict__ dout,
-    const float *__restrict__ lse, const float *__restrict__ delta,
+    const float *__restrict__ lse2, const float *__restrict__ delta,
     const int32_t *__restrict__ seg_info, const int32_t *__restrict__ tile_seg,
     const int32_t *__restrict__ tok_meta, const int32_t *__restrict__ qt_ptr,
     const int32_t *__restrict__ qt_col, const uint8_t *__restrict__ qt_cls,
@@ -556,7 +685,7 @@ __global__ void __launch_bounds__(256, 2) k_attn_bwd_dq2(
   const int qr = tr.row0 + (qvalid ? qloc : 0);
   const long qrow_abs = tr.start + qr;
   const int qstep = tok_meta[qrow_abs] >> 2;
-  const float lse2 = lse[(long)h * P + qrow_abs] * LOG2E;
+  const float l2 = lse2[(long)h * P + qrow_abs];
   const float dlt = delta[(long)h * P + qrow_abs];
 
   bf16x8 qf[KK], df[KK];
@@ -573,34 +702,30 @@ __global__ void __launch_bounds__(256, 2) k_attn_bwd_dq2(
 #pragma unroll
   for (int db = 0; db < DB; ++db) dqacc[db] = f32x16{};
 
+  LaneOffsets<D> lo;
+  lo.init(lane, 0);
+  FillPlan<D, 4> fp;
+  fp.init(wave, lane);
   const long kv_stride = (long)hkv * D;
   const unsigned short *kbase = k + (long)hk * D + (long)tr.start * kv_stride;
   const unsigned short *vbase = v + (long)hk * D + (long)tr.start * kv_stride;
-  auto issue = [&](const Unit &u, int b) {
-    auto rowoff = [&](int r) { return (long)(u.r0 + min(r, u.vrows - 1)) * kv_stride; };
-    fill64<D>(smem + b * T64, kbase, rowoff, wave, lane);
-    fill64<D>(smem + (2 + b) * T64, vbase, rowoff, wave, lane);
+  const char *sbase = reinterpret_cast<const char *>(smem);
+
+  auto issue = [&](const Unit &u, const int b) __attribute__((always_inline)) {
+    fp.issue(smem + b * T64, kbase, kv_stride, u.r0, u.vrows, wave);
+    fp.issue(smem + (2 + b) * T64, vbase, kv_stride, u.r0, u.vrows, wave);
     if (wave == 0) fill64_dw(&sMeta[b][0], tok_meta + tr.start + u.r0 + min(lane, u.vrows - 1));
   };
-
-  const int e0 = qt_ptr[g], e1 = qt_ptr[g + 1];
-  Unit u = make_unit(qt_col, qt_cls, e0, 0, tr.qbase, tr.len);
-  issue(u, 0);
-  wait_all_and_sync();
-  int b = 0;
-  for (;;) {
-    Unit nu;
-    const bool more = next_unit(u, e1, qt_col, qt_cls, tr.qbase, tr.len, nu);
-    if (more) issue(nu, b ^ 1);
-    const unsigned short *sK = smem + b * T64, *sV = smem + (2 + b) * T64;
+  auto compute = [&](const Unit &u, const int b) __attribute__((always_inline)) {
+    const char *sK = sbase + b * T64 * 2, *sV = sbase + (2 + b) * T64 * 2;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       if (kb * 32 >= u.vrows) break;
       bf16x8 ak[KK], av[KK];
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
-        ak[kk] = ld_row8<D>(sK, kb * 32 + col, kk * 2 + hh);
-        av[kk] = ld_row8<D>(sV, kb * 32 + col, kk * 2 + hh);
+        ak[kk] = frag_row<D>(sK, kb * 32, lo.row[kk]);
+        av[kk] = frag_row<D>(sV, kb * 32, lo.row[kk]);
       }
       f32x16 s = f32x16{}, dp = f32x16{};
 #pragma unroll
@@ -609,28 +734,48 @@ __global__ void __launch_bounds__(256, 2) k_attn_bwd_dq2(
         dp = mfma32(av[kk], df[kk], dp);
       }
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int kl = kb * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-        float pv = exp2f(s[r] * scale_log2 - lse2);
-        bool vis = qvalid && kl < u.vrows;
-        if (u.partial) vis = vis && (u.r0 + kl <= qr) && (qstep < key_expiry(sMeta[b][kl], W));
-        pv = vis ? pv : 0.f;
-        s[r] = pv * (dp[r] - dlt);
+      for (int rg = 0; rg < 4; ++rg) {
+        const int kb0 = kb * 32 + 8 * rg + 4 * hh;
+        const i32x4 M4 = *reinterpret_cast<const i32x4 *>(&sMeta[b][kb0]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int r = rg * 4 + j, kl = kb0 + j;
+          const float pv = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -l2));
+          bool vis = qvalid && kl < u.vrows;
+          if (u.partial) vis = vis && (u.r0 + kl <= qr) && (qstep < key_expiry(M4[j], W));
+          s[r] = vis ? pv * (dp[r] - dlt) : 0.f;
+        }
       }
 #pragma unroll
       for (int c2 = 0; c2 < 2; ++c2) {
         bf16x8 kt[DB];
 #pragma unroll
-        for (int db = 0; db < DB; ++db) kt[db] = ld_tr8<D>(sK, kb * 32 + c2 * 16, db * 32, lane);
+        for (int db = 0; db < DB; ++db)
+          kt[db] = frag_tr<D>(sK, kb * 32 + c2 * 16, lo.tra[db], lo.trb[db]);
         const bf16x8 dsb = pack8(s, c2 * 8);
 #pragma unroll
         for (int db = 0; db < DB; ++db) dqacc[db] = mfma32(kt[db], dsb, dqacc[db]);
       }
     }
+  };
+
+  const int e0 = qt_ptr[g], e1 = qt_ptr[g + 1];
+  Unit u = make_unit(qt_col, qt_cls, e0, 0, tr.qbase, tr.len), nu;
+  issue(u, 0);
+  wait_all_and_sync();
+  for (;;) {
+    bool more = next_unit(u, e1, qt_col, qt_cls, tr.qbase, tr.len, nu);
+    if (more) issue(nu, 1);
+    compute(u, 0);
     wait_all_and_sync();
     if (!more) break;
     u = nu;
-    b ^= 1;
+    more = next_unit(u, e1, qt_col, qt_cls, tr.qbase, tr.len, nu);
+    if (more) issue(nu, 0);
+    compute(u, 1);
+    wait_all_and_sync();
+    if (!more) break;
+    u = nu;
   }
 
   if (qvalid) {
@@ -649,7 +794,7 @@ __global__ void __launch_bounds__(256, 2) k_attn_bwd_dq2(
 // ------------------------------------------------------------- host side
 
 struct AttnWs {
-  size_t delta, qb, kb, vb, dob, total;
+  size_t delta, lse2, qb, kb, vb, dob, total;
 };
 
 AttnWs attn_ws(const seg_sizes &sz, seg_dtype dt, int hq, int hkv, int d, int bwd) {
@@ -661,7 +806,10 @@ AttnWs attn_ws(const seg_sizes &sz, seg_dtype dt, int hq, int hkv, int d, int bw
     return o;
   };
   const size_t P = (size_t)std::max<int64_t>(1, sz.packed_tokens);
-  if (bwd) w.delta = take(P * hq * sizeof(float));
+  if (bwd) {
+    w.delta = take(P * hq * sizeof(float));
+    w.lse2 = take(P * hq * sizeof(float));
+  }
   if (dt == SEG_F32) {
     w.qb = take(P * hq * d * 2);
     w.kb = take(P * hkv * d * 2);
@@ -697,7 +845,7 @@ void fwd_impl(const seg_layout *L, const seg_sizes *sz, int hq, int hkv, float s
               float *lse, hipStream_t st) {
   const int G = sz->num_qtiles;
   ProfScope prof("attn_fwd", st);
-  k_attn_fwd2<D, TO><<<G * hq, 256, 0, st>>>(q, k, v, L->seg_info, L->tile_seg, L->tok_meta,
+  k_attn_fwd<D, TO><<<G * hq, 256, 0, st>>>(q, k, v, L->seg_info, L->tile_seg, L->tok_meta,
                                              L->qt_ptr, L->qt_col, L->qt_cls, L->work_order, hq,
                                              hkv, L->window, scale * LOG2E, sz->packed_tokens,
                                              static_cast<TO *>(o), lse);
@@ -708,26 +856,28 @@ template <int D, class TO, class TI>
 void bwd_impl(const seg_layout *L, const seg_sizes *sz, int hq, int hkv, float scale,
               const unsigned short *q, const unsigned short *k, const unsigned short *v,
               const unsigned short *dout, const TI *o_raw, const TI *dout_raw,
-              const float *lse, float *delta, void *dq, void *dk, void *dv, hipStream_t st) {
+              const float *lse, float *delta, float *lse2, void *dq, void *dk, void *dv,
+              hipStream_t st) {
   const int G = sz->num_qtiles;
   const long P = sz->packed_tokens;
   {
     const long threads = P * hq * (D / 8);
     ProfScope prof("attn_delta", st);
-    k_delta<TI, D><<<(int)((threads + 255) / 256), 256, 0, st>>>(o_raw, dout_raw, hq, P, delta);
+    k_delta<TI, D><<<(int)((threads + 255) / 256), 256, 0, st>>>(o_raw, dout_raw, lse, hq, P, delta,
+                                                                 lse2);
     SEG_LAUNCH_CHECK();
   }
   {
     ProfScope prof("attn_bwd_dkdv", st);
-    k_attn_bwd_dkdv2<D, TO><<<G * hkv, 256, 0, st>>>(
-        q, k, v, dout, lse, delta, L->seg_info, L->tile_seg, L->tok_meta, L->kt_ptr, L->kt_row,
+    k_attn_bwd_dkdv<D, TO><<<G * hkv, 512, 0, st>>>(
+        q, k, v, dout, lse2, delta, L->seg_info, L->tile_seg, L->tok_meta, L->kt_ptr, L->kt_row,
         L->kt_cls, hq, hkv, L->window, scale * LOG2E, scale, P, static_cast<TO *>(dk),
         static_cast<TO *>(dv));
     SEG_LAUNCH_CHECK();
   }
   ProfScope prof("attn_bwd_dq", st);
-  k_attn_bwd_dq2<D, TO><<<G * hq, 256, 0, st>>>(
-      q, k, v, dout, lse, delta, L->seg_info, L->tile_seg, L->tok_meta, L->qt_ptr, L->qt_col,
+  k_attn_bwd_dq<D, TO><<<G * hq, 256, 0, st>>>(
+      q, k, v, dout, lse2, delta, L->seg_info, L->tile_seg, L->tok_meta, L->qt_ptr, L->qt_col,
       L->qt_cls, L->work_order, hq, hkv, L->window, scale * LOG2E, scale, P,
       static_cast<TO *>(dq));
   SEG_LAUNCH_CHECK();
@@ -801,6 +951,7 @@ extern "C" seg_status seg_attn_bwd(const seg_layout *L, const seg_sizes *sz, seg
     char *base = static_cast<char *>(ws);
     const long P = sz->packed_tokens;
     float *delta = reinterpret_cast<float *>(base + w.delta);
+    float *lse2 = reinterpret_cast<float *>(base + w.lse2);
     if (dt == SEG_F32) {
       unsigned short *q2 = reinterpret_cast<unsigned short *>(base + w.qb);
       unsigned short *k2 = reinterpret_cast<unsigned short *>(base + w.kb);
@@ -813,10 +964,10 @@ extern "C" seg_status seg_attn_bwd(const seg_layout *L, const seg_sizes *sz, seg
       const float *o32 = static_cast<const float *>(o), *do32 = static_cast<const float *>(d_o);
       if (d == 128)
         bwd_impl<128, float, float>(L, sz, hq, hkv, softmax_scale, q2, k2, v2, do2, o32, do32,
-                                    lse, delta, dq, dk, dv, stream);
+                                    lse, delta, lse2, dq, dk, dv, stream);
       else
         bwd_impl<64, float, float>(L, sz, hq, hkv, softmax_scale, q2, k2, v2, do2, o32, do32, lse,
-                                   delta, dq, dk, dv, stream);
+                                   delta, lse2, dq, dk, dv, stream);
     } else {
       const unsigned short *qb = static_cast<const unsigned short *>(q);
       const unsigned short *kb = static_cast<const unsigned short *>(k);
@@ -825,12 +976,12 @@ extern "C" seg_status seg_attn_bwd(const seg_layout *L, const seg_sizes *sz, seg
       const unsigned short *o16 = static_cast<const unsigned short *>(o);
       if (d == 128)
         bwd_impl<128, unsigned short, unsigned short>(L, sz, hq, hkv, softmax_scale, qb, kb, vb,
-                                                      dob, o16, dob, lse, delta, dq, dk, dv,
-                                                      stream);
+                                                      dob, o16, dob, lse, delta, lse2, dq, dk,
+                                                      dv, stream);
       else
         bwd_impl<64, unsigned short, unsigned short>(L, sz, hq, hkv, softmax_scale, qb, kb, vb,
-                                                     dob, o16, dob, lse, delta, dq, dk, dv,
-                                                     stream);
+                                                     dob, o16, dob, lse, delta, lse2, dq, dk,
+                                                     dv, stream);
     }
   });
 }
