@@ -186,7 +186,10 @@ __device__ __forceinline__ bf16x8 frag_tr(const char *tile, int R, int offa, int
   return r;
 }
 
-// Lane coordinates of a 64-row tile fill by NW waves (PW 1-KB loads each).
+// Lane coordinates of a 64-row tile fill by NW waves (PW direct 16-byte
+// global->LDS loads per lane; each wave instruction fills 1 KB of LDS,
+// lane-contiguous).  The swizzle is applied by choosing which global chunk
+// each lane loads.
 template <int D, int NW>
 struct FillPlan {
   static constexpr int CPR = D / 8, PW = 64 * CPR / (64 * NW);
@@ -217,16 +220,33 @@ struct FillPlan {
   }
 };
 
-// 64 consecutive 4-byte values (one per lane) into LDS
+// one dword per lane into 64 consecutive dwords of LDS (direct load)
 __device__ __forceinline__ void fill64_dw(void *dst, const void *src_lane) {
 #if defined(__HIP_DEVICE_COMPILE__)
   __builtin_amdgcn_global_load_lds(src_lane, (__attribute__((address_space(3))) void *)dst, 4, 0, 0);
 #endif
 }
 
+// Software pipelining over units.  The direct loads of unit n+1 are issued,
+// then unit n is computed from the other buffer, then a barrier (which waits
+// for the loads) ends the step.  Both happen inside one always-inline step
+// whose LDS buffers are distinct __restrict__ parameters: a direct load's LDS
+// write is counted with the global loads, and without the no-alias facts the
+// compiler would wait for the loads in flight before the first LDS read of
+// the compute.  Every LDS access of a step goes through those parameters.
+
 __device__ __forceinline__ void wait_all_and_sync() {
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
+}
+
+// Barrier for LDS traffic only: waits for this wave's LDS operations but not
+// for its direct loads in flight (the prefetch of the next unit).
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
 // sum of 8 bf16 values (fp32 accumulation)
@@ -238,15 +258,80 @@ __device__ __forceinline__ float sum8(const bf16x8 &v, float acc) {
   return acc;
 }
 
+// XCD-aware block mapping.  Blocks are dispatched round-robin over the 8
+// XCDs (block b runs on XCD b % 8), each with its own L2.  XCD x takes the
+// contiguous tile range [x*C, (x+1)*C), C = ceil(ntiles / 8), and runs the nh
+// heads of one tile back to back: heads of a tile read the same key/value
+// tiles, and neighbouring tiles of a segment read mostly the same ones, so
+// they meet in one L2.  Each range holds several whole segments, which keeps
+// the XCDs balanced.  `reverse` walks the range from its end (the longest
+// rows of each segment first).  The grid is 8*C*nh blocks; blocks past the
+// last tile exit at once.
+__device__ __forceinline__ bool xcd_block(int nh, int ntiles, bool reverse, int &tile, int &head) {
+  const int b = blockIdx.x, x = b & 7, i = b >> 3;
+  const int C = (ntiles + 7) >> 3;
+  const int t = i / nh;
+  head = i - t * nh;
+  tile = x * C + (reverse ? C - 1 - t : t);
+  return tile < ntiles;
+}
+
+__host__ __device__ inline int xcd_grid(int ntiles, int nh) { return (ntiles + 7) / 8 * 8 * nh; }
+
 // A unit of work: 64 rows (half of a 128-row tile) of the tile listed at CSR
 // entry e.
 struct Unit {
   int e, half;
-  int r0;     // segment-relative first row of the unit
-  int vrows;  // valid rows (1..64)
-  bool partial;
+  int r0;       // segment-relative first row of the unit
+  int vrows;    // valid rows (1..64)
+  int partial;  // PARTIAL tile (an int: a struct without padding bytes is
+                // copied field by field, never through private memory)
 };
 
+// The CSR entries (tile index, class) of one block, staged in LDS in chunks
+// of CAP (the dK/dV kernel, which revisits each entry once per query head of
+// the group).
+template <int CAP>
+struct EntryStage {
+  int tile[CAP];
+  int cls[CAP];
+};
+
+template <int CAP, int NT>
+__device__ __forceinline__ void stage_entries(EntryStage<CAP> &st, const int32_t *idx,
+                                              const uint8_t *cls, int from, int to) {
+  for (int i = threadIdx.x; i < CAP && from + i < to; i += NT) {
+    st.tile[i] = idx[from + i];
+    st.cls[i] = cls[from + i];
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+}
+
+// Unit (e, half) of a block whose entries are [cbase, e1) staged in `st`.
+// Every thread calls it with the same arguments, in increasing e, between
+// steps (no direct load in flight); a chunk boundary re-stages.
+template <int CAP, int NT>
+__device__ __forceinline__ Unit unit_at(EntryStage<CAP> &st, int &cbase, int e, int half, int e1,
+                                        const int32_t *idx, const uint8_t *cls, int qbase,
+                                        int seg_len) {
+  if (e - cbase >= CAP) {
+    __syncthreads();  // every wave is done with the staged chunk
+    cbase += CAP;
+    stage_entries<CAP, NT>(st, idx, cls, cbase, e1);
+  }
+  Unit u;
+  u.e = e;
+  u.half = half;
+  u.r0 = (st.tile[e - cbase] - qbase) * TQ + half * 64;
+  u.vrows = min(64, seg_len - u.r0);
+  u.partial = st.cls[e - cbase] == SEG_TILE_PARTIAL;
+  return u;
+}
+
+// Unit (e, half) read straight from the CSR arrays (the forward and dQ
+// kernels: the tile index is a uniform load through the scalar cache, which
+// measured faster there than staging the entries in LDS).
 __device__ __forceinline__ Unit make_unit(const int32_t *col_idx, const uint8_t *cls, int e,
                                           int half, int qbase, int seg_len) {
   Unit u;
@@ -283,14 +368,14 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd(
     const unsigned short *__restrict__ v, const int32_t *__restrict__ seg_info,
     const int32_t *__restrict__ tile_seg, const int32_t *__restrict__ tok_meta,
     const int32_t *__restrict__ qt_ptr, const int32_t *__restrict__ qt_col,
-    const uint8_t *__restrict__ qt_cls, const int32_t *__restrict__ work_order, int hq, int hkv,
-    int W, float scale_log2, long P, TO *__restrict__ o, float *__restrict__ lse) {
+    const uint8_t *__restrict__ qt_cls, const int32_t *__restrict__ work_order, int ntiles, int hq,
+    int hkv, int W, float scale_log2, long P, TO *__restrict__ o, float *__restrict__ lse) {
   constexpr int KK = D / 16, DB = D / 32, T64 = 64 * D;
-  __shared__ __attribute__((aligned(16))) unsigned short smem[4 * T64];  // K[2], V[2]
-  __shared__ __attribute__((aligned(16))) int sMeta[2][64];
+  __shared__ __attribute__((aligned(16))) unsigned short sK0[T64], sK1[T64], sV0[T64], sV1[T64];
+  __shared__ __attribute__((aligned(16))) int sM0[64], sM1[64];
 
-  const int g = work_order[blockIdx.x / hq];
-  const int h = blockIdx.x % hq;
+  int g, h;
+  if (!xcd_block(hq, ntiles, true, g, h)) return;
   const int hk = h / (hq / hkv);
   const TileRows tr = tile_rows(seg_info, tile_seg, g);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -318,15 +403,15 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd(
   const long kv_stride = (long)hkv * D;
   const unsigned short *kbase = k + (long)hk * D + (long)tr.start * kv_stride;
   const unsigned short *vbase = v + (long)hk * D + (long)tr.start * kv_stride;
-  const char *sbase = reinterpret_cast<const char *>(smem);
 
-  auto issue = [&](const Unit &u, const int b) __attribute__((always_inline)) {
-    fp.issue(smem + b * T64, kbase, kv_stride, u.r0, u.vrows, wave);
-    fp.issue(smem + (2 + b) * T64, vbase, kv_stride, u.r0, u.vrows, wave);
-    if (wave == 0) fill64_dw(&sMeta[b][0], tok_meta + tr.start + u.r0 + min(lane, u.vrows - 1));
+  auto issue = [&](const Unit &u, unsigned short *__restrict__ nK, unsigned short *__restrict__ nV,
+                   int *__restrict__ nM) __attribute__((always_inline)) {
+    fp.issue(nK, kbase, kv_stride, u.r0, u.vrows, wave);
+    fp.issue(nV, vbase, kv_stride, u.r0, u.vrows, wave);
+    if (wave == 0) fill64_dw(nM, tok_meta + tr.start + u.r0 + min(lane, u.vrows - 1));
   };
-  auto compute = [&](const Unit &u, const int b) __attribute__((always_inline)) {
-    const char *sK = sbase + b * T64 * 2, *sV = sbase + (2 + b) * T64 * 2;
+  auto compute = [&](const Unit &u, const char *__restrict__ sK, const char *__restrict__ sV,
+                     const int *__restrict__ sM) __attribute__((always_inline)) {
     f32x16 sacc[2];
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
@@ -338,17 +423,18 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd(
       for (int kk = 0; kk < KK; ++kk) sacc[kb] = mfma32(ak[kk], qf[kk], sacc[kb]);
     }
     // raw scores; masked entries -inf (scale > 0 keeps the order)
-    if (u.partial) {
+    if (__builtin_expect(u.partial, 0)) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
         for (int rg = 0; rg < 4; ++rg) {
           const int kb0 = kb * 32 + 8 * rg + 4 * hh;
-          const i32x4 M4 = *reinterpret_cast<const i32x4 *>(&sMeta[b][kb0]);
+          const i32x4 M4 = *reinterpret_cast<const i32x4 *>(sM + kb0);
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
+            // bitwise, not short-circuit: no branch per element
             const int key = kb0 + j;
-            const bool vis = qvalid && key < u.vrows && (u.r0 + key <= qr) &&
+            const bool vis = qvalid & (key < u.vrows) & (u.r0 + key <= qr) &
                              (qstep < key_expiry(M4[j], W));
             sacc[kb][rg * 4 + j] = vis ? sacc[kb][rg * 4 + j] : -INFINITY;
           }
@@ -398,22 +484,31 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd(
         for (int db = 0; db < DB; ++db) oacc[db] = mfma32(av[db], pf[kb][c2], oacc[db]);
       }
   };
+  auto step = [&](const Unit &u, const bool more, const Unit &nu,
+                  const unsigned short *__restrict__ cK, const unsigned short *__restrict__ cV,
+                  const int *__restrict__ cM, unsigned short *__restrict__ nK,
+                  unsigned short *__restrict__ nV, int *__restrict__ nM)
+                  __attribute__((always_inline)) {
+    if (more) issue(nu, nK, nV, nM);
+    compute(u, reinterpret_cast<const char *>(cK), reinterpret_cast<const char *>(cV), cM);
+  };
 
   const int e0 = qt_ptr[g], e1 = qt_ptr[g + 1];
+  auto next = [&](const Unit &u, Unit &n) __attribute__((always_inline)) -> bool {
+    return next_unit(u, e1, qt_col, qt_cls, tr.qbase, tr.len, n);
+  };
   Unit u = make_unit(qt_col, qt_cls, e0, 0, tr.qbase, tr.len), nu;
-  issue(u, 0);
+  issue(u, sK0, sV0, sM0);
   wait_all_and_sync();
   for (;;) {
-    bool more = next_unit(u, e1, qt_col, qt_cls, tr.qbase, tr.len, nu);
-    if (more) issue(nu, 1);
-    compute(u, 0);
-    wait_all_and_sync();
+    bool more = next(u, nu);
+    step(u, more, nu, sK0, sV0, sM0, sK1, sV1, sM1);
+    __syncthreads();
     if (!more) break;
     u = nu;
-    more = next_unit(u, e1, qt_col, qt_cls, tr.qbase, tr.len, nu);
-    if (more) issue(nu, 0);
-    compute(u, 1);
-    wait_all_and_sync();
+    more = next(u, nu);
+    step(u, more, nu, sK1, sV1, sM1, sK0, sV0, sM0);
+    __syncthreads();
     if (!more) break;
     u = nu;
   }
@@ -442,7 +537,7 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd(
 // S = Q K^T keeps queries on accumulator rows, so P and dS feed
 // dV += P^T dO and dK += dS^T Q directly (dO^T, Q^T by transpose reads).
 // Units are 64-row halves of the listed q-tiles, for every query head of the
-// group; no atomics.
+// group, double-buffered in LDS.  No atomics.
 template <int D, class TO>
 __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
     const unsigned short *__restrict__ q, const unsigned short *__restrict__ k,
@@ -450,18 +545,21 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
     const float *__restrict__ lse2, const float *__restrict__ delta,
     const int32_t *__restrict__ seg_info, const int32_t *__restrict__ tile_seg,
     const int32_t *__restrict__ tok_meta, const int32_t *__restrict__ kt_ptr,
-    const int32_t *__restrict__ kt_row, const uint8_t *__restrict__ kt_cls, int hq, int hkv,
-    int W, float scale_log2, float scale, long P, TO *__restrict__ dk, TO *__restrict__ dv) {
-  constexpr int KK = D / 16, T64 = 64 * D, DH = D / 2, DBH = DH / 32;
-  __shared__ __attribute__((aligned(16))) unsigned short smem[4 * T64];  // Q[2], dO[2]
-  __shared__ __attribute__((aligned(16))) float sLse[2][64];
-  __shared__ __attribute__((aligned(16))) float sDel[2][64];
-  __shared__ __attribute__((aligned(16))) int sMeta[2][64];
-  __shared__ __attribute__((aligned(16))) f32x4 xP[2][4][4][64];     // [qb][key group][quarter][lane]
-  __shared__ __attribute__((aligned(16))) bf16x8 xdS[2][4][2][64];   // [qb][key group][c][lane]
+    const int32_t *__restrict__ kt_row, const uint8_t *__restrict__ kt_cls, int ntiles, int hq,
+    int hkv, int W, float scale_log2, float scale, long P, TO *__restrict__ dk,
+    TO *__restrict__ dv) {
+  constexpr int KK = D / 16, T64 = 64 * D, DH = D / 2, DBH = DH / 32, CAP = 256;
+  __shared__ __attribute__((aligned(16))) unsigned short sQ0[T64], sQ1[T64], sD0[T64], sD1[T64];
+  __shared__ __attribute__((aligned(16))) float sL0[64], sL1[64], sE0[64], sE1[64];
+  __shared__ __attribute__((aligned(16))) int sM0[64], sM1[64];
+  __shared__ __attribute__((aligned(16))) f32x4 xP[2][4][4][64];    // [qb][key group][quarter][lane]
+  __shared__ __attribute__((aligned(16))) bf16x8 xdS[2][4][2][64];  // [qb][key group][c][lane]
+  __shared__ EntryStage<CAP> ent;
 
-  const int g = blockIdx.x / hkv;
-  const int hk = blockIdx.x % hkv;
+  // k-tiles in natural order: within a segment the earliest k-tiles have the
+  // longest transposed-CSR columns, so they start first
+  int g, hk;
+  if (!xcd_block(hkv, ntiles, false, g, hk)) return;
   const int grp = hq / hkv;
   const TileRows tr = tile_rows(seg_info, tile_seg, g);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -491,27 +589,36 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
   FillPlan<D, 8> fp;
   fp.init(wave, lane);
   const long q_stride = (long)hq * D;
-  const char *sbase = reinterpret_cast<const char *>(smem);
   const int e0 = kt_ptr[g], e1 = kt_ptr[g + 1];
 
-  auto issue = [&](const Unit &u, int hi, const int b) __attribute__((always_inline)) {
+  // Q and dO rows of one unit, and one per-row value by waves 0-2
+  // (log2-sum-exp, Delta, turn)
+  auto issue = [&](const Unit &u, int hi, unsigned short *__restrict__ nQ,
+                   unsigned short *__restrict__ nD, float *__restrict__ nL,
+                   float *__restrict__ nE, int *__restrict__ nM) __attribute__((always_inline)) {
     const int h = hk * grp + hi;
-    fp.issue(smem + b * T64, q + (long)h * D + (long)tr.start * q_stride, q_stride, u.r0, u.vrows,
-             wave);
-    fp.issue(smem + (2 + b) * T64, dout + (long)h * D + (long)tr.start * q_stride, q_stride, u.r0,
-             u.vrows, wave);
+    fp.issue(nQ, q + (long)h * D + (long)tr.start * q_stride, q_stride, u.r0, u.vrows, wave);
+    fp.issue(nD, dout + (long)h * D + (long)tr.start * q_stride, q_stride, u.r0, u.vrows, wave);
     const long lrow = tr.start + u.r0 + min(lane, u.vrows - 1);
-    if (wave == 0) fill64_dw(&sLse[b][0], lse2 + (long)h * P + lrow);
-    if (wave == 1) fill64_dw(&sDel[b][0], delta + (long)h * P + lrow);
-    if (wave == 2) fill64_dw(&sMeta[b][0], tok_meta + lrow);
+    if (wave == 0) fill64_dw(nL, lse2 + (long)h * P + lrow);
+    else if (wave == 1) fill64_dw(nE, delta + (long)h * P + lrow);
+    else if (wave == 2) fill64_dw(nM, tok_meta + lrow);
   };
-  auto compute = [&](const Unit &u, const int b) __attribute__((always_inline)) {
-    const char *sQ = sbase + b * T64 * 2, *sdO = sbase + (2 + b) * T64 * 2;
+  auto compute = [&](const Unit &u, const char *__restrict__ sQ, const char *__restrict__ sdO,
+                     const float *__restrict__ sLse, const float *__restrict__ sDel,
+                     const int *__restrict__ sMeta, f32x4 *__restrict__ eP,
+                     bf16x8 *__restrict__ edS) __attribute__((always_inline)) {
     const char *sA = role == 0 ? sQ : sdO;  // S-role reads Q, dP-role reads dO
     const int nqb = (u.vrows + 31) >> 5;
+    // FULL units with 64 query rows and every key of the tile valid need no
+    // predicate (kvalid is false only in a segment's last k-tile, which is
+    // a diagonal, PARTIAL tile)
+    const bool masked = u.partial | (u.vrows < 64);
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
       if (qb >= nqb) break;
+      f32x4 *xp = eP + (qb * 4 + kg) * 4 * 64;   // [quarter][lane]
+      bf16x8 *xd = edS + (qb * 4 + kg) * 2 * 64;  // [c][lane]
       // phase 1: S (role 0) or dP (role 1), queries on accumulator rows
       bf16x8 af[KK];
 #pragma unroll
@@ -521,31 +628,44 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
       for (int kk = 0; kk < KK; ++kk) acc = mfma32(af[kk], kv_f[kk], acc);
       bf16x8 pa[2], dsa[2];
       if (role == 0) {
+        // P = exp2(S * scale - lse); a masked pair gets exponent -inf (P = 0).
+        // One uniform branch; inside, the predicate is bitwise.
+        if (__builtin_expect(masked, 0)) {
 #pragma unroll
-        for (int rg = 0; rg < 4; ++rg) {
-          const int base = qb * 32 + 8 * rg + 4 * hh;
-          const f32x4 L4 = *reinterpret_cast<const f32x4 *>(&sLse[b][base]);
-          const i32x4 M4 = *reinterpret_cast<const i32x4 *>(&sMeta[b][base]);
+          for (int rg = 0; rg < 4; ++rg) {
+            const int base = qb * 32 + 8 * rg + 4 * hh;
+            const f32x4 L4 = *reinterpret_cast<const f32x4 *>(sLse + base);
+            const i32x4 M4 = *reinterpret_cast<const i32x4 *>(sMeta + base);
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int r = rg * 4 + j, ql = base + j;
-            const float pv = __builtin_amdgcn_exp2f(fmaf(acc[r], scale_log2, -L4[j]));
-            bool vis = kvalid && ql < u.vrows;
-            if (u.partial) vis = vis && (kr <= u.r0 + ql) && ((M4[j] >> 2) < kexp);
-            acc[r] = vis ? pv : 0.f;
+            for (int j = 0; j < 4; ++j) {
+              const int r = rg * 4 + j, ql = base + j;
+              const bool vis = kvalid & (ql < u.vrows) & (kr <= u.r0 + ql) & ((M4[j] >> 2) < kexp);
+              const float x = vis ? fmaf(acc[r], scale_log2, -L4[j]) : -INFINITY;
+              acc[r] = __builtin_amdgcn_exp2f(x);
+            }
           }
-          xP[qb][kg][rg][lane] = f32x4{acc[rg * 4], acc[rg * 4 + 1], acc[rg * 4 + 2], acc[rg * 4 + 3]};
+        } else {
+#pragma unroll
+          for (int rg = 0; rg < 4; ++rg) {
+            const f32x4 L4 = *reinterpret_cast<const f32x4 *>(sLse + qb * 32 + 8 * rg + 4 * hh);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+              acc[rg * 4 + j] = __builtin_amdgcn_exp2f(fmaf(acc[rg * 4 + j], scale_log2, -L4[j]));
+          }
         }
+#pragma unroll
+        for (int rg = 0; rg < 4; ++rg)
+          xp[rg * 64 + lane] = f32x4{acc[rg * 4], acc[rg * 4 + 1], acc[rg * 4 + 2], acc[rg * 4 + 3]};
         pa[0] = pack8(acc, 0);
         pa[1] = pack8(acc, 8);
       }
-      __syncthreads();
+      lds_barrier();
       if (role == 1) {
         f32x16 pv;
 #pragma unroll
         for (int rg = 0; rg < 4; ++rg) {
-          const f32x4 p4 = xP[qb][kg][rg][lane];
-          const f32x4 D4 = *reinterpret_cast<const f32x4 *>(&sDel[b][qb * 32 + 8 * rg + 4 * hh]);
+          const f32x4 p4 = xp[rg * 64 + lane];
+          const f32x4 D4 = *reinterpret_cast<const f32x4 *>(sDel + qb * 32 + 8 * rg + 4 * hh);
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             pv[rg * 4 + j] = p4[j];
@@ -556,8 +676,8 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
         pa[1] = pack8(pv, 8);
         dsa[0] = pack8(acc, 0);
         dsa[1] = pack8(acc, 8);
-        xdS[qb][kg][0][lane] = dsa[0];
-        xdS[qb][kg][1][lane] = dsa[1];
+        xd[lane] = dsa[0];
+        xd[64 + lane] = dsa[1];
       }
       // dV half += P^T dO[:, half]  (role 0 while role 1 forms dS)
 #pragma unroll
@@ -569,10 +689,10 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
 #pragma unroll
         for (int db = 0; db < DBH; ++db) dvacc[db] = mfma32(pa[c2], bo[db], dvacc[db]);
       }
-      __syncthreads();
+      lds_barrier();
       if (role == 0) {
-        dsa[0] = xdS[qb][kg][0][lane];
-        dsa[1] = xdS[qb][kg][1][lane];
+        dsa[0] = xd[lane];
+        dsa[1] = xd[64 + lane];
       }
       // dK half += dS^T Q[:, half]
 #pragma unroll
@@ -586,74 +706,102 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
       }
     }
   };
+  auto step = [&](const Unit &u, const bool more, const Unit &nu, int nhi,
+                  const unsigned short *__restrict__ cQ, const unsigned short *__restrict__ cD,
+                  const float *__restrict__ cL, const float *__restrict__ cE,
+                  const int *__restrict__ cM, unsigned short *__restrict__ nQ,
+                  unsigned short *__restrict__ nD, float *__restrict__ nL, float *__restrict__ nE,
+                  int *__restrict__ nM, f32x4 *__restrict__ eP, bf16x8 *__restrict__ edS)
+                  __attribute__((always_inline)) {
+    if (more) issue(nu, nhi, nQ, nD, nL, nE, nM);
+    compute(u, reinterpret_cast<const char *>(cQ), reinterpret_cast<const char *>(cD), cL, cE, cM,
+            eP, edS);
+  };
 
   if (e0 < e1) {
-    Unit u = make_unit(kt_row, kt_cls, e0, 0, tr.qbase, tr.len), nu;
-    int hi = 0, nhi = 0;
+    int cbase = e0;  // first entry staged in `ent`
+    stage_entries<CAP, 512>(ent, kt_row, kt_cls, cbase, e1);
     // next unit: other half of this tile, else next head, else next entry
     auto advance = [&](const Unit &cu, int chi, Unit &n, int &nh) __attribute__((always_inline)) -> bool {
       if (cu.half == 0 && cu.r0 + 64 < tr.len) {
-        n = make_unit(kt_row, kt_cls, cu.e, 1, tr.qbase, tr.len);
+        n = cu;
+        n.half = 1;
+        n.r0 = cu.r0 + 64;
+        n.vrows = min(64, tr.len - n.r0);
         nh = chi;
       } else if (chi + 1 < grp) {
-        n = make_unit(kt_row, kt_cls, cu.e, 0, tr.qbase, tr.len);
+        n = cu;
+        n.half = 0;
+        n.r0 = cu.r0 - cu.half * 64;
+        n.vrows = min(64, tr.len - n.r0);
         nh = chi + 1;
       } else if (cu.e + 1 < e1) {
-        n = make_unit(kt_row, kt_cls, cu.e + 1, 0, tr.qbase, tr.len);
+        n = unit_at<CAP, 512>(ent, cbase, cu.e + 1, 0, e1, kt_row, kt_cls, tr.qbase, tr.len);
         nh = 0;
       } else {
         return false;
       }
       return true;
     };
-    issue(u, hi, 0);
+    f32x4 *eP = &xP[0][0][0][0];
+    bf16x8 *edS = &xdS[0][0][0][0];
+    Unit cur = unit_at<CAP, 512>(ent, cbase, e0, 0, e1, kt_row, kt_cls, tr.qbase, tr.len), nx;
+    int hcur = 0, hnx = 0;
+    issue(cur, hcur, sQ0, sD0, sL0, sE0, sM0);
     wait_all_and_sync();
     for (;;) {
-      bool more = advance(u, hi, nu, nhi);
-      if (more) issue(nu, nhi, 1);
-      compute(u, 0);
-      wait_all_and_sync();
+      bool more = advance(cur, hcur, nx, hnx);
+      step(cur, more, nx, hnx, sQ0, sD0, sL0, sE0, sM0, sQ1, sD1, sL1, sE1, sM1, eP, edS);
+      __syncthreads();
       if (!more) break;
-      u = nu;
-      hi = nhi;
-      more = advance(u, hi, nu, nhi);
-      if (more) issue(nu, nhi, 0);
-      compute(u, 1);
-      wait_all_and_sync();
+      cur = nx;
+      hcur = hnx;
+      more = advance(cur, hcur, nx, hnx);
+      step(cur, more, nx, hnx, sQ1, sD1, sL1, sE1, sM1, sQ0, sD0, sL0, sE0, sM0, eP, edS);
+      __syncthreads();
       if (!more) break;
-      u = nu;
-      hi = nhi;
+      cur = nx;
+      hcur = hnx;
     }
   }
 
-  // stage through LDS for coalesced stores; accumulator D[i = key][j = d]
-  TO *st = reinterpret_cast<TO *>(smem);  // [128][D] of TO
-  constexpr int CH = 16 / sizeof(TO);
+  // stage through LDS (one 64-row tile, RP key rows per pass) for coalesced
+  // stores; accumulator D[i = key][j = d]
+  wait_all_and_sync();
+  TO *st = reinterpret_cast<TO *>(sQ0);
+  constexpr int CH = 16 / sizeof(TO);       // elements per 16-byte chunk
+  constexpr int RP = 128 / sizeof(TO);      // key rows per pass (16 KB)
 #pragma unroll
   for (int which = 0; which < 2; ++which) {
-#pragma unroll
-    for (int db = 0; db < DBH; ++db)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int kl = kg * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-        const float val = which == 0 ? dkacc[db][r] * scale : dvacc[db][r];
-        const int dd = role * DH + db * 32 + col;
-        if constexpr (sizeof(TO) == 2)
-          st[kl * D + dd] = f2bf_bits(val);
-        else
-          st[kl * D + dd] = val;
-      }
-    __syncthreads();
     TO *dst = which == 0 ? dk : dv;
-    for (int c = threadIdx.x; c < TQ * D / CH; c += 512) {
-      const int kl = c / (D / CH), ch = c % (D / CH);
-      if (kl < tr.nrows) {
-        const long row = tr.start + tr.row0 + kl;
-        *reinterpret_cast<u16x8 *>(dst + (row * hkv + hk) * D + ch * CH) =
-            *reinterpret_cast<const u16x8 *>(st + kl * D + ch * CH);
+#pragma unroll
+    for (int pass = 0; pass < TQ / RP; ++pass) {
+      if (kg * 32 >= pass * RP && kg * 32 < (pass + 1) * RP) {
+#pragma unroll
+        for (int db = 0; db < DBH; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int kl = kg * 32 + 8 * (r >> 2) + 4 * hh + (r & 3) - pass * RP;
+            const float val = which == 0 ? dkacc[db][r] * scale : dvacc[db][r];
+            const int dd = role * DH + db * 32 + col;
+            if constexpr (sizeof(TO) == 2)
+              st[kl * D + dd] = f2bf_bits(val);
+            else
+              st[kl * D + dd] = val;
+          }
       }
+      __syncthreads();
+      for (int c = threadIdx.x; c < RP * D / CH; c += 512) {
+        const int kl = c / (D / CH), ch = c % (D / CH);
+        const int key = pass * RP + kl;
+        if (key < tr.nrows) {
+          const long row = tr.start + tr.row0 + key;
+          *reinterpret_cast<u16x8 *>(dst + (row * hkv + hk) * D + ch * CH) =
+              *reinterpret_cast<const u16x8 *>(st + kl * D + ch * CH);
+        }
+      }
+      __syncthreads();
     }
-    __syncthreads();
   }
 }
 
@@ -668,14 +816,14 @@ __global__ void __launch_bounds__(256, 2) k_attn_bwd_dq(
     const int32_t *__restrict__ seg_info, const int32_t *__restrict__ tile_seg,
     const int32_t *__restrict__ tok_meta, const int32_t *__restrict__ qt_ptr,
     const int32_t *__restrict__ qt_col, const uint8_t *__restrict__ qt_cls,
-    const int32_t *__restrict__ work_order, int hq, int hkv, int W, float scale_log2,
-    float scale, long P, TO *__restrict__ dq) {
+    const int32_t *__restrict__ work_order, int ntiles, int hq, int hkv, int W,
+    float scale_log2, float scale, long P, TO *__restrict__ dq) {
   constexpr int KK = D / 16, DB = D / 32, T64 = 64 * D;
-  __shared__ __attribute__((aligned(16))) unsigned short smem[4 * T64];  // K[2], V[2]
-  __shared__ __attribute__((aligned(16))) int sMeta[2][64];
+  __shared__ __attribute__((aligned(16))) unsigned short sK0[T64], sK1[T64], sV0[T64], sV1[T64];
+  __shared__ __attribute__((aligned(16))) int sM0[64], sM1[64];
 
-  const int g = work_order[blockIdx.x / hq];
-  const int h = blockIdx.x % hq;
+  int g, h;
+  if (!xcd_block(hq, ntiles, true, g, h)) return;
   const int hk = h / (hq / hkv);
   const TileRows tr = tile_rows(seg_info, tile_seg, g);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -709,15 +857,15 @@ __global__ void __launch_bounds__(256, 2) k_attn_bwd_dq(
   const long kv_stride = (long)hkv * D;
   const unsigned short *kbase = k + (long)hk * D + (long)tr.start * kv_stride;
   const unsigned short *vbase = v + (long)hk * D + (long)tr.start * kv_stride;
-  const char *sbase = reinterpret_cast<const char *>(smem);
 
-  auto issue = [&](const Unit &u, const int b) __attribute__((always_inline)) {
-    fp.issue(smem + b * T64, kbase, kv_stride, u.r0, u.vrows, wave);
-    fp.issue(smem + (2 + b) * T64, vbase, kv_stride, u.r0, u.vrows, wave);
-    if (wave == 0) fill64_dw(&sMeta[b][0], tok_meta + tr.start + u.r0 + min(lane, u.vrows - 1));
+  auto issue = [&](const Unit &u, unsigned short *__restrict__ nK, unsigned short *__restrict__ nV,
+                   int *__restrict__ nM) __attribute__((always_inline)) {
+    fp.issue(nK, kbase, kv_stride, u.r0, u.vrows, wave);
+    fp.issue(nV, vbase, kv_stride, u.r0, u.vrows, wave);
+    if (wave == 0) fill64_dw(nM, tok_meta + tr.start + u.r0 + min(lane, u.vrows - 1));
   };
-  auto compute = [&](const Unit &u, const int b) __attribute__((always_inline)) {
-    const char *sK = sbase + b * T64 * 2, *sV = sbase + (2 + b) * T64 * 2;
+  auto compute = [&](const Unit &u, const char *__restrict__ sK, const char *__restrict__ sV,
+                     const int *__restrict__ sM) __attribute__((always_inline)) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       if (kb * 32 >= u.vrows) break;
@@ -733,18 +881,27 @@ __global__ void __launch_bounds__(256, 2) k_attn_bwd_dq(
         s = mfma32(ak[kk], qf[kk], s);
         dp = mfma32(av[kk], df[kk], dp);
       }
+      // dS^T = P^T (dP^T - Delta); a masked pair gets exponent -inf (P = 0).
+      // One uniform branch; inside, the predicate is bitwise (no branch per
+      // element).
+      if (__builtin_expect(u.partial, 0)) {
 #pragma unroll
-      for (int rg = 0; rg < 4; ++rg) {
-        const int kb0 = kb * 32 + 8 * rg + 4 * hh;
-        const i32x4 M4 = *reinterpret_cast<const i32x4 *>(&sMeta[b][kb0]);
+        for (int rg = 0; rg < 4; ++rg) {
+          const int kb0 = kb * 32 + 8 * rg + 4 * hh;
+          const i32x4 M4 = *reinterpret_cast<const i32x4 *>(sM + kb0);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int r = rg * 4 + j, kl = kb0 + j;
-          const float pv = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -l2));
-          bool vis = qvalid && kl < u.vrows;
-          if (u.partial) vis = vis && (u.r0 + kl <= qr) && (qstep < key_expiry(M4[j], W));
-          s[r] = vis ? pv * (dp[r] - dlt) : 0.f;
+          for (int j = 0; j < 4; ++j) {
+            const int r = rg * 4 + j, kl = kb0 + j;
+            const bool vis = qvalid & (kl < u.vrows) & (u.r0 + kl <= qr) &
+                             (qstep < key_expiry(M4[j], W));
+            const float x = vis ? fmaf(s[r], scale_log2, -l2) : -INFINITY;
+            s[r] = __builtin_amdgcn_exp2f(x) * (dp[r] - dlt);
+          }
         }
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          s[r] = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -l2)) * (dp[r] - dlt);
       }
 #pragma unroll
       for (int c2 = 0; c2 < 2; ++c2) {
@@ -758,22 +915,31 @@ __global__ void __launch_bounds__(256, 2) k_attn_bwd_dq(
       }
     }
   };
+  auto step = [&](const Unit &u, const bool more, const Unit &nu,
+                  const unsigned short *__restrict__ cK, const unsigned short *__restrict__ cV,
+                  const int *__restrict__ cM, unsigned short *__restrict__ nK,
+                  unsigned short *__restrict__ nV, int *__restrict__ nM)
+                  __attribute__((always_inline)) {
+    if (more) issue(nu, nK, nV, nM);
+    compute(u, reinterpret_cast<const char *>(cK), reinterpret_cast<const char *>(cV), cM);
+  };
 
   const int e0 = qt_ptr[g], e1 = qt_ptr[g + 1];
+  auto next = [&](const Unit &u, Unit &n) __attribute__((always_inline)) -> bool {
+    return next_unit(u, e1, qt_col, qt_cls, tr.qbase, tr.len, n);
+  };
   Unit u = make_unit(qt_col, qt_cls, e0, 0, tr.qbase, tr.len), nu;
-  issue(u, 0);
+  issue(u, sK0, sV0, sM0);
   wait_all_and_sync();
   for (;;) {
-    bool more = next_unit(u, e1, qt_col, qt_cls, tr.qbase, tr.len, nu);
-    if (more) issue(nu, 1);
-    compute(u, 0);
-    wait_all_and_sync();
+    bool more = next(u, nu);
+    step(u, more, nu, sK0, sV0, sM0, sK1, sV1, sM1);
+    __syncthreads();
     if (!more) break;
     u = nu;
-    more = next_unit(u, e1, qt_col, qt_cls, tr.qbase, tr.len, nu);
-    if (more) issue(nu, 0);
-    compute(u, 1);
-    wait_all_and_sync();
+    more = next(u, nu);
+    step(u, more, nu, sK1, sV1, sM1, sK0, sV0, sM0);
+    __syncthreads();
     if (!more) break;
     u = nu;
   }
@@ -845,10 +1011,10 @@ void fwd_impl(const seg_layout *L, const seg_sizes *sz, int hq, int hkv, float s
               float *lse, hipStream_t st) {
   const int G = sz->num_qtiles;
   ProfScope prof("attn_fwd", st);
-  k_attn_fwd<D, TO><<<G * hq, 256, 0, st>>>(q, k, v, L->seg_info, L->tile_seg, L->tok_meta,
-                                             L->qt_ptr, L->qt_col, L->qt_cls, L->work_order, hq,
-                                             hkv, L->window, scale * LOG2E, sz->packed_tokens,
-                                             static_cast<TO *>(o), lse);
+  k_attn_fwd<D, TO><<<xcd_grid(G, hq), 256, 0, st>>>(
+      q, k, v, L->seg_info, L->tile_seg, L->tok_meta, L->qt_ptr, L->qt_col, L->qt_cls,
+      L->work_order, G, hq, hkv, L->window, scale * LOG2E, sz->packed_tokens, static_cast<TO *>(o),
+      lse);
   SEG_LAUNCH_CHECK();
 }
 
@@ -869,16 +1035,16 @@ void bwd_impl(const seg_layout *L, const seg_sizes *sz, int hq, int hkv, float s
   }
   {
     ProfScope prof("attn_bwd_dkdv", st);
-    k_attn_bwd_dkdv<D, TO><<<G * hkv, 512, 0, st>>>(
+    k_attn_bwd_dkdv<D, TO><<<xcd_grid(G, hkv), 512, 0, st>>>(
         q, k, v, dout, lse2, delta, L->seg_info, L->tile_seg, L->tok_meta, L->kt_ptr, L->kt_row,
-        L->kt_cls, hq, hkv, L->window, scale * LOG2E, scale, P, static_cast<TO *>(dk),
+        L->kt_cls, G, hq, hkv, L->window, scale * LOG2E, scale, P, static_cast<TO *>(dk),
         static_cast<TO *>(dv));
     SEG_LAUNCH_CHECK();
   }
   ProfScope prof("attn_bwd_dq", st);
-  k_attn_bwd_dq<D, TO><<<G * hq, 256, 0, st>>>(
+  k_attn_bwd_dq<D, TO><<<xcd_grid(G, hq), 256, 0, st>>>(
       q, k, v, dout, lse2, delta, L->seg_info, L->tile_seg, L->tok_meta, L->qt_ptr, L->qt_col,
-      L->qt_cls, L->work_order, hq, hkv, L->window, scale * LOG2E, scale, P,
+      L->qt_cls, L->work_order, G, hq, hkv, L->window, scale * LOG2E, scale, P,
       static_cast<TO *>(dq));
   SEG_LAUNCH_CHECK();
 }
