@@ -118,25 +118,32 @@ __global__ void __launch_bounds__(256) k_delta(const TI *__restrict__ o, const T
 
 // ------------------------------------------------------------- pipelined kernels
 //
-// Tiles of 64 rows x d (row-major, bf16) are staged in LDS by direct 16-byte
-// global->LDS loads (each wave instruction fills 1 KB, lane-contiguous) into a
-// double buffer: the loads of the next unit are issued before the MFMA work of
-// the current one.  Rows are stored with a 16-byte-chunk swizzle that keeps
-// both 16-byte row reads (MFMA operands contracting over d) and 4x16 transpose
-// reads (ds_read_b64_tr_b16: operands contracting over the rows) free of bank
-// conflicts, so no transposed copy of any tensor is needed.  Every lane's
-// swizzled offsets are computed once; inside the loops a read is a register
-// offset plus an immediate (row block and buffer are compile-time).
+// Tiles of 64 rows x d (row-major, bf16) are double-buffered in LDS: the
+// loads of the next unit are in flight while the current one is computed.
+// The forward and dQ kernels fill with direct 16-byte global->LDS loads; the
+// dK/dV kernel, which has registers to spare, stages the next unit in
+// registers (see the note on wait counts below).  Rows are stored with a
+// 16-byte-chunk swizzle that keeps both 16-byte row reads (MFMA operands
+// contracting over d; 16 lanes per LDS cycle) and 4x16 transpose reads
+// (ds_read_b64_tr_b16: operands contracting over the rows; 32 lanes per
+// cycle) free of bank conflicts on 64 four-byte banks, so no transposed copy
+// of any tensor is needed.  Every lane's swizzled offsets are computed once;
+// inside the loops a read is a register offset plus an immediate.
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 
+// 16-byte chunk swizzle of row `row`: a bijection on row % 16 (a 16-lane row
+// read of one logical chunk hits 16 distinct chunks), and rows 4m..4m+3 differ
+// in bits 2-3 (a 32-lane transpose read of 4 rows x 4 chunks hits 16 distinct
+// chunks).  For d = 64 two rows share one 256-byte bank line, so the same two
+// properties are built from row / 2.
 template <int D>
 __device__ __forceinline__ int swz(int row) {
-  if constexpr (D == 128) return ((row & 7) << 1) | ((row >> 3) & 1);
-  else return (((row >> 1) & 3) << 1) | ((row >> 3) & 1);
+  if constexpr (D == 128) return ((row & 3) << 2) | ((row >> 2) & 3);
+  else return (((row >> 1) & 1) << 2) | ((row >> 2) & 3);
 }
 
 // element offset of (row, col) in a swizzled row-major tile of d columns
@@ -220,6 +227,36 @@ struct FillPlan {
   }
 };
 
+// Register-staged fill of the same lane coordinates: `load` issues the global
+// loads into registers, `store` writes them to LDS.
+template <int D, int NW>
+struct StagePlan {
+  static constexpr int CPR = D / 8, PW = 64 * CPR / (64 * NW);
+  int row[PW], chunk[PW];
+  __device__ __forceinline__ void init(int wave, int lane) {
+#pragma unroll
+    for (int i = 0; i < PW; ++i) {
+      const int s = (wave * PW + i) * 64 + lane;
+      row[i] = s / CPR;
+      chunk[i] = ((s % CPR) ^ swz<D>(row[i])) * 8;
+    }
+  }
+  __device__ __forceinline__ void load(u16x8 (&st)[PW], const unsigned short *base, long stride,
+                                       int r0, int vrows) const {
+#pragma unroll
+    for (int i = 0; i < PW; ++i) {
+      const long r = r0 + min(row[i], vrows - 1);
+      st[i] = *reinterpret_cast<const u16x8 *>(base + r * stride + chunk[i]);
+    }
+  }
+  __device__ __forceinline__ void store(unsigned short *tile, const u16x8 (&st)[PW], int wave,
+                                        int lane) const {
+#pragma unroll
+    for (int i = 0; i < PW; ++i)
+      *reinterpret_cast<u16x8 *>(tile + ((wave * PW + i) * 64 + lane) * 8) = st[i];
+  }
+};
+
 // one dword per lane into 64 consecutive dwords of LDS (direct load)
 __device__ __forceinline__ void fill64_dw(void *dst, const void *src_lane) {
 #if defined(__HIP_DEVICE_COMPILE__)
@@ -227,26 +264,20 @@ __device__ __forceinline__ void fill64_dw(void *dst, const void *src_lane) {
 #endif
 }
 
-// Software pipelining over units.  The direct loads of unit n+1 are issued,
-// then unit n is computed from the other buffer, then a barrier (which waits
-// for the loads) ends the step.  Both happen inside one always-inline step
-// whose LDS buffers are distinct __restrict__ parameters: a direct load's LDS
-// write is counted with the global loads, and without the no-alias facts the
-// compiler would wait for the loads in flight before the first LDS read of
-// the compute.  Every LDS access of a step goes through those parameters.
+// Software pipelining over units.  The loads of unit n+1 are issued, then
+// unit n is computed from the other buffer, then a barrier ends the step.
+// With direct loads, both happen inside one always-inline step whose LDS
+// buffers are distinct __restrict__ parameters: a direct load's LDS write is
+// counted with the global loads, and without the no-alias facts the compiler
+// would wait for the loads in flight before the first LDS read of the
+// compute.  Every LDS access of a step goes through those parameters.  While
+// a direct load is in flight the compiler also gives up counted LDS waits
+// (every wait becomes lgkmcnt(0)), which serialises read-ahead; the dK/dV
+// kernel therefore stages its next unit in registers instead.
 
 __device__ __forceinline__ void wait_all_and_sync() {
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-}
-
-// Barrier for LDS traffic only: waits for this wave's LDS operations but not
-// for its direct loads in flight (the prefetch of the next unit).
-__device__ __forceinline__ void lds_barrier() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
 }
 
 // sum of 8 bf16 values (fp32 accumulation)
@@ -288,50 +319,9 @@ struct Unit {
                 // copied field by field, never through private memory)
 };
 
-// The CSR entries (tile index, class) of one block, staged in LDS in chunks
-// of CAP (the dK/dV kernel, which revisits each entry once per query head of
-// the group).
-template <int CAP>
-struct EntryStage {
-  int tile[CAP];
-  int cls[CAP];
-};
-
-template <int CAP, int NT>
-__device__ __forceinline__ void stage_entries(EntryStage<CAP> &st, const int32_t *idx,
-                                              const uint8_t *cls, int from, int to) {
-  for (int i = threadIdx.x; i < CAP && from + i < to; i += NT) {
-    st.tile[i] = idx[from + i];
-    st.cls[i] = cls[from + i];
-  }
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-}
-
-// Unit (e, half) of a block whose entries are [cbase, e1) staged in `st`.
-// Every thread calls it with the same arguments, in increasing e, between
-// steps (no direct load in flight); a chunk boundary re-stages.
-template <int CAP, int NT>
-__device__ __forceinline__ Unit unit_at(EntryStage<CAP> &st, int &cbase, int e, int half, int e1,
-                                        const int32_t *idx, const uint8_t *cls, int qbase,
-                                        int seg_len) {
-  if (e - cbase >= CAP) {
-    __syncthreads();  // every wave is done with the staged chunk
-    cbase += CAP;
-    stage_entries<CAP, NT>(st, idx, cls, cbase, e1);
-  }
-  Unit u;
-  u.e = e;
-  u.half = half;
-  u.r0 = (st.tile[e - cbase] - qbase) * TQ + half * 64;
-  u.vrows = min(64, seg_len - u.r0);
-  u.partial = st.cls[e - cbase] == SEG_TILE_PARTIAL;
-  return u;
-}
-
-// Unit (e, half) read straight from the CSR arrays (the forward and dQ
-// kernels: the tile index is a uniform load through the scalar cache, which
-// measured faster there than staging the entries in LDS).
+// Unit (e, half) read straight from the CSR arrays (the tile index is a
+// uniform load through the scalar cache, which measured faster than staging
+// the entries in LDS).
 __device__ __forceinline__ Unit make_unit(const int32_t *col_idx, const uint8_t *cls, int e,
                                           int half, int qbase, int seg_len) {
   Unit u;
@@ -529,17 +519,18 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd(
   }
 }
 
-// dK/dV with the head dimension split over wave pairs: one block = one
-// k-tile x one kv head, 8 waves (two per SIMD).  Wave w serves keys
-// 32*(w%4)..+31; waves 0-3 hold K fragments and compute S and P, waves 4-7
-// hold V fragments and compute dP and dS; P and dS are exchanged through LDS
-// and each wave accumulates dK and dV for one half of the head dimension.
-// S = Q K^T keeps queries on accumulator rows, so P and dS feed
-// dV += P^T dO and dK += dS^T Q directly (dO^T, Q^T by transpose reads).
-// Units are 64-row halves of the listed q-tiles, for every query head of the
-// group, double-buffered in LDS.  No atomics.
+// dK/dV, one wave per SIMD: one block = one k-tile x one kv head, 4 waves of
+// 32 keys each.  A wave holds the K and V fragments of its keys and the dK
+// and dV accumulators over the whole head dimension (about 300 registers, so
+// one wave per SIMD).  Per unit (64 rows of one query head) and 32-row block:
+//   S = Q K^T, dP = dO V^T (queries on accumulator rows),
+//   P = exp2(S * scale - lse), dS = P (dP - Delta),
+//   dV += P^T dO, dK += dS^T Q (dO^T, Q^T by transpose reads).
+// P and dS never leave the wave: the only barrier of a unit is the swap of
+// the double buffer, whose next unit is staged in registers.  Units are 64-row halves of the listed q-tiles, for
+// every query head of the group.  No atomics.
 template <int D, class TO>
-__global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
+__global__ void __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) k_attn_bwd_dkdv(
     const unsigned short *__restrict__ q, const unsigned short *__restrict__ k,
     const unsigned short *__restrict__ v, const unsigned short *__restrict__ dout,
     const float *__restrict__ lse2, const float *__restrict__ delta,
@@ -548,13 +539,10 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
     const int32_t *__restrict__ kt_row, const uint8_t *__restrict__ kt_cls, int ntiles, int hq,
     int hkv, int W, float scale_log2, float scale, long P, TO *__restrict__ dk,
     TO *__restrict__ dv) {
-  constexpr int KK = D / 16, T64 = 64 * D, DH = D / 2, DBH = DH / 32, CAP = 256;
+  constexpr int KK = D / 16, T64 = 64 * D, DB = D / 32;
   __shared__ __attribute__((aligned(16))) unsigned short sQ0[T64], sQ1[T64], sD0[T64], sD1[T64];
   __shared__ __attribute__((aligned(16))) float sL0[64], sL1[64], sE0[64], sE1[64];
   __shared__ __attribute__((aligned(16))) int sM0[64], sM1[64];
-  __shared__ __attribute__((aligned(16))) f32x4 xP[2][4][4][64];    // [qb][key group][quarter][lane]
-  __shared__ __attribute__((aligned(16))) bf16x8 xdS[2][4][2][64];  // [qb][key group][c][lane]
-  __shared__ EntryStage<CAP> ent;
 
   // k-tiles in natural order: within a segment the earliest k-tiles have the
   // longest transposed-CSR columns, so they start first
@@ -564,163 +552,182 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
   const TileRows tr = tile_rows(seg_info, tile_seg, g);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int col = lane & 31, hh = lane >> 5;
-  const int kg = wave & 3, role = wave >> 2;
-  const int kloc = kg * 32 + col;
+  const int kloc = wave * 32 + col;
   const bool kvalid = kloc < tr.nrows;
   const int kr = tr.row0 + (kvalid ? kloc : 0);
   const int kexp = key_expiry(tok_meta[tr.start + kr], W);
 
-  bf16x8 kv_f[KK];  // K fragments (role 0) or V fragments (role 1)
+  bf16x8 kf[KK], vf[KK];
   {
     const long row = tr.start + kr;
-    const unsigned short *src = (role == 0 ? k : v) + (row * hkv + hk) * D;
+    const unsigned short *ks = k + (row * hkv + hk) * D, *vs = v + (row * hkv + hk) * D;
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) kv_f[kk] = lds8(src + kk * 16 + hh * 8);
+    for (int kk = 0; kk < KK; ++kk) {
+      kf[kk] = lds8(ks + kk * 16 + hh * 8);
+      vf[kk] = lds8(vs + kk * 16 + hh * 8);
+    }
   }
-  f32x16 dkacc[DBH], dvacc[DBH];
+  f32x16 dkacc[DB], dvacc[DB];
 #pragma unroll
-  for (int db = 0; db < DBH; ++db) {
+  for (int db = 0; db < DB; ++db) {
     dkacc[db] = f32x16{};
     dvacc[db] = f32x16{};
   }
 
   LaneOffsets<D> lo;
-  lo.init(lane, role * DH);
-  FillPlan<D, 8> fp;
-  fp.init(wave, lane);
+  lo.init(lane, 0);
   const long q_stride = (long)hq * D;
   const int e0 = kt_ptr[g], e1 = kt_ptr[g + 1];
 
-  // Q and dO rows of one unit, and one per-row value by waves 0-2
-  // (log2-sum-exp, Delta, turn)
-  auto issue = [&](const Unit &u, int hi, unsigned short *__restrict__ nQ,
-                   unsigned short *__restrict__ nD, float *__restrict__ nL,
-                   float *__restrict__ nE, int *__restrict__ nM) __attribute__((always_inline)) {
+  // register-staged prefetch of one unit: Q and dO rows, and one per-row
+  // value by waves 0-2 (log2-sum-exp, Delta, turn)
+  StagePlan<D, 4> sp;
+  sp.init(wave, lane);
+  u16x8 stq[StagePlan<D, 4>::PW], sto[StagePlan<D, 4>::PW];
+  int stv = 0;
+  auto load = [&](const Unit &u, int hi) __attribute__((always_inline)) {
     const int h = hk * grp + hi;
-    fp.issue(nQ, q + (long)h * D + (long)tr.start * q_stride, q_stride, u.r0, u.vrows, wave);
-    fp.issue(nD, dout + (long)h * D + (long)tr.start * q_stride, q_stride, u.r0, u.vrows, wave);
+    sp.load(stq, q + (long)h * D + (long)tr.start * q_stride, q_stride, u.r0, u.vrows);
+    sp.load(sto, dout + (long)h * D + (long)tr.start * q_stride, q_stride, u.r0, u.vrows);
     const long lrow = tr.start + u.r0 + min(lane, u.vrows - 1);
-    if (wave == 0) fill64_dw(nL, lse2 + (long)h * P + lrow);
-    else if (wave == 1) fill64_dw(nE, delta + (long)h * P + lrow);
-    else if (wave == 2) fill64_dw(nM, tok_meta + lrow);
+    if (wave == 0) stv = __builtin_bit_cast(int, lse2[(long)h * P + lrow]);
+    else if (wave == 1) stv = __builtin_bit_cast(int, delta[(long)h * P + lrow]);
+    else if (wave == 2) stv = tok_meta[lrow];
   };
-  auto compute = [&](const Unit &u, const char *__restrict__ sQ, const char *__restrict__ sdO,
-                     const float *__restrict__ sLse, const float *__restrict__ sDel,
-                     const int *__restrict__ sMeta, f32x4 *__restrict__ eP,
-                     bf16x8 *__restrict__ edS) __attribute__((always_inline)) {
-    const char *sA = role == 0 ? sQ : sdO;  // S-role reads Q, dP-role reads dO
-    const int nqb = (u.vrows + 31) >> 5;
-    // FULL units with 64 query rows and every key of the tile valid need no
-    // predicate (kvalid is false only in a segment's last k-tile, which is
-    // a diagonal, PARTIAL tile)
-    const bool masked = u.partial | (u.vrows < 64);
+  auto store = [&](unsigned short *__restrict__ nQ, unsigned short *__restrict__ nD,
+                   float *__restrict__ nL, float *__restrict__ nE, int *__restrict__ nM)
+                   __attribute__((always_inline)) {
+    sp.store(nQ, stq, wave, lane);
+    sp.store(nD, sto, wave, lane);
+    if (wave == 0) nL[lane] = __builtin_bit_cast(float, stv);
+    else if (wave == 1) nE[lane] = __builtin_bit_cast(float, stv);
+    else if (wave == 2) nM[lane] = stv;
+  };
+  // S and dP of one 32-row block
+  auto sdp = [&](const char *__restrict__ sQ, const char *__restrict__ sdO, const int qb,
+                 f32x16 &s, f32x16 &dp) __attribute__((always_inline)) {
+    bf16x8 aq[KK], ad[KK];
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
-      if (qb >= nqb) break;
-      f32x4 *xp = eP + (qb * 4 + kg) * 4 * 64;   // [quarter][lane]
-      bf16x8 *xd = edS + (qb * 4 + kg) * 2 * 64;  // [c][lane]
-      // phase 1: S (role 0) or dP (role 1), queries on accumulator rows
-      bf16x8 af[KK];
+    for (int kk = 0; kk < KK; ++kk) {
+      aq[kk] = frag_row<D>(sQ, qb * 32, lo.row[kk]);
+      ad[kk] = frag_row<D>(sdO, qb * 32, lo.row[kk]);
+    }
+    s = f32x16{};
+    dp = f32x16{};
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) af[kk] = frag_row<D>(sA, qb * 32, lo.row[kk]);
-      f32x16 acc = f32x16{};
+    for (int kk = 0; kk < KK; ++kk) {
+      s = mfma32(aq[kk], kf[kk], s);
+      dp = mfma32(ad[kk], vf[kk], dp);
+    }
+    // Scheduling groups (mask 0x100: LDS reads, 0x008: MFMA), in program
+    // order for the whole unit: row reads run 4 ahead of the products.  The
+    // compiler's own schedule issues each read right before its product.
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) acc = mfma32(af[kk], kv_f[kk], acc);
-      bf16x8 pa[2], dsa[2];
-      if (role == 0) {
-        // P = exp2(S * scale - lse); a masked pair gets exponent -inf (P = 0).
-        // One uniform branch; inside, the predicate is bitwise.
-        if (__builtin_expect(masked, 0)) {
+    for (int i = 0; i < 2 * KK - 4; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+  };
+  // P = exp2(S * scale - lse) (a masked pair gets exponent -inf, P = 0) and
+  // dS = P (dP - Delta), packed to bf16
+  auto pds = [&](const Unit &u, const bool masked, const float *__restrict__ sLse,
+                 const float *__restrict__ sDel, const int *__restrict__ sMeta, const int qb,
+                 f32x16 &s, f32x16 &dp, bf16x8 (&pa)[2], bf16x8 (&dsa)[2])
+                 __attribute__((always_inline)) {
 #pragma unroll
-          for (int rg = 0; rg < 4; ++rg) {
-            const int base = qb * 32 + 8 * rg + 4 * hh;
-            const f32x4 L4 = *reinterpret_cast<const f32x4 *>(sLse + base);
-            const i32x4 M4 = *reinterpret_cast<const i32x4 *>(sMeta + base);
+    for (int rg = 0; rg < 4; ++rg) {
+      const int base = qb * 32 + 8 * rg + 4 * hh;
+      const f32x4 L4 = *reinterpret_cast<const f32x4 *>(sLse + base);
+      const f32x4 D4 = *reinterpret_cast<const f32x4 *>(sDel + base);
+      i32x4 M4;
+      if (masked) M4 = *reinterpret_cast<const i32x4 *>(sMeta + base);
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const int r = rg * 4 + j, ql = base + j;
-              const bool vis = kvalid & (ql < u.vrows) & (kr <= u.r0 + ql) & ((M4[j] >> 2) < kexp);
-              const float x = vis ? fmaf(acc[r], scale_log2, -L4[j]) : -INFINITY;
-              acc[r] = __builtin_amdgcn_exp2f(x);
-            }
-          }
-        } else {
-#pragma unroll
-          for (int rg = 0; rg < 4; ++rg) {
-            const f32x4 L4 = *reinterpret_cast<const f32x4 *>(sLse + qb * 32 + 8 * rg + 4 * hh);
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-              acc[rg * 4 + j] = __builtin_amdgcn_exp2f(fmaf(acc[rg * 4 + j], scale_log2, -L4[j]));
-          }
+      for (int j = 0; j < 4; ++j) {
+        const int r = rg * 4 + j, ql = base + j;
+        float x = fmaf(s[r], scale_log2, -L4[j]);
+        if (masked) {
+          const bool vis = kvalid & (ql < u.vrows) & (kr <= u.r0 + ql) & ((M4[j] >> 2) < kexp);
+          x = vis ? x : -INFINITY;
         }
-#pragma unroll
-        for (int rg = 0; rg < 4; ++rg)
-          xp[rg * 64 + lane] = f32x4{acc[rg * 4], acc[rg * 4 + 1], acc[rg * 4 + 2], acc[rg * 4 + 3]};
-        pa[0] = pack8(acc, 0);
-        pa[1] = pack8(acc, 8);
-      }
-      lds_barrier();
-      if (role == 1) {
-        f32x16 pv;
-#pragma unroll
-        for (int rg = 0; rg < 4; ++rg) {
-          const f32x4 p4 = xp[rg * 64 + lane];
-          const f32x4 D4 = *reinterpret_cast<const f32x4 *>(sDel + qb * 32 + 8 * rg + 4 * hh);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            pv[rg * 4 + j] = p4[j];
-            acc[rg * 4 + j] = p4[j] * (acc[rg * 4 + j] - D4[j]);
-          }
-        }
-        pa[0] = pack8(pv, 0);
-        pa[1] = pack8(pv, 8);
-        dsa[0] = pack8(acc, 0);
-        dsa[1] = pack8(acc, 8);
-        xd[lane] = dsa[0];
-        xd[64 + lane] = dsa[1];
-      }
-      // dV half += P^T dO[:, half]  (role 0 while role 1 forms dS)
-#pragma unroll
-      for (int c2 = 0; c2 < 2; ++c2) {
-        bf16x8 bo[DBH];
-#pragma unroll
-        for (int db = 0; db < DBH; ++db)
-          bo[db] = frag_tr<D>(sdO, qb * 32 + c2 * 16, lo.tra[db], lo.trb[db]);
-#pragma unroll
-        for (int db = 0; db < DBH; ++db) dvacc[db] = mfma32(pa[c2], bo[db], dvacc[db]);
-      }
-      lds_barrier();
-      if (role == 0) {
-        dsa[0] = xd[lane];
-        dsa[1] = xd[64 + lane];
-      }
-      // dK half += dS^T Q[:, half]
-#pragma unroll
-      for (int c2 = 0; c2 < 2; ++c2) {
-        bf16x8 bq[DBH];
-#pragma unroll
-        for (int db = 0; db < DBH; ++db)
-          bq[db] = frag_tr<D>(sQ, qb * 32 + c2 * 16, lo.tra[db], lo.trb[db]);
-#pragma unroll
-        for (int db = 0; db < DBH; ++db) dkacc[db] = mfma32(dsa[c2], bq[db], dkacc[db]);
+        s[r] = __builtin_amdgcn_exp2f(x);
+        dp[r] = s[r] * (dp[r] - D4[j]);
       }
     }
+    pa[0] = pack8(s, 0);
+    pa[1] = pack8(s, 8);
+    dsa[0] = pack8(dp, 0);
+    dsa[1] = pack8(dp, 8);
+    // this block's lse / Delta (/ turn) reads form their own group, so they
+    // do not take the slots of the transpose reads below
+    if (masked)
+      __builtin_amdgcn_sched_group_barrier(0x100, 12, 0);
+    else
+      __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+  };
+  // dV += P^T dO, dK += dS^T Q for one 32-row block
+  auto dkv = [&](const char *__restrict__ sQ, const char *__restrict__ sdO, const int qb,
+                 const bf16x8 (&pa)[2], const bf16x8 (&dsa)[2]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int c2 = 0; c2 < 2; ++c2) {
+      bf16x8 bo[DB], bq[DB];
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        bo[db] = frag_tr<D>(sdO, qb * 32 + c2 * 16, lo.tra[db], lo.trb[db]);
+        bq[db] = frag_tr<D>(sQ, qb * 32 + c2 * 16, lo.tra[db], lo.trb[db]);
+      }
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        dvacc[db] = mfma32(pa[c2], bo[db], dvacc[db]);
+        dkacc[db] = mfma32(dsa[c2], bq[db], dkacc[db]);
+      }
+    }
+    // transpose reads run 4 fragments ahead of the products
+    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+    for (int i = 0; i < 4 * DB - 4; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+  };
+  // One unit, software-pipelined over its two 32-row blocks: the S/dP
+  // products of block 1 are issued before the softmax of block 0, and the
+  // softmax of block 1 sits beside the dV/dK products of block 0.
+  // FULL units with 64 query rows and every key of the tile valid need no
+  // predicate (kvalid is false only in a segment's last k-tile, which is a
+  // diagonal, PARTIAL tile); rows past vrows hold copies of the last row and
+  // are masked.  `masked` is a constant in each inlined copy.
+  auto compute = [&](const Unit &u, const bool masked, const char *__restrict__ sQ,
+                     const char *__restrict__ sdO, const float *__restrict__ sLse,
+                     const float *__restrict__ sDel, const int *__restrict__ sMeta)
+                     __attribute__((always_inline)) {
+    f32x16 s0, dp0, s1, dp1;
+    bf16x8 pa0[2], ds0[2], pa1[2], ds1[2];
+    sdp(sQ, sdO, 0, s0, dp0);
+    sdp(sQ, sdO, 1, s1, dp1);
+    pds(u, masked, sLse, sDel, sMeta, 0, s0, dp0, pa0, ds0);
+    dkv(sQ, sdO, 0, pa0, ds0);
+    pds(u, masked, sLse, sDel, sMeta, 1, s1, dp1, pa1, ds1);
+    dkv(sQ, sdO, 1, pa1, ds1);
   };
   auto step = [&](const Unit &u, const bool more, const Unit &nu, int nhi,
                   const unsigned short *__restrict__ cQ, const unsigned short *__restrict__ cD,
                   const float *__restrict__ cL, const float *__restrict__ cE,
                   const int *__restrict__ cM, unsigned short *__restrict__ nQ,
                   unsigned short *__restrict__ nD, float *__restrict__ nL, float *__restrict__ nE,
-                  int *__restrict__ nM, f32x4 *__restrict__ eP, bf16x8 *__restrict__ edS)
-                  __attribute__((always_inline)) {
-    if (more) issue(nu, nhi, nQ, nD, nL, nE, nM);
-    compute(u, reinterpret_cast<const char *>(cQ), reinterpret_cast<const char *>(cD), cL, cE, cM,
-            eP, edS);
+                  int *__restrict__ nM) __attribute__((always_inline)) {
+    if (more) load(nu, nhi);  // in flight during the products below
+    const char *q8 = reinterpret_cast<const char *>(cQ), *d8 = reinterpret_cast<const char *>(cD);
+    if (__builtin_expect(u.partial | (u.vrows < 64), 0))
+      compute(u, true, q8, d8, cL, cE, cM);
+    else
+      compute(u, false, q8, d8, cL, cE, cM);
+    if (more) store(nQ, nD, nL, nE, nM);
   };
 
   if (e0 < e1) {
-    int cbase = e0;  // first entry staged in `ent`
-    stage_entries<CAP, 512>(ent, kt_row, kt_cls, cbase, e1);
     // next unit: other half of this tile, else next head, else next entry
     auto advance = [&](const Unit &cu, int chi, Unit &n, int &nh) __attribute__((always_inline)) -> bool {
       if (cu.half == 0 && cu.r0 + 64 < tr.len) {
@@ -736,28 +743,27 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
         n.vrows = min(64, tr.len - n.r0);
         nh = chi + 1;
       } else if (cu.e + 1 < e1) {
-        n = unit_at<CAP, 512>(ent, cbase, cu.e + 1, 0, e1, kt_row, kt_cls, tr.qbase, tr.len);
+        n = make_unit(kt_row, kt_cls, cu.e + 1, 0, tr.qbase, tr.len);
         nh = 0;
       } else {
         return false;
       }
       return true;
     };
-    f32x4 *eP = &xP[0][0][0][0];
-    bf16x8 *edS = &xdS[0][0][0][0];
-    Unit cur = unit_at<CAP, 512>(ent, cbase, e0, 0, e1, kt_row, kt_cls, tr.qbase, tr.len), nx;
+    Unit cur = make_unit(kt_row, kt_cls, e0, 0, tr.qbase, tr.len), nx;
     int hcur = 0, hnx = 0;
-    issue(cur, hcur, sQ0, sD0, sL0, sE0, sM0);
-    wait_all_and_sync();
+    load(cur, hcur);
+    store(sQ0, sD0, sL0, sE0, sM0);
+    __syncthreads();
     for (;;) {
       bool more = advance(cur, hcur, nx, hnx);
-      step(cur, more, nx, hnx, sQ0, sD0, sL0, sE0, sM0, sQ1, sD1, sL1, sE1, sM1, eP, edS);
+      step(cur, more, nx, hnx, sQ0, sD0, sL0, sE0, sM0, sQ1, sD1, sL1, sE1, sM1);
       __syncthreads();
       if (!more) break;
       cur = nx;
       hcur = hnx;
       more = advance(cur, hcur, nx, hnx);
-      step(cur, more, nx, hnx, sQ1, sD1, sL1, sE1, sM1, sQ0, sD0, sL0, sE0, sM0, eP, edS);
+      step(cur, more, nx, hnx, sQ1, sD1, sL1, sE1, sM1, sQ0, sD0, sL0, sE0, sM0);
       __syncthreads();
       if (!more) break;
       cur = nx;
@@ -765,25 +771,25 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
     }
   }
 
-  // stage through LDS (one 64-row tile, RP key rows per pass) for coalesced
-  // stores; accumulator D[i = key][j = d]
+  // stage through LDS (RP key rows per pass) for coalesced stores;
+  // accumulator D[i = key][j = d]
   wait_all_and_sync();
   TO *st = reinterpret_cast<TO *>(sQ0);
-  constexpr int CH = 16 / sizeof(TO);       // elements per 16-byte chunk
-  constexpr int RP = 128 / sizeof(TO);      // key rows per pass (16 KB)
+  constexpr int CH = 16 / sizeof(TO);   // elements per 16-byte chunk
+  constexpr int RP = 128 / sizeof(TO);  // key rows per pass (16 KB)
 #pragma unroll
   for (int which = 0; which < 2; ++which) {
     TO *dst = which == 0 ? dk : dv;
 #pragma unroll
     for (int pass = 0; pass < TQ / RP; ++pass) {
-      if (kg * 32 >= pass * RP && kg * 32 < (pass + 1) * RP) {
+      if (wave * 32 >= pass * RP && wave * 32 < (pass + 1) * RP) {
 #pragma unroll
-        for (int db = 0; db < DBH; ++db)
+        for (int db = 0; db < DB; ++db)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const int kl = kg * 32 + 8 * (r >> 2) + 4 * hh + (r & 3) - pass * RP;
+            const int kl = wave * 32 + 8 * (r >> 2) + 4 * hh + (r & 3) - pass * RP;
             const float val = which == 0 ? dkacc[db][r] * scale : dvacc[db][r];
-            const int dd = role * DH + db * 32 + col;
+            const int dd = db * 32 + col;
             if constexpr (sizeof(TO) == 2)
               st[kl * D + dd] = f2bf_bits(val);
             else
@@ -791,7 +797,7 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
           }
       }
       __syncthreads();
-      for (int c = threadIdx.x; c < RP * D / CH; c += 512) {
+      for (int c = threadIdx.x; c < RP * D / CH; c += 256) {
         const int kl = c / (D / CH), ch = c % (D / CH);
         const int key = pass * RP + kl;
         if (key < tr.nrows) {
@@ -1035,7 +1041,7 @@ void bwd_impl(const seg_layout *L, const seg_sizes *sz, int hq, int hkv, float s
   }
   {
     ProfScope prof("attn_bwd_dkdv", st);
-    k_attn_bwd_dkdv<D, TO><<<xcd_grid(G, hkv), 512, 0, st>>>(
+    k_attn_bwd_dkdv<D, TO><<<xcd_grid(G, hkv), 256, 0, st>>>(
         q, k, v, dout, lse2, delta, L->seg_info, L->tile_seg, L->tok_meta, L->kt_ptr, L->kt_row,
         L->kt_cls, G, hq, hkv, L->window, scale * LOG2E, scale, P, static_cast<TO *>(dk),
         static_cast<TO *>(dv));
