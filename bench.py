@@ -11,8 +11,11 @@ same kernels) runs the same step for the comparison.
 
 Prints one JSON line.  `value` is the algorithmic attention forward+backward
 throughput (12*d FLOP per visible (query, key) pair per query head) over the
-device time of the two attention calls; `ms_per_step` and the trajectory
-token rates cover the whole step.
+device time of the two attention calls (the FlashAttention convention, 14*d
+with a 10*d backward that counts the recompute of S, is reported alongside as
+attn_tflops_fa_convention); `ms_per_step` and the trajectory token rates cover
+the whole step.  roofline.traffic is the counter-measured HBM bytes of one
+launch of the dominant kernel (see MEASURED_TRAFFIC).
 """
 from __future__ import annotations
 
@@ -31,8 +34,35 @@ PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 # algorithmic FLOP per visible pair per query head and per head-dim element
 KERNEL_FLOP_PER_PAIR_D = {"attn_fwd": 4, "attn_bwd_dkdv": 6, "attn_bwd_dq": 2}
+# HBM bytes per launch of the attention kernels on the 7b workload: rocprofv3
+# --pmc FETCH_SIZE and WRITE_SIZE passes over `bench.py --pmc-driver`, each
+# scaled by what the same counter reads for the f32->bf16 streaming kernel
+# over a known byte count (reads x2.000, writes x1.000).  They describe the
+# kernel source they were taken on and are reported only while it is unchanged.
+MEASURED_TRAFFIC = {
+    "source": "paper_2607_11185_amd/csrc/seg_attn.hip",
+    "source_sha256": "3fdf29bcd98aa80413d76269076a261276bd776473dc16771c9572836c947922",
+    "config": "7b",
+    "bytes_per_launch": {"attn_bwd_dkdv": 527.33e9, "attn_fwd": 280.35e9,
+                         "attn_bwd_dq": 308.78e9},
+}
 KERNELS = ["layout", "attn_prep", "attn_fwd", "attn_delta", "attn_bwd_dkdv", "attn_bwd_dq",
            "lp_prep", "logits", "row_loss", "dz", "dh", "dw"]
+
+
+def measured_traffic(cfg_name, kernel):
+    """Counter-derived HBM bytes of `kernel` for this workload, or None when the
+    kernel source has changed since the counters were taken."""
+    import hashlib
+    m = MEASURED_TRAFFIC
+    if cfg_name != m["config"] or kernel not in m["bytes_per_launch"]:
+        return None
+    try:
+        with open(os.path.join(ROOT, m["source"]), "rb") as f:
+            digest = hashlib.sha256(f.read()).hexdigest()
+    except OSError:
+        return None
+    return m["bytes_per_launch"][kernel] if digest == m["source_sha256"] else None
 
 
 def log(*a):
@@ -155,6 +185,8 @@ def time_path(run, steps, warmup, profile=True):
         ph["attn_bwd"] += e["t3"].elapsed_time(e["t4"])
         ph["step"] += e["t0"].elapsed_time(e["t4"])
     ph = {k: v / steps for k, v in ph.items()}
+    per_step = sorted(e["t0"].elapsed_time(e["t4"]) for e in evs)
+    ph["step_median"] = per_step[len(per_step) // 2]
     kern = {}
     import ctypes
     for name in KERNELS:
@@ -200,6 +232,76 @@ def cpu_baseline(cfg, budget_note):
             "seconds": dt}
 
 
+def _host_bf16_rows(gen, rows, dev, what, chunk=1 << 16):
+    """bf16 device tensor of generator rows, produced on the host in chunks
+    (no GPU kernel runs: the counter passes profile only the path's kernels)."""
+    import numpy as np
+    import torch
+
+    from paper_2607_11185_amd import workload as WL
+    first = gen(rows[:1])
+    out = np.empty((len(rows),) + first.shape[1:], np.uint16)
+    for c0 in range(0, len(rows), chunk):
+        x = gen(rows[c0:c0 + chunk])
+        out[c0:c0 + len(x)] = WL.bf16_round_np(x.astype(np.float32))
+        if (c0 // chunk) % 4 == 0:
+            log(f"  {what}: rows {c0 + len(x)}/{len(rows)}")
+    return torch.from_numpy(out).view(torch.bfloat16).to(dev)
+
+
+def pmc_driver(cfg_name):
+    """One launch of each attention kernel on the workload, then one launch
+    of the f32->bf16 conversion kernel over a known number of bytes (the
+    plain streaming kernel that calibrates the HBM byte counters).  Inputs
+    are generated on the host; prints one JSON line with the sizes."""
+    import numpy as np
+    import torch
+
+    from paper_2607_11185_amd import seg as S
+    from paper_2607_11185_amd import workload as WL
+    dev = torch.device("cuda:0")
+    cfg = WL.CONFIGS[cfg_name]
+    inp = WL.Inputs(cfg)
+    pr = S.Problem.from_spans(inp.spans, cfg.window, cfg.seg_steps, cfg.max_seg_tokens,
+                              cfg.buffer_tokens, 128)
+    lay = S.seg_build_layout(pr, device=dev)
+    host = lay.host()
+    src = host["tok_src"].astype(np.int64)
+    src[src < 0] = 0
+    P = lay.sizes.packed_tokens
+    q = _host_bf16_rows(inp.q_np, src, dev, "q")
+    k = _host_bf16_rows(inp.k_np, src, dev, "k")
+    v = _host_bf16_rows(inp.v_np, src, dev, "v")
+    dout = _host_bf16_rows(inp.dout_np, np.arange(P), dev, "dout")
+    torch.cuda.synchronize()
+    log("inputs ready")
+    sc = 1.0 / math.sqrt(cfg.head_dim)
+    o, lse = S.seg_attn_fwd(lay, q, k, v, sc)
+    S.seg_attn_bwd(lay, q, k, v, o, lse, dout, sc)
+    torch.cuda.synchronize()
+    pairs = int(host["seg_pairs"].sum())
+    del q, k, v, dout, o, lse
+    torch.cuda.empty_cache()
+    # calibration: 4096 one-turn samples of 256 tokens, 8 heads, d = 128, f32
+    # inputs; the forward converts q, k and v with one streaming kernel each
+    n_s, hc, d = 4096, 8, 128
+    sp = WL.explicit_spans([1] * n_s, [236] * n_s, [0] * n_s, [20] * n_s, [4] * n_s)
+    cal = S.seg_build_layout(S.Problem.from_spans(sp, 1, 1), device=dev)
+    Pc = cal.sizes.packed_tokens
+    zeros = np.zeros((Pc, hc, d), np.float32)
+    qc = torch.from_numpy(zeros).to(dev)
+    kc = torch.from_numpy(zeros).to(dev)
+    vc = torch.from_numpy(zeros).to(dev)
+    torch.cuda.synchronize()
+    S.seg_attn_fwd(cal, qc, kc, vc, sc)
+    torch.cuda.synchronize()
+    n = Pc * hc * d
+    print(json.dumps({"config": cfg.name, "packed_tokens": P, "visible_pairs_per_head": pairs,
+                      "calibration": {"kernel": "k_f32_to_bf16", "elements": n,
+                                      "read_bytes": 4 * n, "write_bytes": 2 * n,
+                                      "launches": 3}}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -208,6 +310,9 @@ def main():
     ap.add_argument("--config", default="7b", help="workload name (7b, small, long, tiny)")
     ap.add_argument("--no-stepwise", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--pmc-driver", action="store_true",
+                    help="one launch of each attention kernel plus a calibration copy, for "
+                         "rocprofv3 --pmc counter passes (no timing, no JSON bench line)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the segmented path runs on a single MI355X and this "
@@ -220,6 +325,9 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
+    if args.pmc_driver:
+        pmc_driver(args.config)
+        return
     dev = torch.device("cuda:0")
     cfg = WL.CONFIGS[args.config]
 
@@ -248,12 +356,14 @@ def main():
                    "segments": seg.sizes.num_segments, "visible_pairs_per_head": seg.pairs},
         "traj_tokens_per_s": round(traj_tokens / (ph["step"] * 1e-3), 1),
         "attn_ms": round(attn_ms, 3),
+        "attn_tflops_fa_convention": round(seg.attn_flop() * 14.0 / 12.0 / (attn_ms * 1e-3) / 1e12, 2),
         "phases_ms": {k: round(v, 3) for k, v in ph.items()},
         "kernels_ms": {k: round(v["ms_per_step"], 3) for k, v in kern.items()},
         "wall_ms_per_step": round(wall_ms, 3),
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": measured_traffic(cfg.name, dom),
                      "flop_per_launch": dom_flop, "ms_per_launch": round(dom_ms, 3)},
     }
     seg.free()
