@@ -692,9 +692,9 @@ __global__ void __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
   };
-  // One unit, software-pipelined over its two 32-row blocks: the S/dP
-  // products of block 1 are issued before the softmax of block 0, and the
-  // softmax of block 1 sits beside the dV/dK products of block 0.
+  // One unit over its two 32-row blocks, in the order S/dP(0), softmax(0),
+  // S/dP(1), dV/dK(0), softmax(1), dV/dK(1) (measured best among the orders
+  // tried; it also keeps the live state within the register budget).
   // FULL units with 64 query rows and every key of the tile valid need no
   // predicate (kvalid is false only in a segment's last k-tile, which is a
   // diagonal, PARTIAL tile); rows past vrows hold copies of the last row and
@@ -706,8 +706,8 @@ __global__ void __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 
     f32x16 s0, dp0, s1, dp1;
     bf16x8 pa0[2], ds0[2], pa1[2], ds1[2];
     sdp(sQ, sdO, 0, s0, dp0);
-    sdp(sQ, sdO, 1, s1, dp1);
     pds(u, masked, sLse, sDel, sMeta, 0, s0, dp0, pa0, ds0);
+    sdp(sQ, sdO, 1, s1, dp1);
     dkv(sQ, sdO, 0, pa0, ds0);
     pds(u, masked, sLse, sDel, sMeta, 1, s1, dp1, pa1, ds1);
     dkv(sQ, sdO, 1, pa1, ds1);
@@ -728,26 +728,34 @@ __global__ void __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 
   };
 
   if (e0 < e1) {
-    // next unit: other half of this tile, else next head, else next entry
+    // Next unit: other half of this tile, else next head, else next entry.
+    // Every field is computed from scalars: partial assignments of a
+    // struct in different branches ended up in dynamically indexed private
+    // memory, whose loads wait behind the prefetch loads.
     auto advance = [&](const Unit &cu, int chi, Unit &n, int &nh) __attribute__((always_inline)) -> bool {
-      if (cu.half == 0 && cu.r0 + 64 < tr.len) {
-        n = cu;
-        n.half = 1;
-        n.r0 = cu.r0 + 64;
-        n.vrows = min(64, tr.len - n.r0);
+      const bool second = cu.half == 0 && cu.r0 + 64 < tr.len;
+      const bool head = !second && chi + 1 < grp;
+      const bool entry = !second && !head && cu.e + 1 < e1;
+      if (!(second || head || entry)) return false;
+      int e = cu.e, half = 0, r0, partial = cu.partial;
+      if (second) {
+        half = 1;
+        r0 = cu.r0 + 64;
         nh = chi;
-      } else if (chi + 1 < grp) {
-        n = cu;
-        n.half = 0;
-        n.r0 = cu.r0 - cu.half * 64;
-        n.vrows = min(64, tr.len - n.r0);
+      } else if (head) {
+        r0 = cu.r0 - cu.half * 64;
         nh = chi + 1;
-      } else if (cu.e + 1 < e1) {
-        n = make_unit(kt_row, kt_cls, cu.e + 1, 0, tr.qbase, tr.len);
-        nh = 0;
       } else {
-        return false;
+        e = cu.e + 1;
+        r0 = (kt_row[e] - tr.qbase) * TQ;
+        partial = kt_cls[e] == SEG_TILE_PARTIAL;
+        nh = 0;
       }
+      n.e = e;
+      n.half = half;
+      n.r0 = r0;
+      n.vrows = min(64, tr.len - r0);
+      n.partial = partial;
       return true;
     };
     Unit cur = make_unit(kt_row, kt_cls, e0, 0, tr.qbase, tr.len), nx;
