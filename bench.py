@@ -3,8 +3,10 @@
 
 One step = the whole hot path over one batch: segmentation and packed layout
 with its tile map (seg_layout_query + seg_build_layout), masked GQA attention
-forward, the fused action-token log-prob / clipped-ratio loss with its
-gradients, and attention backward.  Inputs (packed q/k/v/dO, hidden states,
+forward, the fused action-token log-prob / clipped-ratio loss with its KL
+penalty (lambda = 1e-4) and gradients, and attention backward.  The reference
+/ old-policy forward pass (attention forward + forward-only log-prob) is timed
+separately for both decompositions (reference_forward_ms).  Inputs (packed q/k/v/dO, hidden states,
 projection, targets, advantages, rollout log-probs) are resident in HBM before
 the timed region.  The step-wise decomposition (every turn its own sample,
 same kernels) runs the same step for the comparison.
@@ -46,6 +48,7 @@ MEASURED_TRAFFIC = {
     "bytes_per_launch": {"attn_bwd_dkdv": 527.33e9, "attn_fwd": 280.35e9,
                          "attn_bwd_dq": 308.78e9},
 }
+KL_COEF = 1e-4  # the paper's KL penalty lambda (hyperparameter table)
 KERNELS = ["layout", "attn_prep", "attn_fwd", "attn_delta", "attn_bwd_dkdv", "attn_bwd_dq",
            "lp_prep", "logits", "row_loss", "dz", "dh", "dw"]
 
@@ -115,6 +118,7 @@ class PathRun:
             "logp": torch.empty(R, dtype=torch.float32, device=dev),
             "loss_tok": torch.empty(R, dtype=torch.float32, device=dev),
             "clipped": torch.empty(R, dtype=torch.uint8, device=dev),
+            "kl_tok": torch.empty(R, dtype=torch.float32, device=dev),
             "loss_sum": torch.empty(1, dtype=torch.float32, device=dev),
             "dh": torch.empty((R, cfg.hidden), dtype=torch.bfloat16, device=dev),
             "dw": torch.empty((cfg.vocab, cfg.hidden), dtype=torch.float32, device=dev),
@@ -124,11 +128,15 @@ class PathRun:
         fwd_only = S.LossCfg(cfg.eps_low, cfg.eps_high, 0.0, 1.0 / R, 1.0, False)
         zero = torch.zeros(R, dtype=torch.float32, device=dev)
         S.seg_logprob_loss(self.h, self.lay.loss_pred_row, self.w, self.tgt, zero, self.adv,
-                           self.lay.loss_traj, fwd_only, out=dict(self.lp_out, dh=None, dw=None),
-                           ws=self.ws_lp)
+                           self.lay.loss_traj, fwd_only,
+                           out=dict(self.lp_out, dh=None, dw=None, kl_tok=None), ws=self.ws_lp)
         noise = torch.from_numpy(inp.old_noise_np(host["loss_tgt_src"]).astype(np.float32)).to(dev)
         self.old = (self.lp_out["logp"] + noise).contiguous()
-        self.loss_cfg = S.LossCfg(cfg.eps_low, cfg.eps_high, 0.0, 1.0 / R, 1.0, True)
+        # reference-policy log-probs: the current ones minus the same noise
+        self.ref = (self.lp_out["logp"] - noise).contiguous()
+        self.loss_cfg = S.LossCfg(cfg.eps_low, cfg.eps_high, 0.0, 1.0 / R, 1.0, True, KL_COEF)
+        self.ref_cfg = fwd_only
+        self.ref_out = dict(self.lp_out, dh=None, dw=None, kl_tok=None)
         torch.cuda.synchronize()
 
     def step(self, ev=None):
@@ -142,11 +150,25 @@ class PathRun:
                        ws=self.ws_fwd)
         rec("t2")
         S.seg_logprob_loss(self.h, self.lay.loss_pred_row, self.w, self.tgt, self.old, self.adv,
-                           self.lay.loss_traj, self.loss_cfg, out=self.lp_out, ws=self.ws_lp)
+                           self.lay.loss_traj, self.loss_cfg, out=self.lp_out, ws=self.ws_lp,
+                           ref_logp=self.ref)
         rec("t3")
         S.seg_attn_bwd(self.lay, self.q, self.k, self.v, self.o, self.lse, self.dout, self.scale,
                        dq=self.dq, dk=self.dk, dv=self.dv, ws=self.ws_bwd)
         rec("t4")
+
+    def ref_forward(self, ev=None):
+        """The reference / old-policy pass: attention forward and the
+        forward-only log-prob of the action rows (no gradients)."""
+        S = self.S
+        rec = (lambda name: ev[name].record()) if ev is not None else (lambda name: None)
+        rec("r0")
+        S.seg_attn_fwd(self.lay, self.q, self.k, self.v, self.scale, o=self.o, lse=self.lse,
+                       ws=self.ws_fwd)
+        rec("r1")
+        S.seg_logprob_loss(self.h, self.lay.loss_pred_row, self.w, self.tgt, self.old, self.adv,
+                           self.lay.loss_traj, self.ref_cfg, out=self.ref_out, ws=self.ws_lp)
+        rec("r2")
 
     def attn_flop(self):
         c = self.cfg
@@ -197,6 +219,22 @@ def time_path(run, steps, warmup, profile=True):
             kern[name] = {"ms_per_step": tot.value / steps, "launches_per_step": n.value / steps}
     L.seg_profile_reset()
     return ph, kern, wall / steps * 1e3
+
+
+def time_ref(run, steps, warmup):
+    """Mean device ms of the reference forward pass (attention, log-prob)."""
+    import torch
+    for _ in range(warmup):
+        run.ref_forward()
+    torch.cuda.synchronize()
+    evs = [{n: torch.cuda.Event(enable_timing=True) for n in ("r0", "r1", "r2")}
+           for _ in range(steps)]
+    for i in range(steps):
+        run.ref_forward(evs[i])
+    torch.cuda.synchronize()
+    att = sum(e["r0"].elapsed_time(e["r1"]) for e in evs) / steps
+    lp = sum(e["r1"].elapsed_time(e["r2"]) for e in evs) / steps
+    return {"attn_fwd": round(att, 3), "logprob": round(lp, 3), "total": round(att + lp, 3)}
 
 
 def cpu_baseline(cfg, budget_note):
@@ -333,6 +371,7 @@ def main():
 
     seg = PathRun(cfg, dev)
     ph, kern, wall_ms = time_path(seg, args.steps, args.warmup)
+    ref_seg = time_ref(seg, args.steps, args.warmup)
     attn_ms = ph["attn_fwd"] + ph["attn_bwd"]
     value = seg.attn_flop() / (attn_ms * 1e-3) / 1e12
     traj_tokens = seg.sizes.traj_tokens
@@ -365,6 +404,8 @@ def main():
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": measured_traffic(cfg.name, dom),
                      "flop_per_launch": dom_flop, "ms_per_launch": round(dom_ms, 3)},
+        "kl_coef": KL_COEF,
+        "reference_forward_ms": ref_seg,
     }
     seg.free()
     del seg
@@ -374,6 +415,7 @@ def main():
         sw_cfg = cfg.with_(name=cfg.name + "_stepwise", seg_steps=1)
         sw = PathRun(sw_cfg, dev)
         ph2, kern2, _ = time_path(sw, args.steps, args.warmup)
+        ref_sw = time_ref(sw, args.steps, args.warmup)
         attn2 = ph2["attn_fwd"] + ph2["attn_bwd"]
         out["stepwise"] = {
             "ms_per_step": round(ph2["step"], 3),
@@ -384,6 +426,8 @@ def main():
             "phases_ms": {k: round(v, 3) for k, v in ph2.items()},
         }
         out["speedup_vs_stepwise"] = round(ph2["step"] / ph["step"], 3)
+        out["stepwise"]["reference_forward_ms"] = ref_sw
+        out["reference_forward_speedup_vs_stepwise"] = round(ref_sw["total"] / ref_seg["total"], 3)
         sw.free()
         del sw
         torch.cuda.empty_cache()

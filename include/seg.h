@@ -183,12 +183,14 @@ seg_status seg_attn_bwd(const seg_layout *L, const seg_sizes *sz, seg_dtype dt, 
                         size_t ws_bytes, hipStream_t stream);
 
 /*
- * Settings of the clipped policy-ratio objective (Eq. (loss), App. E):
- * per row, rho = exp(logp - old_logp), A = adv[row_traj];
+ * Settings of the clipped policy-ratio objective with its KL penalty
+ * (Eq. (loss), App. E): per row, rho = exp(logp - old_logp), A = adv[row_traj];
  * objective = min(rho A, clip(rho, 1 - eps_low, 1 + eps_high) A), and when
  * dual_clip_c > 0 and A < 0, objective = max(objective, dual_clip_c A);
- * loss_tok = -objective; loss_sum = loss_scale * sum(loss_tok).  Logits are
- * logit_scale * h W^T.  Clipping uses strict inequalities.
+ * kl = exp(ref_logp - logp) - (ref_logp - logp) - 1 (the per-token estimator
+ * of KL(pi_theta || pi_ref) used by GRPO; the paper does not name one);
+ * loss_tok = -objective + kl_coef * kl; loss_sum = loss_scale * sum(loss_tok).
+ * Logits are logit_scale * h W^T.  Clipping uses strict inequalities.
  */
 typedef struct {
   float eps_low;
@@ -197,27 +199,33 @@ typedef struct {
   float loss_scale;
   float logit_scale;
   int32_t want_grad;  /* 0: forward only (dh and dw untouched, may be NULL) */
+  float kl_coef;      /* lambda >= 0 of the KL penalty; > 0 needs ref_logp */
 } seg_loss_cfg;
 
 size_t seg_logprob_workspace_bytes(int32_t rows, int32_t hidden, int32_t vocab, seg_dtype dt);
 
 /*
- * Fused action-token log-prob, clipped-ratio loss and gradients.
+ * Fused action-token log-prob, clipped-ratio loss with KL penalty, and
+ * gradients (Eq. (loss), App. E).
  *   h [n_h, hidden] (dtype dt) hidden states; row_index [rows] selects the rows
  *   of h to use (e.g. loss_pred_row), or NULL to use rows 0..rows-1;
  *   w [vocab, hidden] (dtype dt) output projection; target [rows] token ids in
- *   [0, vocab); old_logp [rows] fp32 rollout log-probs; adv [num_traj] fp32;
- *   row_traj [rows] index into adv.
+ *   [0, vocab); old_logp [rows] fp32 rollout log-probs; ref_logp [rows] fp32
+ *   reference-policy log-probs, or NULL when cfg->kl_coef == 0 (else
+ *   SEG_ERR_ARG); adv [num_traj] fp32; row_traj [rows] index into adv.
  * Outputs: logp, loss_tok [rows] fp32; clipped [rows] (1 where the clipped
- * branch is taken, so the row has no gradient); loss_sum [1] fp32;
+ * branch of the ratio term is taken, so that term has no gradient); kl_tok
+ * [rows] fp32 per-token KL estimate, or NULL; loss_sum [1] fp32;
  * with want_grad: dh [rows, hidden] (dtype dt) and dw [vocab, hidden] fp32
- * (overwritten), the gradients of loss_sum.
+ * (overwritten), the gradients of loss_sum.  A forward-only call
+ * (want_grad = 0) is the reference / old-policy log-prob pass.
  */
 seg_status seg_logprob_loss(int32_t rows, int32_t hidden, int32_t vocab, seg_dtype dt,
                             const void *h, const int32_t *row_index, const void *w,
-                            const int32_t *target, const float *old_logp, const float *adv,
-                            const int32_t *row_traj, int32_t num_traj, const seg_loss_cfg *cfg,
-                            float *logp, float *loss_tok, uint8_t *clipped, float *loss_sum,
+                            const int32_t *target, const float *old_logp,
+                            const float *ref_logp, const float *adv, const int32_t *row_traj,
+                            int32_t num_traj, const seg_loss_cfg *cfg, float *logp,
+                            float *loss_tok, uint8_t *clipped, float *kl_tok, float *loss_sum,
                             void *dh, float *dw, void *ws, size_t ws_bytes,
                             hipStream_t stream);
 

@@ -58,7 +58,8 @@ class SegLayout(ctypes.Structure):
 class SegLossCfg(ctypes.Structure):
     _fields_ = [("eps_low", ctypes.c_float), ("eps_high", ctypes.c_float),
                 ("dual_clip_c", ctypes.c_float), ("loss_scale", ctypes.c_float),
-                ("logit_scale", ctypes.c_float), ("want_grad", ctypes.c_int32)]
+                ("logit_scale", ctypes.c_float), ("want_grad", ctypes.c_int32),
+                ("kl_coef", ctypes.c_float)]
 
 
 class SegError(RuntimeError):
@@ -101,9 +102,12 @@ def lib() -> ctypes.CDLL:
         L.seg_logprob_workspace_bytes.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                                   ctypes.c_int]
         L.seg_logprob_loss.restype = ctypes.c_int
+        # rows, hidden, vocab, dt, h, row_index, w, target, old_logp, ref_logp, adv,
+        # row_traj, num_traj, cfg, logp, loss_tok, clipped, kl_tok, loss_sum, dh, dw, ws,
+        # ws_bytes, stream
         L.seg_logprob_loss.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int,
-                                       VP, VP, VP, VP, VP, VP, VP, ctypes.c_int32,
-                                       ctypes.POINTER(SegLossCfg), VP, VP, VP, VP, VP, VP, VP,
+                                       VP, VP, VP, VP, VP, VP, VP, VP, ctypes.c_int32,
+                                       ctypes.POINTER(SegLossCfg), VP, VP, VP, VP, VP, VP, VP, VP,
                                        ctypes.c_size_t, VP]
         L.seg_profile_enable.restype = None
         L.seg_profile_enable.argtypes = [ctypes.c_int32]

@@ -182,9 +182,10 @@ __global__ void __launch_bounds__(256, 2) k_gemm_nt(const unsigned short *__rest
 // Per row: LSE over the vocab-tile partials (fixed order), then the loss.
 __global__ void __launch_bounds__(256) k_row_loss(
     const float2 *__restrict__ stats, int ntiles, int rows, const float *__restrict__ ztgt,
-    const float *__restrict__ old_logp, const float *__restrict__ adv,
-    const int32_t *__restrict__ row_traj, int num_traj, seg_loss_cfg cfg, float *__restrict__ logp,
-    float *__restrict__ loss_tok, uint8_t *__restrict__ clipped, float *__restrict__ lse_out,
+    const float *__restrict__ old_logp, const float *__restrict__ ref_logp,
+    const float *__restrict__ adv, const int32_t *__restrict__ row_traj, int num_traj,
+    seg_loss_cfg cfg, float *__restrict__ logp, float *__restrict__ loss_tok,
+    uint8_t *__restrict__ clipped, float *__restrict__ kl_tok, float *__restrict__ lse_out,
     float *__restrict__ g_out) {
   __shared__ float2 red[256];
   const int r = blockIdx.x, t = threadIdx.x;
@@ -230,11 +231,21 @@ __global__ void __launch_bounds__(256) k_row_loss(
       obj = fmaxf(obj, cfg.dual_clip_c * A);
       cl = cl || rho > cfg.dual_clip_c;
     }
+    // KL(pi_theta || pi_ref) per token: e^x - x - 1 with x = ref - logp,
+    // written expm1(x) - x (no cancellation for small x); its logp
+    // derivative is 1 - e^x = -expm1(x)
+    float kl = 0.f, dkl = 0.f;
+    if (ref_logp) {
+      const float x = ref_logp[r] - lp, em1 = expm1f(x);
+      kl = em1 - x;
+      dkl = -em1;
+    }
     logp[r] = lp;
-    loss_tok[r] = -obj;
+    loss_tok[r] = -obj + cfg.kl_coef * kl;
     clipped[r] = cl ? 1 : 0;
+    if (kl_tok) kl_tok[r] = kl;
     lse_out[r] = lse;
-    g_out[r] = cl ? 0.f : -cfg.loss_scale * rho * A;
+    g_out[r] = (cl ? 0.f : -cfg.loss_scale * rho * A) + cfg.loss_scale * cfg.kl_coef * dkl;
   }
 }
 
@@ -365,10 +376,10 @@ dim3 grid2(long cols, long rows, int t = 64) {
 
 template <class TI, class TO>
 void logprob_impl(int rows, int H, int V, const TI *h, const int32_t *row_index, const TI *w,
-                  const int32_t *target, const float *old_logp, const float *adv,
-                  const int32_t *row_traj, int num_traj, const seg_loss_cfg &cfg, float *logp,
-                  float *loss_tok,
-                  uint8_t *clipped, float *loss_sum, void *dh, float *dw, char *base,
+                  const int32_t *target, const float *old_logp, const float *ref_logp,
+                  const float *adv, const int32_t *row_traj, int num_traj,
+                  const seg_loss_cfg &cfg, float *logp, float *loss_tok, uint8_t *clipped,
+                  float *kl_tok, float *loss_sum, void *dh, float *dw, char *base,
                   const LpWs &L, hipStream_t st) {
   const int Rp = L.Rp, Vp = L.Vp;
   unsigned short *hb = reinterpret_cast<unsigned short *>(base + L.hb);
@@ -415,8 +426,8 @@ void logprob_impl(int rows, int H, int V, const TI *h, const int32_t *row_index,
   // 2. per-row loss
   {
   ProfScope prof("row_loss", st);
-  k_row_loss<<<rows, 256, 0, st>>>(stats, L.ntiles, rows, ztgt, old_logp, adv, row_traj, num_traj,
-                                   cfg, logp, loss_tok, clipped, lse, g);
+  k_row_loss<<<rows, 256, 0, st>>>(stats, L.ntiles, rows, ztgt, old_logp, ref_logp, adv, row_traj,
+                                   num_traj, cfg, logp, loss_tok, clipped, kl_tok, lse, g);
   SEG_LAUNCH_CHECK();
   k_loss_sum<<<1, 256, 0, st>>>(loss_tok, rows, cfg.loss_scale, loss_sum);
   SEG_LAUNCH_CHECK();
@@ -468,9 +479,10 @@ extern "C" size_t seg_logprob_workspace_bytes(int32_t rows, int32_t hidden, int3
 extern "C" seg_status seg_logprob_loss(int32_t rows, int32_t hidden, int32_t vocab, seg_dtype dt,
                                        const void *h, const int32_t *row_index, const void *w,
                                        const int32_t *target, const float *old_logp,
-                                       const float *adv, const int32_t *row_traj,
-                                       int32_t num_traj, const seg_loss_cfg *cfg, float *logp,
-                                       float *loss_tok, uint8_t *clipped, float *loss_sum,
+                                       const float *ref_logp, const float *adv,
+                                       const int32_t *row_traj, int32_t num_traj,
+                                       const seg_loss_cfg *cfg, float *logp, float *loss_tok,
+                                       uint8_t *clipped, float *kl_tok, float *loss_sum,
                                        void *dh, float *dw, void *ws, size_t ws_bytes,
                                        hipStream_t stream) {
   return guarded([&] {
@@ -481,9 +493,12 @@ extern "C" seg_status seg_logprob_loss(int32_t rows, int32_t hidden, int32_t voc
     SEG_CHECK(hidden % 8 == 0, SEG_ERR_UNSUPPORTED, "hidden %d must be a multiple of 8", hidden);
     SEG_CHECK(std::isfinite(cfg->eps_low) && std::isfinite(cfg->eps_high) &&
                   std::isfinite(cfg->loss_scale) && std::isfinite(cfg->logit_scale) &&
-                  std::isfinite(cfg->dual_clip_c),
+                  std::isfinite(cfg->dual_clip_c) && std::isfinite(cfg->kl_coef),
               SEG_ERR_ARG, "non-finite loss setting");
     SEG_CHECK(cfg->eps_low >= 0.f && cfg->eps_high >= 0.f, SEG_ERR_ARG, "negative clip range");
+    SEG_CHECK(cfg->kl_coef >= 0.f, SEG_ERR_ARG, "negative kl_coef");
+    SEG_CHECK(cfg->kl_coef == 0.f || ref_logp != nullptr, SEG_ERR_ARG,
+              "kl_coef > 0 needs ref_logp");
     const LpWs L = lp_ws(rows, hidden, vocab, dt);
     SEG_CHECK(ws_bytes >= L.total, SEG_ERR_WORKSPACE, "workspace of %zu bytes < required %zu",
               ws_bytes, L.total);
@@ -500,12 +515,13 @@ extern "C" seg_status seg_logprob_loss(int32_t rows, int32_t hidden, int32_t voc
     char *base = static_cast<char *>(ws);
     if (dt == SEG_F32)
       logprob_impl<float, float>(rows, hidden, vocab, static_cast<const float *>(h), row_index,
-                                 static_cast<const float *>(w), target, old_logp, adv, row_traj,
-                                 num_traj, *cfg, logp, loss_tok, clipped, loss_sum, dh, dw, base, L, stream);
+                                 static_cast<const float *>(w), target, old_logp, ref_logp, adv,
+                                 row_traj, num_traj, *cfg, logp, loss_tok, clipped, kl_tok,
+                                 loss_sum, dh, dw, base, L, stream);
     else
       logprob_impl<unsigned short, unsigned short>(
           rows, hidden, vocab, static_cast<const unsigned short *>(h), row_index,
-          static_cast<const unsigned short *>(w), target, old_logp, adv, row_traj, num_traj, *cfg, logp,
-          loss_tok, clipped, loss_sum, dh, dw, base, L, stream);
+          static_cast<const unsigned short *>(w), target, old_logp, ref_logp, adv, row_traj,
+          num_traj, *cfg, logp, loss_tok, clipped, kl_tok, loss_sum, dh, dw, base, L, stream);
   });
 }

@@ -207,10 +207,11 @@ class LossCfg:
     loss_scale: float = 1.0
     logit_scale: float = 1.0
     want_grad: bool = True
+    kl_coef: float = 0.0
 
     def c(self) -> SegLossCfg:
         return SegLossCfg(self.eps_low, self.eps_high, self.dual_clip_c, self.loss_scale,
-                          self.logit_scale, int(self.want_grad))
+                          self.logit_scale, int(self.want_grad), self.kl_coef)
 
 
 def logprob_workspace(rows, hidden, vocab, dt, device):
@@ -220,12 +221,14 @@ def logprob_workspace(rows, hidden, vocab, dt, device):
 
 
 def seg_logprob_loss(h, row_index, w, target, old_logp, adv, row_traj, cfg: LossCfg, out=None,
-                     ws=None):
-    """Fused log-prob + clipped-ratio loss (+ gradients when cfg.want_grad).
+                     ws=None, ref_logp=None):
+    """Fused log-prob + clipped-ratio loss with KL penalty (+ gradients when
+    cfg.want_grad).
 
     h [n_h, H]; row_index [R] int32 device or None; w [V, H]; target [R] int32;
-    old_logp [R] fp32; adv [num_traj] fp32; row_traj [R] int32.
-    Returns dict(logp, loss_tok, clipped, loss_sum, dh, dw).
+    old_logp [R] fp32; adv [num_traj] fp32; row_traj [R] int32; ref_logp [R]
+    fp32 or None (needed when cfg.kl_coef > 0).
+    Returns dict(logp, loss_tok, clipped, kl_tok, loss_sum, dh, dw).
     """
     import torch
     dev = h.device
@@ -238,6 +241,7 @@ def seg_logprob_loss(h, row_index, w, target, old_logp, adv, row_traj, cfg: Loss
             "logp": torch.empty(max(R, 1), dtype=torch.float32, device=dev),
             "loss_tok": torch.empty(max(R, 1), dtype=torch.float32, device=dev),
             "clipped": torch.empty(max(R, 1), dtype=torch.uint8, device=dev),
+            "kl_tok": torch.empty(max(R, 1), dtype=torch.float32, device=dev),
             "loss_sum": torch.empty(1, dtype=torch.float32, device=dev),
             "dh": torch.empty((max(R, 1), H), dtype=h.dtype, device=dev) if cfg.want_grad else None,
             "dw": torch.empty((V, H), dtype=torch.float32, device=dev) if cfg.want_grad else None,
@@ -246,8 +250,9 @@ def seg_logprob_loss(h, row_index, w, target, old_logp, adv, row_traj, cfg: Loss
         ws = logprob_workspace(R, H, V, dt, dev)
     check(_lib.lib().seg_logprob_loss(
         R, H, V, dt, h.data_ptr(), _ptr(row_index), w.data_ptr(), target.data_ptr(),
-        old_logp.data_ptr(), adv.data_ptr(), row_traj.data_ptr(), int(adv.numel()),
-        ctypes.byref(cfg.c()), out["logp"].data_ptr(), out["loss_tok"].data_ptr(),
-        out["clipped"].data_ptr(), out["loss_sum"].data_ptr(), _ptr(out["dh"]), _ptr(out["dw"]),
-        ws.data_ptr(), ws.numel(), _stream(dev)))
+        old_logp.data_ptr(), _ptr(ref_logp), adv.data_ptr(), row_traj.data_ptr(),
+        int(adv.numel()), ctypes.byref(cfg.c()), out["logp"].data_ptr(),
+        out["loss_tok"].data_ptr(), out["clipped"].data_ptr(), _ptr(out.get("kl_tok")),
+        out["loss_sum"].data_ptr(), _ptr(out["dh"]), _ptr(out["dw"]), ws.data_ptr(), ws.numel(),
+        _stream(dev)))
     return out

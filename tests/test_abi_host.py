@@ -150,12 +150,19 @@ def test_build_and_compute_reject_bad_args_before_any_launch():
     assert st == _lib.SEG_ERR_WORKSPACE
     # log-prob: hidden not a multiple of 8, workspace, null tensors
     cfg = S.LossCfg().c()
-    args = [None] * 7
-    st = L.seg_logprob_loss(4, 12, 10, 0, *args, 1, ctypes.byref(cfg), *([None] * 6), None, 0, None)
+    args = [None] * 8   # h, row_index, w, target, old_logp, ref_logp, adv, row_traj
+    outs = [None] * 7   # logp, loss_tok, clipped, kl_tok, loss_sum, dh, dw
+    st = L.seg_logprob_loss(4, 12, 10, 0, *args, 1, ctypes.byref(cfg), *outs, None, 0, None)
     assert st == _lib.SEG_ERR_UNSUPPORTED
-    st = L.seg_logprob_loss(4, 16, 10, 0, *args, 1, ctypes.byref(cfg), *([None] * 6), None, 0, None)
+    st = L.seg_logprob_loss(4, 16, 10, 0, *args, 1, ctypes.byref(cfg), *outs, None, 0, None)
     assert st == _lib.SEG_ERR_WORKSPACE
     need = L.seg_logprob_workspace_bytes(4, 16, 10, 0)
-    st = L.seg_logprob_loss(4, 16, 10, 0, *args, 1, ctypes.byref(cfg), *([None] * 6), None, need,
-                            None)
+    st = L.seg_logprob_loss(4, 16, 10, 0, *args, 1, ctypes.byref(cfg), *outs, None, need, None)
     assert st == _lib.SEG_ERR_ARG
+    # a KL penalty needs the reference log-probs; a negative one is rejected
+    for kl in (0.1, -1.0):
+        kcfg = S.LossCfg(kl_coef=kl).c()
+        st = L.seg_logprob_loss(4, 16, 10, 0, *args, 1, ctypes.byref(kcfg), *outs, None, need,
+                                None)
+        assert st == _lib.SEG_ERR_ARG
+        assert b"kl" in L.seg_last_error()

@@ -1,7 +1,8 @@
-"""GPU fused log-prob + clipped-ratio loss (seg_logprob_loss through the C ABI)
-against the float64 oracle (Eq. loss): full parity on the tiny and small
-heads, the 7B-class head at full vocabulary and hidden size on a reduced row
-count, and the full 7B-class row count on sampled rows plus the identity
+"""GPU fused log-prob + clipped-ratio loss with its KL penalty
+(seg_logprob_loss through the C ABI) against the float64 oracle (Eq. loss):
+full parity on the tiny and small heads (also with the KL penalty on), the
+7B-class head at full vocabulary and hidden size on a reduced row count, and
+the full 7B-class row count on sampled rows plus the identity
 sum_v dW[v] = 0 (each dz row sums to zero)."""
 import numpy as np
 import pytest
@@ -28,7 +29,7 @@ def _inputs(run, rows_idx=None):
     return sel, h, tgt, adv[hst["loss_traj"][sel]].astype(np.float64)
 
 
-def _run_gpu(run, old_logp, cfg_loss, w=None):
+def _run_gpu(run, old_logp, cfg_loss, w=None, ref_logp=None):
     import torch
     dev = run.dev
     hst = run.host
@@ -37,24 +38,31 @@ def _run_gpu(run, old_logp, cfg_loss, w=None):
     w = run.inp.w_torch(dev) if w is None else w
     tgt = torch.from_numpy(run.inp.tgt_np(hst["loss_tgt_src"])).to(dev)
     adv = torch.from_numpy(run.inp.adv_np().astype(np.float32)).to(dev)
+    ref_t = None if ref_logp is None else torch.from_numpy(ref_logp.astype(np.float32)).to(dev)
     out = S.seg_logprob_loss(h, run.lay.loss_pred_row, w, tgt,
                              torch.from_numpy(old_logp.astype(np.float32)).to(dev), adv,
-                             run.lay.loss_traj, cfg_loss)
+                             run.lay.loss_traj, cfg_loss, ref_logp=ref_t)
     torch.cuda.synchronize()
     return out
 
 
-def _full_case(cfg, dual=0.0, want_grad=True):
+def _full_case(cfg, dual=0.0, want_grad=True, kl=None):
+    """kl: None (no reference log-probs) or the KL coefficient; the reference
+    log-probs are the current ones plus a reversed copy of the rollout noise."""
     run = GpuRun(cfg)
     R = run.lay.sizes.loss_rows
     sel, h, tgt, adv = _inputs(run)
     w = as_model_dtype(run.inp.w_np(), cfg)
     logp_cur, _, _ = OLS.logprob(h, w, tgt)
-    old = (logp_cur + run.inp.old_noise_np(run.host["loss_tgt_src"])).astype(np.float32)
-    lc = S.LossCfg(cfg.eps_low, cfg.eps_high, dual, 1.0 / R, 1.0, want_grad)
+    noise = run.inp.old_noise_np(run.host["loss_tgt_src"])
+    old = (logp_cur + noise).astype(np.float32)
+    refl = None if kl is None else (logp_cur + 2.0 * noise[::-1]).astype(np.float32)
+    lc = S.LossCfg(cfg.eps_low, cfg.eps_high, dual, 1.0 / R, 1.0, want_grad, kl or 0.0)
     ref = OLS.loss_and_grads(h, w, tgt, old.astype(np.float64), adv, cfg.eps_low, cfg.eps_high,
-                             loss_scale=1.0 / R, dual_clip_c=dual, want_grad=want_grad)
-    out = _run_gpu(run, old, lc)
+                             loss_scale=1.0 / R, dual_clip_c=dual, want_grad=want_grad,
+                             ref_logp=None if refl is None else refl.astype(np.float64),
+                             kl_coef=kl or 0.0)
+    out = _run_gpu(run, old, lc, ref_logp=refl)
     return run, ref, out, old
 
 
@@ -82,6 +90,35 @@ def test_full_parity(cfg, dual):
     e_dw = rel(out["dw"].cpu().numpy(), ref["dw"])
     say(f"  dh {e_dh:.2e} dw {e_dw:.2e}")
     assert e_dh < TOL and e_dw < TOL
+
+
+@pytest.mark.parametrize("cfg,kl", [(WL.TINY, 0.5), (WL.SMALL, 0.5), (WL.SMALL, 1e-4)],
+                         ids=["tiny_kl0.5", "small_kl0.5", "small_kl1e-4"])
+def test_kl_penalty_parity(cfg, kl):
+    """Loss, per-token KL and gradients with the KL penalty on."""
+    say(f"logprob {cfg.name} kl={kl}")
+    run, ref, out, old = _full_case(cfg, kl=kl)
+    R = run.lay.sizes.loss_rows
+    e_kl = rel(out["kl_tok"][:R].cpu().numpy(), ref["kl_tok"])
+    e_loss = rel(out["loss_tok"][:R].cpu().numpy(), ref["loss_tok"])
+    e_dh = rel(out["dh"][:R].float().cpu().numpy(), ref["dh"])
+    e_dw = rel(out["dw"].cpu().numpy(), ref["dw"])
+    say(f"  kl {e_kl:.2e} loss {e_loss:.2e} dh {e_dh:.2e} dw {e_dw:.2e}")
+    assert (out["kl_tok"][:R].cpu().numpy() >= 0).all()
+    assert e_kl < TOL and e_loss < TOL and e_dh < TOL and e_dw < TOL
+    assert abs(float(out["loss_sum"][0]) - ref["loss_sum"]) < TOL * max(1e-3, abs(ref["loss_sum"]))
+
+
+def test_kl_zero_coefficient_matches_plain_loss():
+    """kl_coef = 0 with reference log-probs given: the same loss and
+    gradients, bitwise, as without them."""
+    import torch
+    run, _, out_kl, old = _full_case(WL.TINY, kl=0.0)
+    R = run.lay.sizes.loss_rows
+    lc = S.LossCfg(WL.TINY.eps_low, WL.TINY.eps_high, 0.0, 1.0 / R, 1.0, True)
+    out = _run_gpu(run, old, lc)
+    for k in ("logp", "loss_tok", "loss_sum", "dh", "dw"):
+        assert torch.equal(out[k], out_kl[k]), k
 
 
 def test_forward_only():
