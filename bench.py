@@ -340,6 +340,37 @@ def pmc_driver(cfg_name):
                                       "launches": 3}}), flush=True)
 
 
+SWEEP_K = (1, 3, 5, 8, 10, 15)
+
+
+def sweep(cfg, steps, warmup):
+    """Kernel-level half of the paper's window sweep: W = L = K over the same
+    batch; per K the segmented step, the reference forward pass and the
+    training-item and visible-pair counts.  One JSON line."""
+    import torch
+    dev = torch.device("cuda:0")
+    rows = []
+    for K in SWEEP_K:
+        c = cfg.with_(name=f"{cfg.name}_K{K}", window=K, seg_steps=K)
+        run = PathRun(c, dev)
+        ph, kern, _ = time_path(run, steps, warmup, profile=False)
+        ref = time_ref(run, steps, warmup)
+        attn = ph["attn_fwd"] + ph["attn_bwd"]
+        rows.append({"K": K, "segments": run.sizes.num_segments,
+                     "packed_tokens": run.sizes.packed_tokens,
+                     "visible_pairs_per_head": run.pairs,
+                     "step_ms": round(ph["step"], 3), "attn_ms": round(attn, 3),
+                     "attn_tflops": round(run.attn_flop() / (attn * 1e-3) / 1e12, 2),
+                     "traj_tokens_per_s": round(run.sizes.traj_tokens / (ph["step"] * 1e-3), 1),
+                     "reference_forward_ms": ref["total"]})
+        log(f"  K={K}: {rows[-1]}")
+        run.free()
+        del run
+        torch.cuda.empty_cache()
+    print(json.dumps({"sweep": "W = L = K", "workload": cfg.name, "steps": steps,
+                      "warmup": warmup, "rows": rows}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -348,6 +379,9 @@ def main():
     ap.add_argument("--config", default="7b", help="workload name (7b, small, long, tiny)")
     ap.add_argument("--no-stepwise", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sweep", action="store_true",
+                    help="W = L = K sweep over K in (1, 3, 5, 8, 10, 15) on the workload "
+                         "(one JSON line; not the bench line)")
     ap.add_argument("--pmc-driver", action="store_true",
                     help="one launch of each attention kernel plus a calibration copy, for "
                          "rocprofv3 --pmc counter passes (no timing, no JSON bench line)")
@@ -365,6 +399,9 @@ def main():
         sys.exit(1)
     if args.pmc_driver:
         pmc_driver(args.config)
+        return
+    if args.sweep:
+        sweep(WL.CONFIGS[args.config], args.steps, args.warmup)
         return
     dev = torch.device("cuda:0")
     cfg = WL.CONFIGS[args.config]

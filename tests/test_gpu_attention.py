@@ -24,6 +24,9 @@ CASES = {
     "med_f32": MED.with_(dtype="f32", seed=3),
     "med_buffers": MED.with_(buffer_tokens=1400, seed=4, steps=(3, 5)),
     "stepwise_small": MED.with_(seg_steps=1, seed=5, steps=(3, 4)),
+    # the long-window end of the W = L sweep
+    "med_w8_l8": MED.with_(window=8, seg_steps=8, seed=11, steps=(9, 12)),
+    "med_w15_l15": MED.with_(window=15, seg_steps=15, seed=12, steps=(16, 17), img_len=60),
     "tiny": WL.TINY,
 }
 
