@@ -29,6 +29,17 @@ Readings taken where the paper leaves the point open:
 * Packing: segments in (trajectory, first turn) order; with a buffer size B,
   a segment that does not fit in the current buffer opens the next one and
   the tail of the closed buffer is padding.
+
+Anchored mode (the algorithm as printed, App. D): K = W screenshots kept and
+removal threshold Delta = L.  The screenshot count of the current token
+stream is tracked turn by turn; when turn j's screenshot makes it exceed
+K + Delta, the stream is saved as a segment (ending with turn j-1's text),
+the oldest Delta screenshots leave the history and the re-tokenised history
+(all earlier text, the remaining screenshots, turn j's included) starts the
+next segment.  The loop is taken with the observation before the response
+of a turn, the canonical order used here (a response follows the screenshot
+it conditions on).  Inside a segment every token sees every earlier token:
+the window is anchored at the segment start, not slid per query.
 """
 from __future__ import annotations
 
@@ -91,6 +102,54 @@ def segment_turns(p, img, text, W, L, cap=0):
     return segs
 
 
+def anchored_turns(T, K, delta):
+    """The algorithm's segments of a T-turn trajectory: list of (a, b, images)
+    with images the turns whose screenshot is in the segment's stream."""
+    segs = []
+    history = []        # turns whose screenshot is in the text history
+    stream = []         # turns whose screenshot is in the current stream
+    n_img = 0
+    a = 1
+    for t in range(1, T + 1):
+        n_img += 1      # observation with screenshot of turn t
+        history.append(t)
+        if n_img > K + delta:
+            segs.append((a, t, tuple(stream)))      # saved before turn t's tokens
+            history = history[delta:]               # oldest Delta screenshots removed
+            n_img -= delta
+            stream = list(history)                  # re-tokenised history
+            a = t
+        else:
+            stream.append(t)                        # token-diff append
+        # the response of turn t follows (trainable tokens)
+    segs.append((a, T + 1, tuple(stream)))
+    return segs
+
+
+def segment_tokens_with(p, img, text, images, b, canon0):
+    """(canonical index, kind, step) of a segment whose turns are < b and
+    whose screenshots are exactly those of the turns in ``images``."""
+    keep = set(images)
+    canon, kind, step = [], [], []
+    canon.extend(range(canon0, canon0 + p))
+    kind.extend([KIND_PROMPT] * p)
+    step.extend([0] * p)
+    c = canon0 + p
+    for j in range(1, b):
+        m, x = int(img[j - 1]), int(text[j - 1])
+        if j in keep:
+            canon.extend(range(c, c + m))
+            kind.extend([KIND_IMAGE] * m)
+            step.extend([j] * m)
+        c += m
+        canon.extend(range(c, c + x))
+        kind.extend([KIND_TEXT] * x)
+        step.extend([j] * x)
+        c += x
+    return (np.asarray(canon, np.int64), np.asarray(kind, np.int64),
+            np.asarray(step, np.int64))
+
+
 def segment_tokens(p, img, text, W, a, b, canon0):
     """(canonical index, kind, step) of every token of segment [a, b)."""
     canon, kind, step = [], [], []
@@ -113,22 +172,27 @@ def segment_tokens(p, img, text, W, a, b, canon0):
             np.asarray(step, np.int64))
 
 
-def visibility(seg: Segment, W: int) -> np.ndarray:
+def visibility(seg: Segment, W) -> np.ndarray:
     """Dense mask[q, k]: key k visible to query q (same segment, k not after
-    q, and k not a screenshot more than W-1 turns older than q's turn)."""
+    q, and k not a screenshot more than W-1 turns older than q's turn).
+    W = None is the anchored mode: causal inside the segment."""
     n = seg.length
     qi = np.arange(n)[:, None]
     ki = np.arange(n)[None, :]
     causal = ki <= qi
+    if W is None:
+        return causal
     expired = (seg.kind[None, :] == KIND_IMAGE) & (seg.step[None, :] <= seg.step[:, None] - W)
     return causal & ~expired
 
 
-def visibility_rows(seg: Segment, W: int, rows) -> np.ndarray:
+def visibility_rows(seg: Segment, W, rows) -> np.ndarray:
     """Rows ``rows`` of the dense mask of :func:`visibility`."""
     rows = np.asarray(rows)
     ki = np.arange(seg.length)[None, :]
     causal = ki <= rows[:, None]
+    if W is None:
+        return causal
     expired = (seg.kind[None, :] == KIND_IMAGE) & (seg.step[None, :] <= seg.step[rows][:, None] - W)
     return causal & ~expired
 
@@ -175,8 +239,17 @@ class Layout:
     window: int
 
 
-def build(spans, W, L, tile, cap=0, buffer_tokens=0, with_tiles=True) -> Layout:
-    """All layout arrays of a batch (steps O1-O6 of the segmented path)."""
+def build(spans, W, L, tile, cap=0, buffer_tokens=0, with_tiles=True,
+          mode="sliding") -> Layout:
+    """All layout arrays of a batch (steps O1-O6 of the segmented path).
+
+    mode "anchored": segments and screenshots from :func:`anchored_turns`
+    with K = W and Delta = L, causal visibility (no token cap)."""
+    if mode not in ("sliding", "anchored"):
+        raise ValueError(mode)
+    if mode == "anchored" and cap:
+        raise ValueError("the anchored mode has no token cap")
+    Wv = None if mode == "anchored" else W
     canon_off = [0]
     for t in range(spans.num_traj):
         p, img, text, _ = _traj_spans(spans, t)
@@ -186,8 +259,15 @@ def build(spans, W, L, tile, cap=0, buffer_tokens=0, with_tiles=True) -> Layout:
     segs: List[Segment] = []
     for t in range(spans.num_traj):
         p, img, text, _ = _traj_spans(spans, t)
-        for a, b in segment_turns(p, img, text, W, L, cap):
-            c, k, s = segment_tokens(p, img, text, W, a, b, canon_off[t])
+        if mode == "anchored":
+            cuts = anchored_turns(len(img), W, L)
+        else:
+            cuts = [(a, b, None) for a, b in segment_turns(p, img, text, W, L, cap)]
+        for a, b, images in cuts:
+            if images is None:
+                c, k, s = segment_tokens(p, img, text, W, a, b, canon_off[t])
+            else:
+                c, k, s = segment_tokens_with(p, img, text, images, b, canon_off[t])
             if buffer_tokens and len(c) > buffer_tokens:
                 raise CapacityError(f"segment of {len(c)} tokens exceeds the buffer")
             segs.append(Segment(t, a, b, -1, c, k, s))
@@ -243,7 +323,7 @@ def build(spans, W, L, tile, cap=0, buffer_tokens=0, with_tiles=True) -> Layout:
         seg_info[si] = [sg.traj, sg.a, sg.b, sg.start, n, qbase, loss_base, seg_nloss[si]]
         loss_base += seg_nloss[si]
         if with_tiles:
-            cls, npairs = segment_tiles(sg, W, tile)
+            cls, npairs = segment_tiles(sg, Wv, tile)
             pairs.append(npairs)
             for i in range(nt):
                 qt_rows.append([(qbase + j, int(cls[i, j])) for j in range(nt) if cls[i, j]])
@@ -266,4 +346,4 @@ def build(spans, W, L, tile, cap=0, buffer_tokens=0, with_tiles=True) -> Layout:
                   np.asarray(pred, np.int64), np.asarray(tgt, np.int64),
                   np.asarray(trj, np.int64), np.asarray(tile_seg, np.int64),
                   qt_ptr, qt_col, qt_cls, kt_ptr, kt_row, kt_cls,
-                  np.asarray(pairs, np.int64), tile, W)
+                  np.asarray(pairs, np.int64), tile, Wv)

@@ -235,3 +235,77 @@ def test_empty_and_zero_turn_trajectories():
     sp0 = WL.explicit_spans([], [], [], [], [])
     lay0 = OL.build(sp0, 1, 1, 4)
     assert lay0.packed_tokens == 0 and len(lay0.segments) == 0
+
+
+# ---- anchored mode (the algorithm as printed)
+
+def test_anchored_hand_worked_example():
+    with open(os.path.join(GOLD, "alg2_anchored_example.json")) as f:
+        d = json.load(f)
+    s = d["spans"]
+    sp = WL.explicit_spans(s["steps"], s["prompt"], s["img"], s["text"], s["action"])
+    lay = OL.build(sp, d["K"], d["delta"], 4, mode="anchored")
+    got = [[sg.traj, sg.a, sg.b, sg.start, sg.length] for sg in lay.segments]
+    assert got == d["segments"]
+    imgs = [sorted(set(sg.step[sg.kind == OL.KIND_IMAGE].tolist())) for sg in lay.segments]
+    assert imgs == d["images"]
+    assert lay.tok_src.tolist() == d["tok_src"]
+    assert list(zip(lay.loss_pred_row.tolist(), lay.loss_tgt_src.tolist())) == \
+        [tuple(r) for r in d["loss_rows"]]
+    assert lay.seg_pairs.tolist() == d["pairs"]
+    assert OL.anchored_turns(7, 2, 2) == [(1, 5, (1, 2, 3, 4)), (5, 7, (3, 4, 5, 6)),
+                                         (7, 8, (5, 6, 7))]
+
+
+@pytest.mark.parametrize("T,K,D", [(1, 1, 1), (5, 1, 1), (30, 3, 5), (30, 5, 5), (50, 8, 5),
+                                   (12, 3, 40), (9, 2, 1)])
+def test_anchored_counts_and_invariants(T, K, D):
+    """First segment K + Delta turns, then Delta turns each; every stream
+    holds at most K + Delta screenshots and a new stream starts with K + 1;
+    Delta >= T gives the whole trajectory as one item."""
+    segs = OL.anchored_turns(T, K, D)
+    lens = [b - a for a, b, _ in segs]
+    if T <= K + D:
+        assert segs == [(1, T + 1, tuple(range(1, T + 1)))]
+    else:
+        assert lens[0] == K + D and all(n == D for n in lens[1:-1]) and 1 <= lens[-1] <= D
+        assert len(segs) == 1 + -(-(T - K - D) // D)
+    assert segs[0][0] == 1 and segs[-1][1] == T + 1
+    assert all(segs[i][1] == segs[i + 1][0] for i in range(len(segs) - 1))
+    for i, (a, b, imgs) in enumerate(segs):
+        assert len(imgs) <= K + D
+        assert list(imgs) == list(range(max(1, a - K) if i else 1, b))
+        if i:
+            assert sum(1 for j in imgs if j <= a) == K + 1
+
+
+def test_anchored_tokens_equal_window_k_plus_one():
+    """The screenshots the algorithm keeps are those a window of K + 1
+    turns before each segment start would keep (two constructions)."""
+    rng = np.random.default_rng(5)
+    for _ in range(20):
+        T = int(rng.integers(1, 25))
+        K, D = int(rng.integers(1, 6)), int(rng.integers(1, 6))
+        p = int(rng.integers(1, 9))
+        img = rng.integers(0, 5, size=T)
+        text = rng.integers(0, 5, size=T)
+        for a, b, imgs in OL.anchored_turns(T, K, D):
+            c1 = OL.segment_tokens_with(p, img, text, imgs, b, 0)
+            c2 = OL.segment_tokens(p, img, text, K + 1, a, b, 0)
+            for x, y in zip(c1, c2):
+                assert np.array_equal(x, y)
+
+
+def test_anchored_visibility_is_causal_and_trains_every_action_once():
+    rng = np.random.default_rng(6)
+    T = 11
+    sp = WL.explicit_spans([T], [5], rng.integers(1, 4, size=T), rng.integers(2, 6, size=T),
+                           [1] * T)
+    lay = OL.build(sp, 3, 2, 4, mode="anchored")
+    for sg in lay.segments:
+        n = sg.length
+        assert np.array_equal(OL.visibility(sg, None), np.tril(np.ones((n, n), bool)))
+    assert len(lay.loss_tgt_src) == T
+    assert len(set(lay.loss_tgt_src.tolist())) == T
+    with pytest.raises(ValueError):
+        OL.build(sp, 3, 2, 4, cap=100, mode="anchored")
