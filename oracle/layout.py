@@ -104,7 +104,9 @@ def segment_turns(p, img, text, W, L, cap=0):
 
 def anchored_turns(T, K, delta):
     """The algorithm's segments of a T-turn trajectory: list of (a, b, images)
-    with images the turns whose screenshot is in the segment's stream."""
+    with images the turns whose screenshot is in the segment's stream.  A
+    trajectory without turns gives no segment (its final stream would hold
+    no trainable token)."""
     segs = []
     history = []        # turns whose screenshot is in the text history
     stream = []         # turns whose screenshot is in the current stream
@@ -122,7 +124,8 @@ def anchored_turns(T, K, delta):
         else:
             stream.append(t)                        # token-diff append
         # the response of turn t follows (trainable tokens)
-    segs.append((a, T + 1, tuple(stream)))
+    if a <= T:  # the final stream; an episode without turns has no trainable token
+        segs.append((a, T + 1, tuple(stream)))
     return segs
 
 

@@ -257,6 +257,10 @@ def test_anchored_hand_worked_example():
                                          (7, 8, (5, 6, 7))]
 
 
+def test_anchored_no_turns_no_segment():
+    assert OL.anchored_turns(0, 3, 5) == []
+
+
 @pytest.mark.parametrize("T,K,D", [(1, 1, 1), (5, 1, 1), (30, 3, 5), (30, 5, 5), (50, 8, 5),
                                    (12, 3, 40), (9, 2, 1)])
 def test_anchored_counts_and_invariants(T, K, D):
