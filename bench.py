@@ -84,7 +84,7 @@ class PathRun:
         self.S, self.cfg, self.dev = S, cfg, dev
         inp = WL.Inputs(cfg)
         self.problem = S.Problem.from_spans(inp.spans, cfg.window, cfg.seg_steps,
-                                            cfg.max_seg_tokens, cfg.buffer_tokens, 128)
+                                            cfg.max_seg_tokens, cfg.buffer_tokens, 128, cfg.mode)
         self.sizes = S.seg_layout_query(self.problem)
         self.lay = S.seg_build_layout(self.problem, self.sizes, dev)
         host = self.lay.host()

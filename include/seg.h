@@ -84,7 +84,20 @@ enum {
  * and k is not a screenshot token of a turn <= turn(q) - W.
  * tile: tile edge of the block-sparse map; 128 for the numeric kernels, any
  * value >= 1 for layout-only use.
+ *
+ * mode SEG_MODE_ANCHORED follows the App. D algorithm as printed, with
+ * K = window screenshots kept and removal threshold Delta = seg_steps: the
+ * screenshot count of the token stream is tracked turn by turn (observation
+ * before response); when turn j's screenshot makes it exceed K + Delta the
+ * stream is saved as a segment ending with turn j-1, the oldest Delta
+ * screenshots are dropped and the re-tokenised history starts the next
+ * segment at turn j.  So the first segment has K + Delta turns and later ones
+ * Delta turns; segment [a, b) holds the screenshots of turns j >= a - K; every
+ * token sees every earlier token of its segment (no window clause).
+ * max_seg_tokens must be 0 in this mode.
  */
+typedef enum { SEG_MODE_SLIDING = 0, SEG_MODE_ANCHORED = 1 } seg_mode;
+#define SEG_WINDOW_ANCHORED (1 << 28)
 typedef struct {
   int32_t num_traj;
   const int32_t *step_offsets; /* host [num_traj+1], step_offsets[0] = 0, non-decreasing */
@@ -97,6 +110,7 @@ typedef struct {
   int32_t max_seg_tokens;      /* 0 = no cap */
   int32_t buffer_tokens;       /* 0 = one contiguous packed buffer */
   int32_t tile;                /* >= 1 */
+  int32_t mode;                /* seg_mode; 0 = sliding window (default) */
 } seg_problem;
 
 typedef struct {
@@ -134,7 +148,9 @@ typedef struct {
   int64_t *seg_pairs;     /* [S] exact visible (query, key) pairs of each segment */
   int64_t *tile_nnz;      /* [1] non-skipped tiles */
   int32_t *work_order;    /* [G] tiles by decreasing CSR row length (ties: ascending index) */
-  int32_t window;         /* set by seg_build_layout */
+  int32_t window;         /* set by seg_build_layout: the visibility window the
+                             attention kernels apply (W; SEG_WINDOW_ANCHORED,
+                             larger than any turn index, in the anchored mode) */
   int32_t tile;           /* set by seg_build_layout */
 } seg_layout;
 

@@ -28,12 +28,16 @@ P32 = ctypes.POINTER(ctypes.c_int32)
 VP = ctypes.c_void_p
 
 
+SEG_MODE_SLIDING, SEG_MODE_ANCHORED = 0, 1
+SEG_WINDOW_ANCHORED = 1 << 28
+
+
 class SegProblem(ctypes.Structure):
     _fields_ = [("num_traj", ctypes.c_int32), ("step_offsets", P32), ("prompt_len", P32),
                 ("img_len", P32), ("text_len", P32), ("action_len", P32),
                 ("window", ctypes.c_int32), ("seg_steps", ctypes.c_int32),
                 ("max_seg_tokens", ctypes.c_int32), ("buffer_tokens", ctypes.c_int32),
-                ("tile", ctypes.c_int32)]
+                ("tile", ctypes.c_int32), ("mode", ctypes.c_int32)]
 
 
 class SegSizes(ctypes.Structure):

@@ -98,6 +98,12 @@ void validate(const seg_problem *p) {
   SEG_CHECK(p->max_seg_tokens >= 0, SEG_ERR_ARG, "max_seg_tokens < 0");
   SEG_CHECK(p->buffer_tokens >= 0, SEG_ERR_ARG, "buffer_tokens < 0");
   SEG_CHECK(p->tile >= 1, SEG_ERR_ARG, "tile must be >= 1 (got %d)", p->tile);
+  SEG_CHECK(p->mode == SEG_MODE_SLIDING || p->mode == SEG_MODE_ANCHORED, SEG_ERR_ARG,
+            "unknown mode %d", p->mode);
+  SEG_CHECK(p->mode == SEG_MODE_SLIDING || p->max_seg_tokens == 0, SEG_ERR_UNSUPPORTED,
+            "the anchored mode has no token cap (max_seg_tokens must be 0)");
+  SEG_CHECK(p->mode == SEG_MODE_SLIDING || p->window < (SEG_WINDOW_ANCHORED >> 1), SEG_ERR_ARG,
+            "window too large");
   if (p->num_traj == 0) return;
   SEG_CHECK(p->step_offsets && p->prompt_len, SEG_ERR_ARG, "step_offsets/prompt_len is NULL");
   SEG_CHECK(p->step_offsets[0] == 0, SEG_ERR_ARG, "step_offsets[0] must be 0");
@@ -122,7 +128,12 @@ Plan make_plan(const seg_problem *p) {
   validate(p);
   Plan pl;
   seg_sizes &sz = pl.sz;
-  const int W = p->window, L = p->seg_steps, tile = p->tile;
+  // Anchored mode: a segment keeps the K = window screenshots before its
+  // first turn (K + 1 with its own), the first segment runs K + Delta turns
+  // and later ones Delta = seg_steps (the count of the algorithm's trigger).
+  const bool anchored = p->mode == SEG_MODE_ANCHORED;
+  const int W = anchored ? p->window + 1 : p->window, L = p->seg_steps, tile = p->tile;
+  const int L0 = anchored ? p->window + p->seg_steps : L;  // turns of a trajectory's first segment
   const int64_t cap = p->max_seg_tokens, B = p->buffer_tokens;
   sz.num_steps = p->num_traj ? p->step_offsets[p->num_traj] : 0;
 
@@ -146,7 +157,8 @@ Plan make_plan(const seg_problem *p) {
                 "trajectory %d turn %d alone needs %lld tokens > max_seg_tokens %lld", t, a,
                 (long long)one, (long long)cap);
       int b = a + 1;
-      while (b - a < L && b <= T && (!cap || seg_len(img, text, pr, W, a, b + 1) <= cap)) ++b;
+      const int La = a == 1 ? L0 : L;
+      while (b - a < La && b <= T && (!cap || seg_len(img, text, pr, W, a, b + 1) <= cap)) ++b;
       int64_t n = seg_len(img, text, pr, W, a, b);
       SEG_CHECK(!B || n <= B, SEG_ERR_CAPACITY,
                 "segment of %lld tokens (trajectory %d, turns %d..%d) exceeds buffer_tokens %lld",
@@ -341,7 +353,9 @@ __global__ void __launch_bounds__(256) k_classify(
         }
         cnt += lo - qs + 1;
       }
-      if (!(k < q_lo && step_qhi < kexp)) all = false;
+      // every row of the tile sees key k: k <= q_lo (causal; a 1x1 diagonal
+      // tile is full) and the last row's turn is before the key's expiry
+      if (!(k <= q_lo && step_qhi < kexp)) all = false;
     }
     const bool t_any = __any(any);
     const bool t_all = __all(all) && (q_hi - q_lo + 1 == tile) && (k_hi - k_lo + 1 == tile);
@@ -517,7 +531,9 @@ extern "C" seg_status seg_build_layout(const seg_problem *p, const seg_sizes *sz
               "sizes do not match seg_layout_query of this problem");
     SEG_CHECK(ws_bytes >= sz->workspace_bytes, SEG_ERR_WORKSPACE,
               "workspace of %zu bytes < required %zu", ws_bytes, sz->workspace_bytes);
-    out->window = p->window;
+    // visibility window of the kernels: none inside an anchored segment
+    const int Wv = p->mode == SEG_MODE_ANCHORED ? SEG_WINDOW_ANCHORED : p->window;
+    out->window = Wv;
     out->tile = p->tile;
     const int S = sz->num_segments, G = sz->num_qtiles, R = sz->loss_rows;
     const int P = (int)sz->packed_tokens;
@@ -577,7 +593,7 @@ extern "C" seg_status seg_build_layout(const seg_problem *p, const seg_sizes *sz
     }
     k_tile_seg<<<grid_for(G), 256, 0, stream>>>(d_segs, S, G, out->tile_seg);
     SEG_LAUNCH_CHECK();
-    k_classify<<<G, 256, 0, stream>>>(d_segs, out->tile_seg, out->tok_meta, p->window, p->tile,
+    k_classify<<<G, 256, 0, stream>>>(d_segs, out->tile_seg, out->tok_meta, Wv, p->tile,
                                       d_cls, d_qcnt, d_kcnt, out->seg_pairs);
     SEG_LAUNCH_CHECK();
     k_scan<<<1, 1024, 0, stream>>>(d_qcnt, G, out->qt_ptr);

@@ -34,12 +34,16 @@ class Problem:
     max_seg_tokens: int = 0
     buffer_tokens: int = 0
     tile: int = 128
+    mode: int = 0   # _lib.SEG_MODE_SLIDING or _lib.SEG_MODE_ANCHORED
 
     @classmethod
-    def from_spans(cls, spans, window, seg_steps, max_seg_tokens=0, buffer_tokens=0, tile=128):
+    def from_spans(cls, spans, window, seg_steps, max_seg_tokens=0, buffer_tokens=0, tile=128,
+                   mode=0):
+        if isinstance(mode, str):
+            mode = {"sliding": _lib.SEG_MODE_SLIDING, "anchored": _lib.SEG_MODE_ANCHORED}[mode]
         return cls(_i32(spans.step_offsets), _i32(spans.prompt_len), _i32(spans.img_len),
                    _i32(spans.text_len), _i32(spans.action_len), int(window), int(seg_steps),
-                   int(max_seg_tokens), int(buffer_tokens), int(tile))
+                   int(max_seg_tokens), int(buffer_tokens), int(tile), int(mode))
 
     def c(self) -> SegProblem:
         def ptr(a):
@@ -47,7 +51,7 @@ class Problem:
         return SegProblem(len(self.prompt_len), ptr(self.step_offsets), ptr(self.prompt_len),
                           ptr(self.img_len), ptr(self.text_len), ptr(self.action_len),
                           self.window, self.seg_steps, self.max_seg_tokens, self.buffer_tokens,
-                          self.tile)
+                          self.tile, self.mode)
 
 
 def seg_layout_query(problem: Problem) -> SegSizes:

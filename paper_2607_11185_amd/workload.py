@@ -63,6 +63,7 @@ class Config:
     w_std: float = 0.02
     old_noise_std: float = 0.1
     seed: int = 0
+    mode: str = "sliding"   # "sliding" window, or "anchored" (the App. D algorithm as printed)
 
     def with_(self, **kw) -> "Config":
         return dataclasses.replace(self, **kw)

@@ -41,7 +41,7 @@ class GpuRun:
         self.spans = self.inp.spans
         self.dev = torch.device(device)
         self.problem = S.Problem.from_spans(self.spans, cfg.window, cfg.seg_steps,
-                                            cfg.max_seg_tokens, cfg.buffer_tokens, tile)
+                                            cfg.max_seg_tokens, cfg.buffer_tokens, tile, cfg.mode)
         self.lay = S.seg_build_layout(self.problem, device=self.dev)
         self.host = self.lay.host()
         self.P = self.lay.sizes.packed_tokens
@@ -74,3 +74,9 @@ class GpuRun:
         v = as_model_dtype(self.inp.v_np(sg.canon), c)
         dout = as_model_dtype(self.inp.dout_np(np.arange(sg.start, sg.start + sg.length)), c)
         return q, k, v, dout
+
+
+def vis_window(cfg):
+    """Window argument of the oracle's visibility for a workload (None: the
+    anchored mode's causal visibility)."""
+    return None if cfg.mode == "anchored" else cfg.window

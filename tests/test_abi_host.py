@@ -32,8 +32,8 @@ def test_exports_every_declared_symbol():
         assert hasattr(L, name), name
 
 
-def _sizes_oracle(sp, W, L, tile, cap=0, buf=0):
-    lay = OL.build(sp, W, L, tile, cap=cap, buffer_tokens=buf, with_tiles=False)
+def _sizes_oracle(sp, W, L, tile, cap=0, buf=0, mode="sliding"):
+    lay = OL.build(sp, W, L, tile, cap=cap, buffer_tokens=buf, with_tiles=False, mode=mode)
     G = sum(-(-sg.length // tile) for sg in lay.segments)
     Z = sum((n := -(-sg.length // tile)) * (n + 1) // 2 for sg in lay.segments)
     return dict(num_segments=len(lay.segments), num_buffers=lay.num_buffers,
@@ -86,6 +86,8 @@ def _prob(**kw):
     (dict(tile=0), _lib.SEG_ERR_ARG, "tile"),
     (dict(max_seg_tokens=10), _lib.SEG_ERR_CAPACITY, "max_seg_tokens"),
     (dict(buffer_tokens=12), _lib.SEG_ERR_CAPACITY, "buffer_tokens"),
+    (dict(mode=7), _lib.SEG_ERR_ARG, "mode"),
+    (dict(mode=1, max_seg_tokens=100), _lib.SEG_ERR_UNSUPPORTED, "anchored"),
 ])
 def test_query_errors(kw, status, text):
     _lib_or_skip()
@@ -166,3 +168,29 @@ def test_build_and_compute_reject_bad_args_before_any_launch():
                                 None)
         assert st == _lib.SEG_ERR_ARG
         assert b"kl" in L.seg_last_error()
+
+
+def test_query_anchored_matches_oracle():
+    """Sizes of the anchored mode (the App. D algorithm) against the oracle,
+    on the workloads and on random span lists."""
+    _lib_or_skip()
+    for cfg in (WL.SMALL, WL.SEVEN_B):
+        sp = WL.make_spans(cfg)
+        pr = S.Problem.from_spans(sp, cfg.window, cfg.seg_steps, 0, 0, 128, "anchored")
+        got = S.seg_layout_query(pr).as_dict()
+        want = _sizes_oracle(sp, cfg.window, cfg.seg_steps, 128, mode="anchored")
+        for k, v in want.items():
+            assert got[k] == v, (cfg.name, k, got[k], v)
+    rng = np.random.default_rng(1)
+    for it in range(30):
+        n = int(rng.integers(0, 4))
+        T = rng.integers(0, 12, size=n)
+        ns = int(T.sum())
+        text = rng.integers(0, 9, size=ns)
+        sp = WL.explicit_spans(T, rng.integers(1, 9, size=n), rng.integers(0, 9, size=ns), text,
+                               [int(rng.integers(0, t + 1)) for t in text])
+        K, D, tile = int(rng.integers(1, 5)), int(rng.integers(1, 5)), int(rng.choice([1, 4, 128]))
+        got = S.seg_layout_query(S.Problem.from_spans(sp, K, D, 0, 0, tile, "anchored")).as_dict()
+        want = _sizes_oracle(sp, K, D, tile, mode="anchored")
+        for k, v in want.items():
+            assert got[k] == v, (it, k, got[k], v)

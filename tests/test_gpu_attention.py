@@ -12,7 +12,7 @@ import pytest
 from oracle import attention as OA
 from oracle import layout as OL
 from paper_2607_11185_amd import workload as WL
-from tests.gpu_helpers import TOL, GpuRun, rel, say
+from tests.gpu_helpers import TOL, GpuRun, rel, say, vis_window
 
 pytestmark = pytest.mark.gpu
 
@@ -27,6 +27,10 @@ CASES = {
     # the long-window end of the W = L sweep
     "med_w8_l8": MED.with_(window=8, seg_steps=8, seed=11, steps=(9, 12)),
     "med_w15_l15": MED.with_(window=15, seg_steps=15, seed=12, steps=(16, 17), img_len=60),
+    # the App. D algorithm as printed (window anchored at the segment start)
+    "med_anchored_k2_d3": MED.with_(mode="anchored", window=2, seg_steps=3, seed=13, steps=(8, 11)),
+    "med_anchored_k1_d1_d64": MED.with_(mode="anchored", window=1, seg_steps=1, hq=8, hkv=2,
+                                        head_dim=64, seed=14),
     "tiny": WL.TINY,
 }
 
@@ -34,7 +38,7 @@ CASES = {
 def _ref_layout(run):
     c = run.cfg
     return OL.build(run.spans, c.window, c.seg_steps, 128, c.max_seg_tokens, c.buffer_tokens,
-                    with_tiles=False)
+                    with_tiles=False, mode=c.mode)
 
 
 @pytest.mark.parametrize("name", list(CASES))
@@ -53,7 +57,7 @@ def test_fwd_bwd_full_parity(name):
     acc = {n: [[], []] for n in ("o", "lse", "dq", "dk", "dv")}
     for sg in ref.segments:
         q, k, v, dout = run.seg_np(sg)
-        mask = OL.visibility(sg, cfg.window)
+        mask = OL.visibility(sg, vis_window(cfg))
         o_r, lse_r = OA.forward(q, k, v, mask, run.scale)
         dq_r, dk_r, dv_r = OA.backward(q, k, v, mask, run.scale, dout)
         rows = slice(sg.start, sg.start + sg.length)
@@ -112,7 +116,7 @@ def test_full_size_sampled_rows_and_identities(cfg):
         loc = np.unique(np.concatenate([rng.integers(0, sg.length, 24), [0, sg.length - 1]]))
         q = run.inp.q_np(sg.canon[loc])
         dout = run.inp.dout_np(sg.start + loc)
-        mask = OL.visibility_rows(sg, cfg.window, loc)
+        mask = OL.visibility_rows(sg, vis_window(cfg), loc)
         o_r, lse_r = OA.forward_generic(q, k, v, mask, run.scale)
         rows = sg.start + loc
         o_g = run.o[torch.from_numpy(rows).cuda()].float().cpu().numpy()

@@ -16,9 +16,9 @@ pytestmark = pytest.mark.gpu
 GOLD = os.path.join(os.path.dirname(__file__), "golden")
 
 
-def _gpu(sp, W, L, tile, cap=0, buf=0):
-    say(f"  layout W={W} L={L} tile={tile} cap={cap} buf={buf} traj={sp.num_traj}")
-    pr = S.Problem.from_spans(sp, W, L, cap, buf, tile)
+def _gpu(sp, W, L, tile, cap=0, buf=0, mode="sliding"):
+    say(f"  layout W={W} L={L} tile={tile} cap={cap} buf={buf} traj={sp.num_traj} {mode}")
+    pr = S.Problem.from_spans(sp, W, L, cap, buf, tile, mode)
     return S.seg_build_layout(pr, device="cuda").host()
 
 
@@ -120,3 +120,54 @@ def test_empty_batch():
     sp = WL.explicit_spans([0, 0], [3, 3], [], [], [])
     got = _gpu(sp, 2, 2, 128)
     assert got["tok_src"].size == 0 and int(got["qt_ptr"][0]) == 0
+
+
+@pytest.mark.parametrize("mode", ["sliding", "anchored"])
+def test_tile_one(mode):
+    """Single-token tiles: every visible pair is its own tile, the diagonal
+    ones full."""
+    rng = np.random.default_rng(7)
+    T = [4, 0, 6]
+    ns = sum(T)
+    text = rng.integers(0, 9, size=ns)
+    sp = WL.explicit_spans(T, [3, 2, 5], rng.integers(0, 7, size=ns), text,
+                           [int(rng.integers(0, t + 1)) for t in text])
+    ref = OL.build(sp, 2, 2, 1, mode=mode)
+    assert (ref.qt_cls == OL.CLS_FULL).all()
+    _check_all(_gpu(sp, 2, 2, 1, mode=mode), ref)
+
+
+# ---- anchored mode (the App. D algorithm as printed)
+
+def test_anchored_hand_worked():
+    with open(os.path.join(GOLD, "alg2_anchored_example.json")) as f:
+        d = json.load(f)
+    s = d["spans"]
+    sp = WL.explicit_spans(s["steps"], s["prompt"], s["img"], s["text"], s["action"])
+    got = _gpu(sp, d["K"], d["delta"], 4, mode="anchored")
+    assert got["tok_src"].tolist() == d["tok_src"]
+    assert got["seg_info"][:, [0, 1, 2, 3, 4]].tolist() == d["segments"]
+    assert list(zip(got["loss_pred_row"].tolist(), got["loss_tgt_src"].tolist())) == \
+        [tuple(r) for r in d["loss_rows"]]
+    assert got["seg_pairs"].tolist() == d["pairs"]
+    _check_all(got, OL.build(sp, d["K"], d["delta"], 4, mode="anchored"))
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_anchored_random_spans(seed):
+    rng = np.random.default_rng(300 + seed)
+    n = int(rng.integers(1, 5))
+    T = rng.integers(0, 14, size=n)
+    ns = int(T.sum())
+    text = rng.integers(0, 40, size=ns)
+    sp = WL.explicit_spans(T, rng.integers(1, 50, size=n), rng.integers(0, 60, size=ns), text,
+                           [int(rng.integers(0, t + 1)) for t in text])
+    K, D = int(rng.integers(1, 5)), int(rng.integers(1, 5))
+    tile = int(rng.choice([1, 3, 16, 128]))
+    buf = int(rng.choice([0, 0, 900]))
+    try:
+        ref = OL.build(sp, K, D, tile, buffer_tokens=buf, mode="anchored")
+    except OL.CapacityError:
+        ref = OL.build(sp, K, D, tile, mode="anchored")
+        buf = 0
+    _check_all(_gpu(sp, K, D, tile, buf=buf, mode="anchored"), ref)
