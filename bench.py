@@ -125,7 +125,7 @@ class PathRun:
         }
         # rollout log-probs: the current policy's log-probs (one forward-only
         # call before timing) plus N(0, 0.1) noise, as the workload specifies
-        fwd_only = S.LossCfg(cfg.eps_low, cfg.eps_high, 0.0, 1.0 / R, 1.0, False)
+        fwd_only = S.LossCfg(cfg.eps_low, cfg.eps_high, cfg.dual_clip, 1.0 / R, 1.0, False)
         zero = torch.zeros(R, dtype=torch.float32, device=dev)
         S.seg_logprob_loss(self.h, self.lay.loss_pred_row, self.w, self.tgt, zero, self.adv,
                            self.lay.loss_traj, fwd_only,
@@ -134,7 +134,8 @@ class PathRun:
         self.old = (self.lp_out["logp"] + noise).contiguous()
         # reference-policy log-probs: the current ones minus the same noise
         self.ref = (self.lp_out["logp"] - noise).contiguous()
-        self.loss_cfg = S.LossCfg(cfg.eps_low, cfg.eps_high, 0.0, 1.0 / R, 1.0, True, KL_COEF)
+        self.loss_cfg = S.LossCfg(cfg.eps_low, cfg.eps_high, cfg.dual_clip, 1.0 / R, 1.0, True,
+                                  KL_COEF)
         self.ref_cfg = fwd_only
         self.ref_out = dict(self.lp_out, dh=None, dw=None, kl_tok=None)
         torch.cuda.synchronize()
@@ -248,7 +249,7 @@ def cpu_baseline(cfg, budget_note):
     from paper_2607_11185_amd import workload as WL
     inp = WL.Inputs(cfg)
     ref = OL.build(inp.spans, cfg.window, cfg.seg_steps, 128, cfg.max_seg_tokens,
-                   cfg.buffer_tokens, with_tiles=False)
+                   cfg.buffer_tokens, with_tiles=False, mode=cfg.mode)
     sg = ref.segments[0]
     q = inp.q_np(sg.canon)[:, :1]
     k = inp.k_np(sg.canon)[:, :1]
@@ -256,7 +257,7 @@ def cpu_baseline(cfg, budget_note):
     dout = inp.dout_np(np.arange(sg.start, sg.start + sg.length))[:, :1]
     scale = 1.0 / math.sqrt(cfg.head_dim)
     t0 = time.perf_counter()
-    mask = OL.visibility(sg, cfg.window)
+    mask = OL.visibility(sg, None if cfg.mode == "anchored" else cfg.window)
     OA.forward(q, k, v, mask, scale)
     OA.backward(q, k, v, mask, scale, dout)
     dt = time.perf_counter() - t0
@@ -301,7 +302,7 @@ def pmc_driver(cfg_name):
     cfg = WL.CONFIGS[cfg_name]
     inp = WL.Inputs(cfg)
     pr = S.Problem.from_spans(inp.spans, cfg.window, cfg.seg_steps, cfg.max_seg_tokens,
-                              cfg.buffer_tokens, 128)
+                              cfg.buffer_tokens, 128, cfg.mode)
     lay = S.seg_build_layout(pr, device=dev)
     host = lay.host()
     src = host["tok_src"].astype(np.int64)
@@ -344,9 +345,10 @@ SWEEP_K = (1, 3, 5, 8, 10, 15)
 
 
 def sweep(cfg, steps, warmup):
-    """Kernel-level half of the paper's window sweep: W = L = K over the same
-    batch; per K the segmented step, the reference forward pass and the
-    training-item and visible-pair counts.  One JSON line."""
+    """Kernel-level half of the paper's window sweep: W = L = K (sliding) or
+    K = delta (anchored) over the same batch; per K the segmented step, the
+    reference forward pass and the training-item and visible-pair counts.
+    One JSON line."""
     import torch
     dev = torch.device("cuda:0")
     rows = []
@@ -367,7 +369,8 @@ def sweep(cfg, steps, warmup):
         run.free()
         del run
         torch.cuda.empty_cache()
-    print(json.dumps({"sweep": "W = L = K", "workload": cfg.name, "steps": steps,
+    label = "K = delta" if cfg.mode == "anchored" else "W = L = K"
+    print(json.dumps({"sweep": label, "workload": cfg.name, "steps": steps,
                       "warmup": warmup, "rows": rows}), flush=True)
 
 
@@ -376,7 +379,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--config", default="7b", help="workload name (7b, small, long, tiny)")
+    ap.add_argument("--config", default="7b", help="workload name (7b, 7b_anchored, small, long, tiny)")
     ap.add_argument("--no-stepwise", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", action="store_true",
@@ -417,6 +420,8 @@ def main():
     dom_ms = kern[dom]["ms_per_step"] / kern[dom]["launches_per_step"]
     dom_flop = KERNEL_FLOP_PER_PAIR_D[dom] * cfg.head_dim * seg.pairs * cfg.hq
     achieved = dom_flop / (dom_ms * 1e-3) / 1e12
+    cut = (f"anchored K={cfg.window} delta={cfg.seg_steps}" if cfg.mode == "anchored"
+           else f"W={cfg.window}, L={cfg.seg_steps}")
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ph["step"], 3),
@@ -425,9 +430,10 @@ def main():
         "config": {"workload": f"{cfg.name}-class segmented VCS step: {cfg.num_traj} trajectories "
                                f"x {cfg.steps[0]}-{cfg.steps[1]} turns, prompt {cfg.prompt_len}, "
                                f"{cfg.img_len} screenshot tokens, text {cfg.text_len[0]}-"
-                               f"{cfg.text_len[1]} (last {cfg.action_len} trained), W={cfg.window}, "
-                               f"L={cfg.seg_steps}, {cfg.hq}q/{cfg.hkv}kv heads, d={cfg.head_dim}, "
-                               f"hidden {cfg.hidden}, vocab {cfg.vocab}",
+                               f"{cfg.text_len[1]} (last {cfg.action_len} trained), {cut}, "
+                               f"{cfg.hq}q/{cfg.hkv}kv heads, d={cfg.head_dim}, "
+                               f"hidden {cfg.hidden}, vocab {cfg.vocab}, clip {cfg.eps_low}/"
+                               f"{cfg.eps_high}" + (f" cap {cfg.dual_clip}" if cfg.dual_clip else ""),
                    "packed_tokens": seg.sizes.packed_tokens, "traj_tokens": traj_tokens,
                    "segments": seg.sizes.num_segments, "visible_pairs_per_head": seg.pairs},
         "traj_tokens_per_s": round(traj_tokens / (ph["step"] * 1e-3), 1),
@@ -449,7 +455,9 @@ def main():
     torch.cuda.empty_cache()
 
     if not args.no_stepwise:
-        sw_cfg = cfg.with_(name=cfg.name + "_stepwise", seg_steps=1)
+        # step-wise decomposition: one item per turn holding its K (or W)
+        # most recent screenshots
+        sw_cfg = cfg.with_(name=cfg.name + "_stepwise", seg_steps=1, mode="sliding")
         sw = PathRun(sw_cfg, dev)
         ph2, kern2, _ = time_path(sw, args.steps, args.warmup)
         ref_sw = time_ref(sw, args.steps, args.warmup)

@@ -60,6 +60,7 @@ class Config:
     buffer_tokens: int = 0
     eps_low: float = 0.2
     eps_high: float = 0.2
+    dual_clip: float = 0.0  # ratio cap c of the dual clip (0: off)
     w_std: float = 0.02
     old_noise_std: float = 0.1
     seed: int = 0
@@ -81,7 +82,12 @@ SEVEN_B = Config("7b", 8, (30, 30), 512, 2691, (150, 400), 32, 3, 5, 28, 4, 128,
 STEPWISE_7B = SEVEN_B.with_(name="7b_stepwise", seg_steps=1)
 LONG = Config("long", 16, (10, 50), 512, 4096, (100, 600), 32, 5, 8, 28, 4, 128,
               3584, 151936, max_seg_tokens=65536, buffer_tokens=65536)
-CONFIGS = {c.name: c for c in (TINY, SMALL, SEVEN_B, STEPWISE_7B, LONG)}
+# The 7B-class batch cut the way the App. D algorithm does, with the paper's
+# RL settings (hyperparameter table): K = 5 screenshots kept, removal
+# threshold delta = 5, clip 0.2 / 0.28 with ratio cap c = 3.
+SEVEN_B_ANCHORED = SEVEN_B.with_(name="7b_anchored", mode="anchored", window=5, seg_steps=5,
+                                 eps_high=0.28, dual_clip=3.0)
+CONFIGS = {c.name: c for c in (TINY, SMALL, SEVEN_B, STEPWISE_7B, LONG, SEVEN_B_ANCHORED)}
 
 
 @dataclasses.dataclass
