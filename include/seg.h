@@ -119,7 +119,7 @@ typedef struct {
   int32_t loss_rows;      /* R: trained action tokens */
   int32_t num_qtiles;     /* tiles over all segments (q-tiles = k-tiles) */
   int32_t num_steps;
-  int32_t pad0;
+  int32_t max_seg_len;    /* rows of the longest segment */
   int64_t packed_tokens;  /* rows of the packed buffer, padding included */
   int64_t traj_tokens;    /* canonical tokens of the batch */
   int64_t tile_nnz_max;   /* lower-triangular tile count: bound on non-skipped tiles */

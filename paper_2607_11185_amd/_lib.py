@@ -43,12 +43,12 @@ class SegProblem(ctypes.Structure):
 class SegSizes(ctypes.Structure):
     _fields_ = [("num_segments", ctypes.c_int32), ("num_buffers", ctypes.c_int32),
                 ("loss_rows", ctypes.c_int32), ("num_qtiles", ctypes.c_int32),
-                ("num_steps", ctypes.c_int32), ("pad0", ctypes.c_int32),
+                ("num_steps", ctypes.c_int32), ("max_seg_len", ctypes.c_int32),
                 ("packed_tokens", ctypes.c_int64), ("traj_tokens", ctypes.c_int64),
                 ("tile_nnz_max", ctypes.c_int64), ("workspace_bytes", ctypes.c_size_t)]
 
     def as_dict(self):
-        return {f: getattr(self, f) for f, _ in self._fields_ if f != "pad0"}
+        return {f: getattr(self, f) for f, _ in self._fields_}
 
 
 class SegLayout(ctypes.Structure):

@@ -118,11 +118,14 @@ __global__ void __launch_bounds__(256) k_delta(const TI *__restrict__ o, const T
 
 // ------------------------------------------------------------- pipelined kernels
 //
-// Tiles of 64 rows x d (row-major, bf16) are double-buffered in LDS: the
+// Tiles of 64 rows x d (row-major, bf16) are multi-buffered in LDS: the
 // loads of the next unit are in flight while the current one is computed.
-// The forward and dQ kernels fill with direct 16-byte global->LDS loads; the
-// dK/dV kernel, which has registers to spare, stages the next unit in
-// registers (see the note on wait counts below).  Rows are stored with a
+// The forward and dQ kernels fill with direct 16-byte buffer->LDS loads; the
+// dK/dV kernel stages the next unit in registers (see the note on wait counts
+// below).  All tile loads go through buffer resources that start at the
+// segment's first row, so a lane's offset inside a tile is fixed for the
+// kernel and a unit adds one scalar; rows past the segment read as zeros.
+// Rows are stored with a
 // 16-byte-chunk swizzle that keeps both 16-byte row reads (MFMA operands
 // contracting over d; 16 lanes per LDS cycle) and 4x16 transpose reads
 // (ds_read_b64_tr_b16: operands contracting over the rows; 32 lanes per
@@ -193,12 +196,12 @@ __device__ __forceinline__ bf16x8 frag_tr(const char *tile, int R, int offa, int
   return r;
 }
 
-// Lane coordinates of a 64-row tile fill by NW waves (PW direct 16-byte
-// global->LDS loads per lane; each wave instruction fills 1 KB of LDS,
-// lane-contiguous).  The swizzle is applied by choosing which global chunk
-// each lane loads.
+// Lane coordinates of a register-staged 64-row tile fill by NW waves (PW
+// 16-byte chunks per lane, each wave instruction covering 1 KB of the tile,
+// lane-contiguous in LDS); the swizzle is applied by choosing which global
+// chunk each lane loads.  `store` writes the staged registers to LDS.
 template <int D, int NW>
-struct FillPlan {
+struct StagePlan {
   static constexpr int CPR = D / 8, PW = 64 * CPR / (64 * NW);
   static_assert(PW >= 1, "tile too small for the wave count");
   int row[PW], chunk[PW];  // tile row and element offset of the lane's 16 bytes
@@ -210,45 +213,6 @@ struct FillPlan {
       chunk[i] = ((s % CPR) ^ swz<D>(row[i])) * 8;
     }
   }
-  // rows r0 + min(row, vrows - 1) of `base` (stride elements per row)
-  __device__ __forceinline__ void issue(unsigned short *tile, const unsigned short *base, long stride,
-                                        int r0, int vrows, int wave) const {
-    // device pass only: the host pass of clang drops the launch stub of a
-    // kernel that reaches this address-space cast
-#if defined(__HIP_DEVICE_COMPILE__)
-#pragma unroll
-    for (int i = 0; i < PW; ++i) {
-      const long r = r0 + min(row[i], vrows - 1);
-      __builtin_amdgcn_global_load_lds(
-          base + r * stride + chunk[i],
-          (__attribute__((address_space(3))) void *)(tile + (wave * PW + i) * 64 * 8), 16, 0, 0);
-    }
-#endif
-  }
-};
-
-// Register-staged fill of the same lane coordinates: `load` issues the global
-// loads into registers, `store` writes them to LDS.
-template <int D, int NW>
-struct StagePlan {
-  static constexpr int CPR = D / 8, PW = 64 * CPR / (64 * NW);
-  int row[PW], chunk[PW];
-  __device__ __forceinline__ void init(int wave, int lane) {
-#pragma unroll
-    for (int i = 0; i < PW; ++i) {
-      const int s = (wave * PW + i) * 64 + lane;
-      row[i] = s / CPR;
-      chunk[i] = ((s % CPR) ^ swz<D>(row[i])) * 8;
-    }
-  }
-  __device__ __forceinline__ void load(u16x8 (&st)[PW], const unsigned short *base, long stride,
-                                       int r0, int vrows) const {
-#pragma unroll
-    for (int i = 0; i < PW; ++i) {
-      const long r = r0 + min(row[i], vrows - 1);
-      st[i] = *reinterpret_cast<const u16x8 *>(base + r * stride + chunk[i]);
-    }
-  }
   __device__ __forceinline__ void store(unsigned short *tile, const u16x8 (&st)[PW], int wave,
                                         int lane) const {
 #pragma unroll
@@ -257,10 +221,45 @@ struct StagePlan {
   }
 };
 
-// one dword per lane into 64 consecutive dwords of LDS (direct load)
-__device__ __forceinline__ void fill64_dw(void *dst, const void *src_lane) {
+// Raw buffer resource over [base, base + bytes): loads past the end return
+// zeros, so a tile fill needs no clamping of its rows.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, unsigned bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes,
+                                           0x00020000);
+}
+
+// Direct buffer->LDS fill of a 64-row tile by NW waves: per-lane byte offsets
+// are fixed for the kernel (tile row * row stride + swizzled chunk); a unit
+// only adds its first row's byte offset (a scalar).
+template <int D, int NW>
+struct BufFill {
+  static constexpr int CPR = D / 8, PW = 64 * CPR / (64 * NW);
+  int voff[PW];
+  __device__ __forceinline__ void init(int wave, int lane, int row_bytes) {
+#pragma unroll
+    for (int i = 0; i < PW; ++i) {
+      const int s = (wave * PW + i) * 64 + lane;
+      const int row = s / CPR;
+      voff[i] = row * row_bytes + ((s % CPR) ^ swz<D>(row)) * 16;
+    }
+  }
+  __device__ __forceinline__ void issue(unsigned short *tile, __amdgpu_buffer_rsrc_t rs, int soff,
+                                        int wave) const {
 #if defined(__HIP_DEVICE_COMPILE__)
-  __builtin_amdgcn_global_load_lds(src_lane, (__attribute__((address_space(3))) void *)dst, 4, 0, 0);
+#pragma unroll
+    for (int i = 0; i < PW; ++i)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rs, (__attribute__((address_space(3))) void *)(tile + (wave * PW + i) * 64 * 8), 16,
+          voff[i], soff, 0, 0);
+#endif
+  }
+};
+
+// one dword per lane (lane l: byte l*4 + soff) into 64 consecutive dwords of LDS
+__device__ __forceinline__ void buf64_dw(void *dst, __amdgpu_buffer_rsrc_t rs, int lane, int soff) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void *)dst, 4,
+                                           lane * 4, soff, 0, 0);
 #endif
 }
 
@@ -273,7 +272,8 @@ __device__ __forceinline__ void fill64_dw(void *dst, const void *src_lane) {
 // compute.  Every LDS access of a step goes through those parameters.  While
 // a direct load is in flight the compiler also gives up counted LDS waits
 // (every wait becomes lgkmcnt(0)), which serialises read-ahead; the dK/dV
-// kernel therefore stages its next unit in registers instead.
+// kernel, whose loads must stay in flight across a whole step, therefore
+// stages its next unit in registers instead.
 
 __device__ __forceinline__ void wait_all_and_sync() {
   __builtin_amdgcn_s_waitcnt(0);
@@ -388,17 +388,22 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd(
 
   LaneOffsets<D> lo;
   lo.init(lane, 0);
-  FillPlan<D, 4> fp;
-  fp.init(wave, lane);
   const long kv_stride = (long)hkv * D;
-  const unsigned short *kbase = k + (long)hk * D + (long)tr.start * kv_stride;
-  const unsigned short *vbase = v + (long)hk * D + (long)tr.start * kv_stride;
+  const int row_bytes = (int)(kv_stride * 2);
+  BufFill<D, 4> fp;
+  fp.init(wave, lane, row_bytes);
+  // the segment's rows of this kv head; rows past the segment read as zeros
+  const __amdgpu_buffer_rsrc_t rK =
+      make_rsrc(k + (long)hk * D + (long)tr.start * kv_stride, (unsigned)tr.len * row_bytes);
+  const __amdgpu_buffer_rsrc_t rV =
+      make_rsrc(v + (long)hk * D + (long)tr.start * kv_stride, (unsigned)tr.len * row_bytes);
+  const __amdgpu_buffer_rsrc_t rM = make_rsrc(tok_meta + tr.start, (unsigned)tr.len * 4);
 
   auto issue = [&](const Unit &u, unsigned short *__restrict__ nK, unsigned short *__restrict__ nV,
                    int *__restrict__ nM) __attribute__((always_inline)) {
-    fp.issue(nK, kbase, kv_stride, u.r0, u.vrows, wave);
-    fp.issue(nV, vbase, kv_stride, u.r0, u.vrows, wave);
-    if (wave == 0) fill64_dw(nM, tok_meta + tr.start + u.r0 + min(lane, u.vrows - 1));
+    fp.issue(nK, rK, u.r0 * row_bytes, wave);
+    fp.issue(nV, rV, u.r0 * row_bytes, wave);
+    if (wave == 0) buf64_dw(nM, rM, lane, u.r0 * 4);
   };
   auto compute = [&](const Unit &u, const char *__restrict__ sK, const char *__restrict__ sV,
                      const int *__restrict__ sM) __attribute__((always_inline)) {
@@ -519,18 +524,20 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd(
   }
 }
 
-// dK/dV, one wave per SIMD: one block = one k-tile x one kv head, 4 waves of
-// 32 keys each.  A wave holds the K and V fragments of its keys and the dK
-// and dV accumulators over the whole head dimension (about 300 registers, so
-// one wave per SIMD).  Per unit (64 rows of one query head) and 32-row block:
-//   S = Q K^T, dP = dO V^T (queries on accumulator rows),
-//   P = exp2(S * scale - lse), dS = P (dP - Delta),
-//   dV += P^T dO, dK += dS^T Q (dO^T, Q^T by transpose reads).
-// P and dS never leave the wave: the only barrier of a unit is the swap of
-// the double buffer, whose next unit is staged in registers.  Units are 64-row halves of the listed q-tiles, for
-// every query head of the group.  No atomics.
+// dK/dV: one block = one k-tile x one kv head, 8 waves, two per SIMD.  Waves
+// 0-3 (the P side) each hold K of 32 keys and their dV accumulator; waves
+// 4-7 (the dS side) hold V of the same 32 keys and their dK accumulator.  A
+// unit is 64 rows of one query head; per 32-row block:
+//   P side:  S = Q K^T, P = exp2(S * scale - lse) (masked pairs give 0),
+//            P -> LDS, dV += P^T dO
+//   dS side: dP = dO V^T, P <- LDS, dS = P (dP - Delta), dK += dS^T Q
+// The dS side works one unit behind the P side, so the P of a unit crosses
+// the barrier that ends a step; Q/dO tiles therefore live in three buffers
+// (the P side's unit, the dS side's unit, and the next unit being staged in
+// registers).  Units are 64-row halves of the listed q-tiles, for every query
+// head of the group.  No atomics.
 template <int D, class TO>
-__global__ void __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1))) k_attn_bwd_dkdv(
+__global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
     const unsigned short *__restrict__ q, const unsigned short *__restrict__ k,
     const unsigned short *__restrict__ v, const unsigned short *__restrict__ dout,
     const float *__restrict__ lse2, const float *__restrict__ delta,
@@ -539,264 +546,257 @@ __global__ void __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 
     const int32_t *__restrict__ kt_row, const uint8_t *__restrict__ kt_cls, int ntiles, int hq,
     int hkv, int W, float scale_log2, float scale, long P, TO *__restrict__ dk,
     TO *__restrict__ dv) {
-  constexpr int KK = D / 16, T64 = 64 * D, DB = D / 32;
-  __shared__ __attribute__((aligned(16))) unsigned short sQ0[T64], sQ1[T64], sD0[T64], sD1[T64];
-  __shared__ __attribute__((aligned(16))) float sL0[64], sL1[64], sE0[64], sE1[64];
-  __shared__ __attribute__((aligned(16))) int sM0[64], sM1[64];
+  constexpr int KK = D / 16, T64 = 64 * D, DB = D / 32, NB = 3;
+  __shared__ __attribute__((aligned(16))) unsigned short sQ[NB][T64], sD[NB][T64];
+  __shared__ __attribute__((aligned(16))) unsigned short sP[2][64 * TQ];
+  __shared__ __attribute__((aligned(16))) float sL[NB][64], sE[NB][64];
+  __shared__ __attribute__((aligned(16))) int sM[NB][64];
 
-  // k-tiles in natural order: within a segment the earliest k-tiles have the
-  // longest transposed-CSR columns, so they start first
   int g, hk;
-  if (!xcd_block(hkv, ntiles, false, g, hk)) return;
+  {
+    // XCD x takes tiles [x*C, (x+1)*C) and runs them kv head by kv head, so
+    // the blocks resident on one XCD read the same query heads
+    const int bx = blockIdx.x, x = bx & 7, i = bx >> 3;
+    const int C = (ntiles + 7) >> 3;
+    hk = i / C;
+    g = x * C + (i - hk * C);
+    if (g >= ntiles || hk >= hkv) return;
+  }
   const int grp = hq / hkv;
   const TileRows tr = tile_rows(seg_info, tile_seg, g);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int side = wave >> 2, kg = wave & 3;  // side 0: P, dV; side 1: dS, dK
   const int col = lane & 31, hh = lane >> 5;
-  const int kloc = wave * 32 + col;
+  const int kloc = kg * 32 + col;
   const bool kvalid = kloc < tr.nrows;
   const int kr = tr.row0 + (kvalid ? kloc : 0);
   const int kexp = key_expiry(tok_meta[tr.start + kr], W);
 
-  bf16x8 kf[KK], vf[KK];
+  // K fragments (P side) or V fragments (dS side) of the wave's 32 keys
+  bf16x8 xf[KK];
   {
     const long row = tr.start + kr;
-    const unsigned short *ks = k + (row * hkv + hk) * D, *vs = v + (row * hkv + hk) * D;
+    const unsigned short *src = (side == 0 ? k : v) + (row * hkv + hk) * D;
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      kf[kk] = lds8(ks + kk * 16 + hh * 8);
-      vf[kk] = lds8(vs + kk * 16 + hh * 8);
-    }
+    for (int kk = 0; kk < KK; ++kk) xf[kk] = lds8(src + kk * 16 + hh * 8);
   }
-  f32x16 dkacc[DB], dvacc[DB];
+  f32x16 acc[DB];  // dV (P side) or dK (dS side): D[i = key][j = d]
 #pragma unroll
-  for (int db = 0; db < DB; ++db) {
-    dkacc[db] = f32x16{};
-    dvacc[db] = f32x16{};
-  }
+  for (int db = 0; db < DB; ++db) acc[db] = f32x16{};
 
   LaneOffsets<D> lo;
   lo.init(lane, 0);
   const long q_stride = (long)hq * D;
   const int e0 = kt_ptr[g], e1 = kt_ptr[g + 1];
 
-  // register-staged prefetch of one unit: Q and dO rows, and one per-row
-  // value by waves 0-2 (log2-sum-exp, Delta, turn)
-  StagePlan<D, 4> sp;
+  // register-staged fill of one unit by all 8 waves: Q and dO rows, and one
+  // per-row value by waves 0-2 (log2-sum-exp, Delta, turn).  Buffer
+  // resources start at the segment's first row of the group's first head;
+  // a unit adds a scalar byte offset, and rows past the end read as zeros.
+  StagePlan<D, 8> sp;
   sp.init(wave, lane);
-  u16x8 stq[StagePlan<D, 4>::PW], sto[StagePlan<D, 4>::PW];
+  constexpr int PW = StagePlan<D, 8>::PW;
+  const int qrow_bytes = (int)(q_stride * 2);
+  int voff[PW];
+#pragma unroll
+  for (int i = 0; i < PW; ++i) voff[i] = sp.row[i] * qrow_bytes + sp.chunk[i] * 2;
+  const long hbase = (long)hk * grp * D + (long)tr.start * q_stride;
+  const unsigned qbytes = (unsigned)(tr.len * (long)qrow_bytes);
+  const __amdgpu_buffer_rsrc_t rQ = make_rsrc(q + hbase, qbytes);
+  const __amdgpu_buffer_rsrc_t rO = make_rsrc(dout + hbase, qbytes);
+  const long pbase = (long)hk * grp * P + tr.start;
+  const unsigned pbytes = (unsigned)(((long)(grp - 1) * P + tr.len) * 4);
+  const __amdgpu_buffer_rsrc_t rS = make_rsrc(wave == 0 ? (const void *)(lse2 + pbase)
+                                              : wave == 1 ? (const void *)(delta + pbase)
+                                                          : (const void *)(tok_meta + tr.start),
+                                              wave < 2 ? pbytes : (unsigned)tr.len * 4);
+  u16x8 stq[PW], sto[PW];
   int stv = 0;
-  auto load = [&](const Unit &u, int hi) __attribute__((always_inline)) {
-    const int h = hk * grp + hi;
-    sp.load(stq, q + (long)h * D + (long)tr.start * q_stride, q_stride, u.r0, u.vrows);
-    sp.load(sto, dout + (long)h * D + (long)tr.start * q_stride, q_stride, u.r0, u.vrows);
-    const long lrow = tr.start + u.r0 + min(lane, u.vrows - 1);
-    if (wave == 0) stv = __builtin_bit_cast(int, lse2[(long)h * P + lrow]);
-    else if (wave == 1) stv = __builtin_bit_cast(int, delta[(long)h * P + lrow]);
-    else if (wave == 2) stv = tok_meta[lrow];
-  };
-  auto store = [&](unsigned short *__restrict__ nQ, unsigned short *__restrict__ nD,
-                   float *__restrict__ nL, float *__restrict__ nE, int *__restrict__ nM)
-                   __attribute__((always_inline)) {
-    sp.store(nQ, stq, wave, lane);
-    sp.store(nD, sto, wave, lane);
-    if (wave == 0) nL[lane] = __builtin_bit_cast(float, stv);
-    else if (wave == 1) nE[lane] = __builtin_bit_cast(float, stv);
-    else if (wave == 2) nM[lane] = stv;
-  };
-  // S and dP of one 32-row block
-  auto sdp = [&](const char *__restrict__ sQ, const char *__restrict__ sdO, const int qb,
-                 f32x16 &s, f32x16 &dp) __attribute__((always_inline)) {
-    bf16x8 aq[KK], ad[KK];
+  auto load = [&](int r0, int vrows, int hi) __attribute__((always_inline)) {
+    const int so = r0 * qrow_bytes + hi * D * 2;
 #pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      aq[kk] = frag_row<D>(sQ, qb * 32, lo.row[kk]);
-      ad[kk] = frag_row<D>(sdO, qb * 32, lo.row[kk]);
+    for (int i = 0; i < PW; ++i) {
+      stq[i] = __builtin_bit_cast(u16x8, __builtin_amdgcn_raw_buffer_load_b128(rQ, voff[i], so, 0));
+      sto[i] = __builtin_bit_cast(u16x8, __builtin_amdgcn_raw_buffer_load_b128(rO, voff[i], so, 0));
     }
-    s = f32x16{};
-    dp = f32x16{};
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      s = mfma32(aq[kk], kf[kk], s);
-      dp = mfma32(ad[kk], vf[kk], dp);
-    }
-    // Scheduling groups (mask 0x100: LDS reads, 0x008: MFMA), in program
-    // order for the whole unit: row reads run 4 ahead of the products.  The
-    // compiler's own schedule issues each read right before its product.
-    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
-#pragma unroll
-    for (int i = 0; i < 2 * KK - 4; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+    if (wave < 3)
+      stv = __builtin_amdgcn_raw_buffer_load_b32(rS, lane * 4,
+                                                 (wave < 2 ? hi * (int)P * 4 : 0) + r0 * 4, 0);
   };
-  // P = exp2(S * scale - lse) (a masked pair gets exponent -inf, P = 0) and
-  // dS = P (dP - Delta), packed to bf16
-  auto pds = [&](const Unit &u, const bool masked, const float *__restrict__ sLse,
-                 const float *__restrict__ sDel, const int *__restrict__ sMeta, const int qb,
-                 f32x16 &s, f32x16 &dp, bf16x8 (&pa)[2], bf16x8 (&dsa)[2])
-                 __attribute__((always_inline)) {
+  auto store = [&](int b) __attribute__((always_inline)) {
+    sp.store(sQ[b], stq, wave, lane);
+    sp.store(sD[b], sto, wave, lane);
+    if (wave == 0) sL[b][lane] = __builtin_bit_cast(float, stv);
+    else if (wave == 1) sE[b][lane] = __builtin_bit_cast(float, stv);
+    else if (wave == 2) sM[b][lane] = stv;
+  };
+
+  // P side: one unit (rows r0 .. r0 + vrows - 1, PARTIAL or ragged if masked)
+  auto p_side = [&](const int r0, const int vrows, const bool masked, const int b, const int pb)
+                    __attribute__((always_inline)) {
+    const char *cQ = reinterpret_cast<const char *>(sQ[b]);
+    const char *cD = reinterpret_cast<const char *>(sD[b]);
 #pragma unroll
-    for (int rg = 0; rg < 4; ++rg) {
-      const int base = qb * 32 + 8 * rg + 4 * hh;
-      const f32x4 L4 = *reinterpret_cast<const f32x4 *>(sLse + base);
-      const f32x4 D4 = *reinterpret_cast<const f32x4 *>(sDel + base);
-      i32x4 M4;
-      if (masked) M4 = *reinterpret_cast<const i32x4 *>(sMeta + base);
+    for (int qb = 0; qb < 2; ++qb) {
+      bf16x8 aq[KK];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r = rg * 4 + j, ql = base + j;
-        float x = fmaf(s[r], scale_log2, -L4[j]);
-        if (masked) {
-          const bool vis = kvalid & (ql < u.vrows) & (kr <= u.r0 + ql) & ((M4[j] >> 2) < kexp);
-          x = vis ? x : -INFINITY;
+      for (int kk = 0; kk < KK; ++kk) aq[kk] = frag_row<D>(cQ, qb * 32, lo.row[kk]);
+      f32x16 s = f32x16{};
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) s = mfma32(aq[kk], xf[kk], s);
+#pragma unroll
+      for (int rg = 0; rg < 4; ++rg) {
+        const f32x4 L4 = *reinterpret_cast<const f32x4 *>(&sL[b][qb * 32 + 8 * rg + 4 * hh]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) s[rg * 4 + j] = fmaf(s[rg * 4 + j], scale_log2, -L4[j]);
+      }
+      if (masked) {  // uniform branch: only the exponents change
+#pragma unroll
+        for (int rg = 0; rg < 4; ++rg) {
+          const int base = qb * 32 + 8 * rg + 4 * hh;
+          const i32x4 M4 = *reinterpret_cast<const i32x4 *>(&sM[b][base]);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const int ql = base + j;
+            const bool vis = kvalid & (ql < vrows) & (kr <= r0 + ql) & ((M4[j] >> 2) < kexp);
+            s[rg * 4 + j] = vis ? s[rg * 4 + j] : -INFINITY;
+          }
         }
-        s[r] = __builtin_amdgcn_exp2f(x);
-        dp[r] = s[r] * (dp[r] - D4[j]);
-      }
-    }
-    pa[0] = pack8(s, 0);
-    pa[1] = pack8(s, 8);
-    dsa[0] = pack8(dp, 0);
-    dsa[1] = pack8(dp, 8);
-    // this block's lse / Delta (/ turn) reads form their own group, so they
-    // do not take the slots of the transpose reads below
-    if (masked)
-      __builtin_amdgcn_sched_group_barrier(0x100, 12, 0);
-    else
-      __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
-  };
-  // dV += P^T dO, dK += dS^T Q for one 32-row block
-  auto dkv = [&](const char *__restrict__ sQ, const char *__restrict__ sdO, const int qb,
-                 const bf16x8 (&pa)[2], const bf16x8 (&dsa)[2]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int c2 = 0; c2 < 2; ++c2) {
-      bf16x8 bo[DB], bq[DB];
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        bo[db] = frag_tr<D>(sdO, qb * 32 + c2 * 16, lo.tra[db], lo.trb[db]);
-        bq[db] = frag_tr<D>(sQ, qb * 32 + c2 * 16, lo.tra[db], lo.trb[db]);
       }
 #pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        dvacc[db] = mfma32(pa[c2], bo[db], dvacc[db]);
-        dkacc[db] = mfma32(dsa[c2], bq[db], dkacc[db]);
+      for (int r = 0; r < 16; ++r) s[r] = __builtin_amdgcn_exp2f(s[r]);
+      bf16x8 pa[2];
+      pa[0] = pack8(s, 0);
+      pa[1] = pack8(s, 8);
+      // P in the accumulator's lane order, read back by the dS wave of the same keys
+      bf16x8 *pdst = reinterpret_cast<bf16x8 *>(sP[pb]) + ((qb * 4 + kg) * 2) * 64 + lane;
+      pdst[0] = pa[0];
+      pdst[64] = pa[1];
+#pragma unroll
+      for (int c2 = 0; c2 < 2; ++c2) {
+        bf16x8 bo[DB];
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+          bo[db] = frag_tr<D>(cD, qb * 32 + c2 * 16, lo.tra[db], lo.trb[db]);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) acc[db] = mfma32(pa[c2], bo[db], acc[db]);
       }
     }
-    // transpose reads run 4 fragments ahead of the products
-    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+  };
+  // dS side: one unit, whose P was written in the previous step
+  auto ds_side = [&](const int b, const int pb) __attribute__((always_inline)) {
+    const char *cQ = reinterpret_cast<const char *>(sQ[b]);
+    const char *cD = reinterpret_cast<const char *>(sD[b]);
 #pragma unroll
-    for (int i = 0; i < 4 * DB - 4; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    for (int qb = 0; qb < 2; ++qb) {
+      bf16x8 ad[KK];
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) ad[kk] = frag_row<D>(cD, qb * 32, lo.row[kk]);
+      f32x16 dp = f32x16{};
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) dp = mfma32(ad[kk], xf[kk], dp);
+      const bf16x8 *psrc = reinterpret_cast<const bf16x8 *>(sP[pb]) + ((qb * 4 + kg) * 2) * 64 + lane;
+      const bf16x8 p0 = psrc[0], p1 = psrc[64];
+#pragma unroll
+      for (int rg = 0; rg < 4; ++rg) {
+        const f32x4 D4 = *reinterpret_cast<const f32x4 *>(&sE[b][qb * 32 + 8 * rg + 4 * hh]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int r = rg * 4 + j;
+          const float pr = (float)(r < 8 ? p0[r] : p1[r - 8]);
+          dp[r] = pr * (dp[r] - D4[j]);
+        }
+      }
+      bf16x8 dsa[2];
+      dsa[0] = pack8(dp, 0);
+      dsa[1] = pack8(dp, 8);
+#pragma unroll
+      for (int c2 = 0; c2 < 2; ++c2) {
+        bf16x8 bq[DB];
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+          bq[db] = frag_tr<D>(cQ, qb * 32 + c2 * 16, lo.tra[db], lo.trb[db]);
+#pragma unroll
+        for (int db = 0; db < DB; ++db) acc[db] = mfma32(dsa[c2], bq[db], acc[db]);
+      }
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-  };
-  // One unit over its two 32-row blocks, in the order S/dP(0), softmax(0),
-  // S/dP(1), dV/dK(0), softmax(1), dV/dK(1) (measured best among the orders
-  // tried; it also keeps the live state within the register budget).
-  // FULL units with 64 query rows and every key of the tile valid need no
-  // predicate (kvalid is false only in a segment's last k-tile, which is a
-  // diagonal, PARTIAL tile); rows past vrows hold copies of the last row and
-  // are masked.  `masked` is a constant in each inlined copy.
-  auto compute = [&](const Unit &u, const bool masked, const char *__restrict__ sQ,
-                     const char *__restrict__ sdO, const float *__restrict__ sLse,
-                     const float *__restrict__ sDel, const int *__restrict__ sMeta)
-                     __attribute__((always_inline)) {
-    f32x16 s0, dp0, s1, dp1;
-    bf16x8 pa0[2], ds0[2], pa1[2], ds1[2];
-    sdp(sQ, sdO, 0, s0, dp0);
-    pds(u, masked, sLse, sDel, sMeta, 0, s0, dp0, pa0, ds0);
-    sdp(sQ, sdO, 1, s1, dp1);
-    dkv(sQ, sdO, 0, pa0, ds0);
-    pds(u, masked, sLse, sDel, sMeta, 1, s1, dp1, pa1, ds1);
-    dkv(sQ, sdO, 1, pa1, ds1);
-  };
-  auto step = [&](const Unit &u, const bool more, const Unit &nu, int nhi,
-                  const unsigned short *__restrict__ cQ, const unsigned short *__restrict__ cD,
-                  const float *__restrict__ cL, const float *__restrict__ cE,
-                  const int *__restrict__ cM, unsigned short *__restrict__ nQ,
-                  unsigned short *__restrict__ nD, float *__restrict__ nL, float *__restrict__ nE,
-                  int *__restrict__ nM) __attribute__((always_inline)) {
-    if (more) load(nu, nhi);  // in flight during the products below
-    const char *q8 = reinterpret_cast<const char *>(cQ), *d8 = reinterpret_cast<const char *>(cD);
-    if (__builtin_expect(u.partial | (u.vrows < 64), 0))
-      compute(u, true, q8, d8, cL, cE, cM);
-    else
-      compute(u, false, q8, d8, cL, cE, cM);
-    if (more) store(nQ, nD, nL, nE, nM);
   };
 
   if (e0 < e1) {
-    // Next unit: other half of this tile, else next head, else next entry.
-    // Every field is computed from scalars: partial assignments of a
-    // struct in different branches ended up in dynamically indexed private
-    // memory, whose loads wait behind the prefetch loads.
-    auto advance = [&](const Unit &cu, int chi, Unit &n, int &nh) __attribute__((always_inline)) -> bool {
-      const bool second = cu.half == 0 && cu.r0 + 64 < tr.len;
-      const bool head = !second && chi + 1 < grp;
-      const bool entry = !second && !head && cu.e + 1 < e1;
-      if (!(second || head || entry)) return false;
-      int e = cu.e, half = 0, r0, partial = cu.partial;
-      if (second) {
-        half = 1;
-        r0 = cu.r0 + 64;
-        nh = chi;
-      } else if (head) {
-        r0 = cu.r0 - cu.half * 64;
-        nh = chi + 1;
-      } else {
-        e = cu.e + 1;
-        r0 = (kt_row[e] - tr.qbase) * TQ;
-        partial = kt_cls[e] == SEG_TILE_PARTIAL;
-        nh = 0;
-      }
-      n.e = e;
-      n.half = half;
-      n.r0 = r0;
-      n.vrows = min(64, tr.len - r0);
-      n.partial = partial;
-      return true;
-    };
-    Unit cur = make_unit(kt_row, kt_cls, e0, 0, tr.qbase, tr.len), nx;
-    int hcur = 0, hnx = 0;
-    load(cur, hcur);
-    store(sQ0, sD0, sL0, sE0, sM0);
+    // Unit state as scalars: CSR entry, half, query head, first row.
+    int ce = e1 - 1, chalf = 0, chi = 0;
+    int cr0 = (kt_row[ce] - tr.qbase) * TQ;
+    int cpart = kt_cls[ce] == SEG_TILE_PARTIAL;
+    load(cr0, min(64, tr.len - cr0), 0);
+    store(0);
     __syncthreads();
-    for (;;) {
-      bool more = advance(cur, hcur, nx, hnx);
-      step(cur, more, nx, hnx, sQ0, sD0, sL0, sE0, sM0, sQ1, sD1, sL1, sE1, sM1);
+    bool have_cur = true;  // the P side has a unit this step
+    int b = 0, pb = 0;     // buffers of the P side's unit (the dS side uses the previous ones)
+    for (int n = 0;; ++n) {
+      // next unit: other half of this tile, else next head, else next entry
+      int ne = ce, nhalf = 0, nhi = chi, nr0 = 0, npart = cpart;
+      bool more = false;
+      if (have_cur) {
+        const bool second = chalf == 0 && cr0 + 64 < tr.len;
+        const bool head = !second && chi + 1 < grp;
+        const bool entry = !second && !head && ce > e0;
+        more = second || head || entry;
+        if (second) {
+          nhalf = 1;
+          nr0 = cr0 + 64;
+        } else if (head) {
+          nr0 = cr0 - chalf * 64;
+          nhi = chi + 1;
+        } else if (entry) {
+          ne = ce - 1;
+          nr0 = (kt_row[ne] - tr.qbase) * TQ;
+          npart = kt_cls[ne] == SEG_TILE_PARTIAL;
+          nhi = 0;
+        }
+      }
+      const int nb = b == NB - 1 ? 0 : b + 1;
+      if (more) load(nr0, min(64, tr.len - nr0), nhi);
+      if (side == 0) {
+        if (have_cur) {
+          const int vrows = min(64, tr.len - cr0);
+          p_side(cr0, vrows, (cpart | (vrows < 64)) != 0, b, pb);
+        }
+      } else if (n > 0) {
+        ds_side(b == 0 ? NB - 1 : b - 1, pb ^ 1);
+      }
+      if (more) store(nb);
       __syncthreads();
-      if (!more) break;
-      cur = nx;
-      hcur = hnx;
-      more = advance(cur, hcur, nx, hnx);
-      step(cur, more, nx, hnx, sQ1, sD1, sL1, sE1, sM1, sQ0, sD0, sL0, sE0, sM0);
-      __syncthreads();
-      if (!more) break;
-      cur = nx;
-      hcur = hnx;
+      if (!have_cur) break;
+      have_cur = more;
+      ce = ne;
+      chalf = nhalf;
+      chi = nhi;
+      cr0 = nr0;
+      cpart = npart;
+      b = nb;
+      pb ^= 1;
     }
   }
 
   // stage through LDS (RP key rows per pass) for coalesced stores;
   // accumulator D[i = key][j = d]
   wait_all_and_sync();
-  TO *st = reinterpret_cast<TO *>(sQ0);
+  TO *st = reinterpret_cast<TO *>(&sQ[0][0]);
   constexpr int CH = 16 / sizeof(TO);   // elements per 16-byte chunk
   constexpr int RP = 128 / sizeof(TO);  // key rows per pass (16 KB)
+  const float mul = side == 0 ? 1.f : scale;
 #pragma unroll
   for (int which = 0; which < 2; ++which) {
-    TO *dst = which == 0 ? dk : dv;
+    TO *dst = which == 0 ? dv : dk;
 #pragma unroll
     for (int pass = 0; pass < TQ / RP; ++pass) {
-      if (wave * 32 >= pass * RP && wave * 32 < (pass + 1) * RP) {
+      if (side == which && kg * 32 >= pass * RP && kg * 32 < (pass + 1) * RP) {
 #pragma unroll
         for (int db = 0; db < DB; ++db)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const int kl = wave * 32 + 8 * (r >> 2) + 4 * hh + (r & 3) - pass * RP;
-            const float val = which == 0 ? dkacc[db][r] * scale : dvacc[db][r];
+            const int kl = kg * 32 + 8 * (r >> 2) + 4 * hh + (r & 3) - pass * RP;
+            const float val = acc[db][r] * mul;
             const int dd = db * 32 + col;
             if constexpr (sizeof(TO) == 2)
               st[kl * D + dd] = f2bf_bits(val);
@@ -805,7 +805,7 @@ __global__ void __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 
           }
       }
       __syncthreads();
-      for (int c = threadIdx.x; c < RP * D / CH; c += 256) {
+      for (int c = threadIdx.x; c < RP * D / CH; c += 512) {
         const int kl = c / (D / CH), ch = c % (D / CH);
         const int key = pass * RP + kl;
         if (key < tr.nrows) {
@@ -866,17 +866,22 @@ __global__ void __launch_bounds__(256, 2) k_attn_bwd_dq(
 
   LaneOffsets<D> lo;
   lo.init(lane, 0);
-  FillPlan<D, 4> fp;
-  fp.init(wave, lane);
   const long kv_stride = (long)hkv * D;
-  const unsigned short *kbase = k + (long)hk * D + (long)tr.start * kv_stride;
-  const unsigned short *vbase = v + (long)hk * D + (long)tr.start * kv_stride;
+  const int row_bytes = (int)(kv_stride * 2);
+  BufFill<D, 4> fp;
+  fp.init(wave, lane, row_bytes);
+  // the segment's rows of this kv head; rows past the segment read as zeros
+  const __amdgpu_buffer_rsrc_t rK =
+      make_rsrc(k + (long)hk * D + (long)tr.start * kv_stride, (unsigned)tr.len * row_bytes);
+  const __amdgpu_buffer_rsrc_t rV =
+      make_rsrc(v + (long)hk * D + (long)tr.start * kv_stride, (unsigned)tr.len * row_bytes);
+  const __amdgpu_buffer_rsrc_t rM = make_rsrc(tok_meta + tr.start, (unsigned)tr.len * 4);
 
   auto issue = [&](const Unit &u, unsigned short *__restrict__ nK, unsigned short *__restrict__ nV,
                    int *__restrict__ nM) __attribute__((always_inline)) {
-    fp.issue(nK, kbase, kv_stride, u.r0, u.vrows, wave);
-    fp.issue(nV, vbase, kv_stride, u.r0, u.vrows, wave);
-    if (wave == 0) fill64_dw(nM, tok_meta + tr.start + u.r0 + min(lane, u.vrows - 1));
+    fp.issue(nK, rK, u.r0 * row_bytes, wave);
+    fp.issue(nV, rV, u.r0 * row_bytes, wave);
+    if (wave == 0) buf64_dw(nM, rM, lane, u.r0 * 4);
   };
   auto compute = [&](const Unit &u, const char *__restrict__ sK, const char *__restrict__ sV,
                      const int *__restrict__ sM) __attribute__((always_inline)) {
@@ -1010,6 +1015,13 @@ void check_common(const seg_layout *L, const seg_sizes *sz, seg_dtype dt, int hq
             L->tile);
   SEG_CHECK(L->window >= 1, SEG_ERR_ARG, "layout window not set (build the layout first)");
   SEG_CHECK((long)sz->packed_tokens * hq * d < (1L << 40), SEG_ERR_CAPACITY, "tensor too large");
+  // tile loads address a segment's rows, and the per-row values of a head
+  // group, with 32-bit byte offsets from one buffer resource
+  SEG_CHECK((long)sz->max_seg_len * hq * d * 2 <= INT32_MAX, SEG_ERR_CAPACITY,
+            "a segment of %d rows exceeds the 2 GiB addressable per tile stream", sz->max_seg_len);
+  SEG_CHECK((long)sz->packed_tokens * hq * 4 <= INT32_MAX, SEG_ERR_CAPACITY,
+            "%lld packed rows x %d heads of fp32 row values exceed 2 GiB",
+            (long long)sz->packed_tokens, hq);
 }
 
 void to_bf16(const void *x, unsigned short *y, long n, hipStream_t st) {
@@ -1049,7 +1061,7 @@ void bwd_impl(const seg_layout *L, const seg_sizes *sz, int hq, int hkv, float s
   }
   {
     ProfScope prof("attn_bwd_dkdv", st);
-    k_attn_bwd_dkdv<D, TO><<<xcd_grid(G, hkv), 256, 0, st>>>(
+    k_attn_bwd_dkdv<D, TO><<<xcd_grid(G, hkv), 512, 0, st>>>(
         q, k, v, dout, lse2, delta, L->seg_info, L->tile_seg, L->tok_meta, L->kt_ptr, L->kt_row,
         L->kt_cls, G, hq, hkv, L->window, scale * LOG2E, scale, P, static_cast<TO *>(dk),
         static_cast<TO *>(dv));

@@ -193,6 +193,8 @@ Plan make_plan(const seg_problem *p) {
   sz.packed_tokens = packed;
   sz.num_buffers = nbuf;
   sz.num_segments = (int32_t)segs.size();
+  sz.max_seg_len = 0;
+  for (const S0 &sg : segs) sz.max_seg_len = std::max(sz.max_seg_len, (int32_t)sg.len);
 
   // per-segment tables
   int64_t qbase = 0, tri = 0, rows = 0;

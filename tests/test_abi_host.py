@@ -39,7 +39,8 @@ def _sizes_oracle(sp, W, L, tile, cap=0, buf=0, mode="sliding"):
     return dict(num_segments=len(lay.segments), num_buffers=lay.num_buffers,
                 loss_rows=len(lay.loss_pred_row), num_qtiles=G,
                 packed_tokens=lay.packed_tokens,
-                traj_tokens=int(sp.canon_offsets()[-1]), tile_nnz_max=Z)
+                traj_tokens=int(sp.canon_offsets()[-1]), tile_nnz_max=Z,
+                max_seg_len=max((sg.length for sg in lay.segments), default=0))
 
 
 @pytest.mark.parametrize("cfg", [WL.TINY, WL.SMALL, WL.SEVEN_B, WL.STEPWISE_7B, WL.LONG],
