@@ -13,5 +13,7 @@ Modules
 layout     segmentation, packing, visibility mask, tile map, loss rows
 attention  masked GQA softmax attention forward and backward
 loss       action-token log-prob, clipped policy-ratio loss, gradients
+layer      decoder layer (RMSNorm, rotary GQA attention, SwiGLU) around the
+           segmented attention, forward and backward
 """
-from . import layout, attention, loss  # noqa: F401
+from . import layout, attention, loss, layer  # noqa: F401
