@@ -246,11 +246,77 @@ seg_status seg_logprob_loss(int32_t rows, int32_t hidden, int32_t vocab, seg_dty
                             hipStream_t stream);
 
 /*
+ * One decoder layer of the language model around the segmented attention
+ * (row f4 of the build: the policy update trains the language model on VCS
+ * segments while the vision encoder stays fixed, App. E RL stage, so the
+ * screenshot tokens enter as given hidden states).  The paper does not spell
+ * the layer out; it is the pre-norm layer of the Qwen-style backbones it
+ * trains, all matrices row-major, y = x W^T for a weight W [out, in]:
+ *   a = rms(x) * g1,  rms(x) = x / sqrt(mean(x^2) + rms_eps)
+ *   q, k, v = a wq^T, a wk^T, a wv^T       ([P, hq, d], [P, hkv, d])
+ *   q, k = rope(q), rope(k)                (rotate-half pairs (i, i + d/2) by
+ *                                           pos * rope_base^(-2i/d); pos = the
+ *                                           row inside its segment)
+ *   o = seg_attn_fwd(q, k, v)              (scale 1/sqrt(d))
+ *   y1 = x + o wo^T
+ *   b = rms(y1) * g2
+ *   y = y1 + (silu(b wg^T) * (b wu^T)) wd^T
+ * bf16 storage, fp32 accumulation.  Padding rows: their outputs are
+ * undefined and they contribute nothing to any gradient (dy there counts as
+ * zero; dx there is 0).  Projections and the MLP run over chunks of
+ * chunk_rows rows (0 = all rows at once); weight gradients are summed over
+ * the chunks in order, so results are bitwise reproducible.
+ */
+typedef struct {
+  int32_t hidden;      /* H (multiple of 8) */
+  int32_t inter;       /* I of the MLP (multiple of 8) */
+  int32_t hq, hkv, d;  /* attention heads, as for seg_attn_fwd */
+  float rms_eps;       /* > 0 */
+  float rope_base;     /* > 1 */
+  int32_t chunk_rows;  /* >= 0 */
+} seg_layer_cfg;
+typedef struct {       /* device, bf16: g1, g2 [H]; wq [hq*d, H]; wk, wv [hkv*d, H];
+                          wo [H, hq*d]; wg, wu [I, H]; wd [H, I] */
+  const void *g1, *wq, *wk, *wv, *wo, *g2, *wg, *wu, *wd;
+} seg_layer_weights;
+typedef struct {       /* device buffers written by seg_layer_fwd and read by seg_layer_bwd */
+  void *q, *k, *v;     /* [P, hq, d], [P, hkv, d] bf16, after the rotary embedding */
+  void *o;             /* [P, hq, d] bf16 (zero at padding rows) */
+  float *lse;          /* [hq, P] */
+  void *y1;            /* [P, H] bf16 */
+  float *rstd1, *rstd2; /* [P] */
+} seg_layer_saved;
+typedef struct {       /* device fp32 gradients, same shapes as the weights; overwritten */
+  float *g1, *wq, *wk, *wv, *wo, *g2, *wg, *wu, *wd;
+} seg_layer_grads;
+
+/* Workspace of seg_layer_fwd (bwd = 0) or seg_layer_bwd (bwd = 1). */
+size_t seg_layer_workspace_bytes(const seg_sizes *sz, const seg_layer_cfg *cfg, int32_t bwd);
+
+/* Layer forward: x [P, H] bf16 -> y [P, H] bf16 and the saved buffers.
+ * Errors: SEG_ERR_ARG (null pointer, bad setting), SEG_ERR_UNSUPPORTED
+ * (shape the attention or GEMM kernels do not take), SEG_ERR_WORKSPACE. */
+seg_status seg_layer_fwd(const seg_layout *L, const seg_sizes *sz, const seg_layer_cfg *cfg,
+                         const seg_layer_weights *w, const void *x, void *y,
+                         const seg_layer_saved *saved, void *ws, size_t ws_bytes,
+                         hipStream_t stream);
+
+/* Layer backward: gradients of sum(y * dy) over the segment rows, given the
+ * saved buffers of seg_layer_fwd on the same x and weights.  dx [P, H] bf16;
+ * the weight gradients are written in fp32.  The MLP activations and the
+ * normalised inputs are recomputed from x, y1 and the saved rstd values. */
+seg_status seg_layer_bwd(const seg_layout *L, const seg_sizes *sz, const seg_layer_cfg *cfg,
+                         const seg_layer_weights *w, const void *x, const seg_layer_saved *saved,
+                         const void *dy, void *dx, const seg_layer_grads *g, void *ws,
+                         size_t ws_bytes, hipStream_t stream);
+
+/*
  * Kernel timing.  While enabled, every kernel the library launches is
  * bracketed by HIP events recorded on its launch stream.  seg_profile_read sums
  * the device time of all recorded launches of one kernel (names: "layout",
  * "attn_prep", "attn_fwd", "attn_delta", "attn_bwd_dkdv", "attn_bwd_dq",
- * "logits", "row_loss", "dz", "lp_prep", "dh", "dw"), waiting for them to
+ * "logits", "row_loss", "dz", "lp_prep", "dh", "dw", and for the layer
+ * "ly_norm", "ly_rope", "ly_proj", "ly_mlp", "ly_wgrad", "ly_misc"), waiting for them to
  * finish; seg_profile_reset forgets the records.  Timing adds two event
  * records per launch and is off by default.
  */

@@ -21,7 +21,8 @@ SEG_BF16, SEG_F32 = 0, 1
 
 # every symbol include/seg.h declares
 EXPORTS = ["seg_layout_query", "seg_build_layout", "seg_attn_workspace_bytes", "seg_attn_fwd",
-           "seg_attn_bwd", "seg_logprob_workspace_bytes", "seg_logprob_loss", "seg_profile_enable",
+           "seg_attn_bwd", "seg_logprob_workspace_bytes", "seg_logprob_loss",
+           "seg_layer_workspace_bytes", "seg_layer_fwd", "seg_layer_bwd", "seg_profile_enable",
            "seg_profile_reset", "seg_profile_read", "seg_last_error"]
 
 P32 = ctypes.POINTER(ctypes.c_int32)
@@ -64,6 +65,28 @@ class SegLossCfg(ctypes.Structure):
                 ("dual_clip_c", ctypes.c_float), ("loss_scale", ctypes.c_float),
                 ("logit_scale", ctypes.c_float), ("want_grad", ctypes.c_int32),
                 ("kl_coef", ctypes.c_float)]
+
+
+class SegLayerCfg(ctypes.Structure):
+    _fields_ = [("hidden", ctypes.c_int32), ("inter", ctypes.c_int32), ("hq", ctypes.c_int32),
+                ("hkv", ctypes.c_int32), ("d", ctypes.c_int32), ("rms_eps", ctypes.c_float),
+                ("rope_base", ctypes.c_float), ("chunk_rows", ctypes.c_int32)]
+
+
+LAYER_WEIGHTS = ("g1", "wq", "wk", "wv", "wo", "g2", "wg", "wu", "wd")
+
+
+class SegLayerWeights(ctypes.Structure):
+    _fields_ = [(n, VP) for n in LAYER_WEIGHTS]
+
+
+class SegLayerSaved(ctypes.Structure):
+    _fields_ = [("q", VP), ("k", VP), ("v", VP), ("o", VP), ("lse", VP), ("y1", VP),
+                ("rstd1", VP), ("rstd2", VP)]
+
+
+class SegLayerGrads(ctypes.Structure):
+    _fields_ = [(n, VP) for n in LAYER_WEIGHTS]
 
 
 class SegError(RuntimeError):
@@ -113,6 +136,18 @@ def lib() -> ctypes.CDLL:
                                        VP, VP, VP, VP, VP, VP, VP, VP, ctypes.c_int32,
                                        ctypes.POINTER(SegLossCfg), VP, VP, VP, VP, VP, VP, VP, VP,
                                        ctypes.c_size_t, VP]
+        L.seg_layer_workspace_bytes.restype = ctypes.c_size_t
+        L.seg_layer_workspace_bytes.argtypes = [ctypes.POINTER(SegSizes), ctypes.POINTER(SegLayerCfg),
+                                                ctypes.c_int32]
+        L.seg_layer_fwd.restype = ctypes.c_int
+        L.seg_layer_fwd.argtypes = [ctypes.POINTER(SegLayout), ctypes.POINTER(SegSizes),
+                                    ctypes.POINTER(SegLayerCfg), ctypes.POINTER(SegLayerWeights),
+                                    VP, VP, ctypes.POINTER(SegLayerSaved), VP, ctypes.c_size_t, VP]
+        L.seg_layer_bwd.restype = ctypes.c_int
+        L.seg_layer_bwd.argtypes = [ctypes.POINTER(SegLayout), ctypes.POINTER(SegSizes),
+                                    ctypes.POINTER(SegLayerCfg), ctypes.POINTER(SegLayerWeights),
+                                    VP, ctypes.POINTER(SegLayerSaved), VP, VP,
+                                    ctypes.POINTER(SegLayerGrads), VP, ctypes.c_size_t, VP]
         L.seg_profile_enable.restype = None
         L.seg_profile_enable.argtypes = [ctypes.c_int32]
         L.seg_profile_reset.restype = None

@@ -11,7 +11,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libseg.so")
-SOURCES = ["seg_layout.hip", "seg_attn.hip", "seg_logprob.hip", "seg_profile.hip"]
+SOURCES = ["seg_layout.hip", "seg_attn.hip", "seg_logprob.hip", "seg_layer.hip",
+           "seg_profile.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -11,23 +11,27 @@
 //   3. dz = g * (onehot(target) - softmax(z)) as bf16, written in both
 //      orientations (one pass over zT);
 //   4. dH = s * dz W and dW = s * dz^T h (MFMA).
-// All GEMMs use one "NT" kernel: C[m][n] = sum_k A[m][k] B[n][k] with both
-// operands k-contiguous, 128x128 block tiles, 4 waves of 64x64.
+// All GEMMs use the shared "NT" kernel of gemm.h: C[m][n] = sum_k A[m][k] B[n][k]
+// with both operands k-contiguous.
 #include <climits>
 #include <cmath>
 
 #include "common.h"
+#include "gemm.h"
 
 namespace seg {
 namespace {
 
-constexpr int BM = 128, BN = 128, BK = 32;
+using gemm::BM;
+using gemm::BN;
+using gemm::EpiStore;
+using gemm::k_gemm_nt;
+using gemm::k_transpose2d;
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
 
-__device__ __forceinline__ bf16x8 as_bf8(const u16x8 &v) { return __builtin_bit_cast(bf16x8, v); }
-
-// Epilogue of the logits GEMM (M = vocab, N = rows).
+// Epilogue of the logits GEMM (M = vocab, N = rows): writes zT, captures the
+// target logit and the per-(row, vocab tile) max / sum-exp partials.
 struct EpiLogits {
   float *zt;        // [M][ldz] fp32
   long ldz;
@@ -36,116 +40,25 @@ struct EpiLogits {
   const int32_t *target;  // [N]
   float *ztgt;      // [N]
   float scale;
-};
-
-// Epilogue writing C (times scale) as dtype TO with leading dimension ldc.
-template <class TO>
-struct EpiStore {
-  TO *c;
-  long ldc;
-  float scale;
-};
-
-template <class Epi>
-__device__ __forceinline__ void epilogue(const Epi &, const f32x16 (&)[2][2], int, int, int, int,
-                                         int, int, int, int);
-
-template <class TO>
-__device__ __forceinline__ void epilogue_store(const EpiStore<TO> &ep, const f32x16 (&acc)[2][2],
-                                               int m0, int n0, int M, int N, int wm, int wn,
-                                               int col, int hh) {
-#pragma unroll
-  for (int bm = 0; bm < 2; ++bm)
+  __device__ __forceinline__ void operator()(const f32x16 (&acc)[2][2], const gemm::Tile &t) const {
+    __shared__ float2 sStat[2][BN];
+    const int tid = threadIdx.x;
+    // accumulator lane holds one row n
 #pragma unroll
     for (int bn = 0; bn < 2; ++bn) {
-      const int n = n0 + wn * 64 + bn * 32 + col;
-      if (n >= N) continue;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int m = m0 + wm * 64 + bm * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-        if (m < M) store_val(ep.c, (long)m * ep.ldc + n, acc[bm][bn][r] * ep.scale);
-      }
-    }
-}
-
-// C[m][n] = sum_k A[m][k] * B[n][k]; K % 32 == 0 is not required but
-// lda/ldb/K must be multiples of 8 (16-byte chunks).  Rows beyond M / N and
-// chunks beyond K are read as zero.
-template <int EPI, class Epi>
-__global__ void __launch_bounds__(256, 2) k_gemm_nt(const unsigned short *__restrict__ A, long lda,
-                                                    const unsigned short *__restrict__ B, long ldb,
-                                                    int M, int N, int K, Epi ep) {
-  __shared__ unsigned short sA[2][BM * BK];
-  __shared__ unsigned short sB[2][BN * BK];
-  __shared__ float2 sStat[2][BN];
-  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int wm = wave >> 1, wn = wave & 1, col = lane & 31, hh = lane >> 5;
-
-  f32x16 acc[2][2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
-
-  auto load = [&](int kt, int buf) {
-#pragma unroll
-    for (int it = 0; it < 2; ++it) {
-      const int c = tid + it * 256;
-      const int row = c >> 2, ch = c & 3;
-      const int gk = kt * BK + ch * 8;
-      const int sw = (ch ^ ((row >> 2) & 3)) * 8;
-      u16x8 va = {0, 0, 0, 0, 0, 0, 0, 0}, vb = va;
-      if (m0 + row < M && gk < K) va = *reinterpret_cast<const u16x8 *>(A + (long)(m0 + row) * lda + gk);
-      if (n0 + row < N && gk < K) vb = *reinterpret_cast<const u16x8 *>(B + (long)(n0 + row) * ldb + gk);
-      *reinterpret_cast<u16x8 *>(&sA[buf][row * BK + sw]) = va;
-      *reinterpret_cast<u16x8 *>(&sB[buf][row * BK + sw]) = vb;
-    }
-  };
-
-  const int nk = (K + BK - 1) / BK;
-  load(0, 0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) load(kt + 1, buf ^ 1);
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      const int ch = kk * 2 + hh;
-      bf16x8 a[2], b[2];
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int ra = wm * 64 + i * 32 + col;
-        const int rb = wn * 64 + i * 32 + col;
-        a[i] = *reinterpret_cast<const bf16x8 *>(&sA[buf][ra * BK + ((ch ^ ((ra >> 2) & 3)) * 8)]);
-        b[i] = *reinterpret_cast<const bf16x8 *>(&sB[buf][rb * BK + ((ch ^ ((rb >> 2) & 3)) * 8)]);
-      }
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = mfma32(a[i], b[j], acc[i][j]);
-    }
-    __syncthreads();
-  }
-
-  if constexpr (EPI == 0) {
-    // logits: C[m = vocab][n = row]; accumulator lane holds one row n
-    const EpiLogits &e = ep;
-#pragma unroll
-    for (int bn = 0; bn < 2; ++bn) {
-      const int n = n0 + wn * 64 + bn * 32 + col;
-      const bool nok = n < N;
-      const int tgt = nok ? e.target[n] : -1;
+      const int n = t.column(bn);
+      const bool nok = n < t.N;
+      const int tgt = nok ? target[n] : -1;
       float mx = -INFINITY;
 #pragma unroll
       for (int bm = 0; bm < 2; ++bm)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int m = m0 + wm * 64 + bm * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-          const float z = acc[bm][bn][r] * e.scale;
-          if (nok && m < M) {
-            e.zt[(long)m * e.ldz + n] = z;
-            if (m == tgt) e.ztgt[n] = z;
+          const int m = t.row(bm, r);
+          const float z = acc[bm][bn][r] * scale;
+          if (nok && m < t.M) {
+            zt[(long)m * ldz + n] = z;
+            if (m == tgt) ztgt[n] = z;
             mx = fmaxf(mx, z * LOG2E);
           }
         }
@@ -156,15 +69,15 @@ __global__ void __launch_bounds__(256, 2) k_gemm_nt(const unsigned short *__rest
         for (int bm = 0; bm < 2; ++bm)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const int m = m0 + wm * 64 + bm * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-            if (m < M) sm += exp2f(acc[bm][bn][r] * e.scale * LOG2E - mx);
+            const int m = t.row(bm, r);
+            if (m < t.M) sm += exp2f(acc[bm][bn][r] * scale * LOG2E - mx);
           }
       }
       sm += __shfl_xor(sm, 32, 64);
-      if (hh == 0) sStat[wm][wn * 64 + bn * 32 + col] = make_float2(mx, sm);
+      if (t.hh == 0) sStat[t.wm][t.wn * 64 + bn * 32 + t.col] = make_float2(mx, sm);
     }
     __syncthreads();
-    if (tid < BN && n0 + tid < N) {
+    if (tid < BN && t.n0 + tid < t.N) {
       const float2 a = sStat[0][tid], b = sStat[1][tid];
       const float mx = fmaxf(a.x, b.x);
       float sm = 0.f;
@@ -172,14 +85,11 @@ __global__ void __launch_bounds__(256, 2) k_gemm_nt(const unsigned short *__rest
         if (a.x != -INFINITY) sm += a.y * exp2f(a.x - mx);
         if (b.x != -INFINITY) sm += b.y * exp2f(b.x - mx);
       }
-      e.stats[(long)blockIdx.y * e.nrows + n0 + tid] = make_float2(mx, sm);
+      stats[(long)blockIdx.y * nrows + t.n0 + tid] = make_float2(mx, sm);
     }
-  } else {
-    epilogue_store(ep, acc, m0, n0, M, N, wm, wn, col, hh);
   }
-}
+};
 
-// Per row: LSE over the vocab-tile partials (fixed order), then the loss.
 __global__ void __launch_bounds__(256) k_row_loss(
     const float2 *__restrict__ stats, int ntiles, int rows, const float *__restrict__ ztgt,
     const float *__restrict__ old_logp, const float *__restrict__ ref_logp,
@@ -298,33 +208,6 @@ __global__ void __launch_bounds__(256) k_dz(const float *__restrict__ zt, long l
   }
 }
 
-// y[c][r] = x[r][c] for a [rows][cols] matrix (ldx), output [cols][ldy]; x is
-// bf16 bits or fp32 (rounded); optional row gather; zero for r >= rows up to
-// pad_rows.
-template <class TI>
-__global__ void __launch_bounds__(256) k_transpose2d(const TI *__restrict__ x, long ldx,
-                                                     const int32_t *__restrict__ rowmap, int rows,
-                                                     int cols, int pad_rows,
-                                                     unsigned short *__restrict__ y, long ldy) {
-  __shared__ unsigned short t[64][66];
-  const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  for (int i = ty; i < 64; i += 4) {
-    const int r = r0 + i, c = c0 + tx;
-    unsigned short b = 0;
-    if (r < rows && c < cols) {
-      const long sr = rowmap ? rowmap[r] : r;
-      b = load_bf(x, sr * ldx + c);
-    }
-    t[i][tx] = b;
-  }
-  __syncthreads();
-  for (int i = ty; i < 64; i += 4) {
-    const int c = c0 + i, r = r0 + tx;
-    if (c < cols && r < pad_rows) y[(long)c * ldy + r] = t[tx][i];
-  }
-}
-
 // y[r][:] = x[rowmap[r]][:] as bf16 (rows < rows_pad are zero beyond rows).
 template <class TI>
 __global__ void k_gather_rows(const TI *__restrict__ x, long ldx, const int32_t *__restrict__ rowmap,
@@ -420,7 +303,7 @@ void logprob_impl(int rows, int H, int V, const TI *h, const int32_t *row_index,
     EpiLogits e{zt, Rp, stats, rows, target, ztgt, cfg.logit_scale};
     dim3 grid((rows + BN - 1) / BN, (V + BM - 1) / BM);
     ProfScope prof("logits", st);
-    k_gemm_nt<0, EpiLogits><<<grid, 256, 0, st>>>(wb, H, hb, H, V, rows, H, e);
+    k_gemm_nt<EpiLogits><<<grid, 256, 0, st>>>(wb, H, hb, H, V, rows, H, e);
     SEG_LAUNCH_CHECK();
   }
   // 2. per-row loss
@@ -452,7 +335,7 @@ void logprob_impl(int rows, int H, int V, const TI *h, const int32_t *row_index,
     EpiStore<TO> e{static_cast<TO *>(dh), H, cfg.logit_scale};
     dim3 grid((H + BN - 1) / BN, (rows + BM - 1) / BM);
     ProfScope prof("dh", st);
-    k_gemm_nt<1, EpiStore<TO>><<<grid, 256, 0, st>>>(dz, Vp, wt, Vp, rows, H, Vp, e);
+    k_gemm_nt<EpiStore<TO>><<<grid, 256, 0, st>>>(dz, Vp, wt, Vp, rows, H, Vp, e);
     SEG_LAUNCH_CHECK();
   }
   //    dW = s * dz^T h  (M = V, N = H, K = Rp)
@@ -460,7 +343,7 @@ void logprob_impl(int rows, int H, int V, const TI *h, const int32_t *row_index,
     EpiStore<float> e{dw, H, cfg.logit_scale};
     dim3 grid((H + BN - 1) / BN, (V + BM - 1) / BM);
     ProfScope prof("dw", st);
-    k_gemm_nt<1, EpiStore<float>><<<grid, 256, 0, st>>>(dzt, Rp, ht, Rp, V, H, Rp, e);
+    k_gemm_nt<EpiStore<float>><<<grid, 256, 0, st>>>(dzt, Rp, ht, Rp, V, H, Rp, e);
     SEG_LAUNCH_CHECK();
   }
 }

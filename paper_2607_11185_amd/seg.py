@@ -1,7 +1,8 @@
 """Python binding of the libseg entry points, on PyTorch device tensors.
 
 Functions carry the C names (seg_layout_query, seg_build_layout, seg_attn_fwd,
-seg_attn_bwd, seg_logprob_loss) and only marshal arguments: they allocate
+seg_attn_bwd, seg_logprob_loss, seg_layer_fwd, seg_layer_bwd) and only marshal
+arguments: they allocate
 outputs and workspace with torch on the tensors' device and pass raw
 pointers plus torch's current stream to the library.
 """
@@ -260,3 +261,82 @@ def seg_logprob_loss(h, row_index, w, target, old_logp, adv, row_traj, cfg: Loss
         out["loss_sum"].data_ptr(), _ptr(out["dh"]), _ptr(out["dw"]), ws.data_ptr(), ws.numel(),
         _stream(dev)))
     return out
+
+
+@dataclasses.dataclass
+class LayerCfg:
+    """Shape and settings of the decoder layer (seg_layer_cfg)."""
+    hidden: int
+    inter: int
+    hq: int
+    hkv: int
+    d: int
+    rms_eps: float = 1e-6
+    rope_base: float = 1e6
+    chunk_rows: int = 0
+
+    def c(self) -> "_lib.SegLayerCfg":
+        return _lib.SegLayerCfg(self.hidden, self.inter, self.hq, self.hkv, self.d, self.rms_eps,
+                                self.rope_base, self.chunk_rows)
+
+
+def layer_workspace(lay: Layout, cfg: LayerCfg, bwd: bool):
+    import torch
+    n = _lib.lib().seg_layer_workspace_bytes(ctypes.byref(lay.sizes), ctypes.byref(cfg.c()),
+                                             int(bwd))
+    return torch.empty(max(n, 1), dtype=torch.uint8, device=lay.device)
+
+
+def _layer_weights(w: dict):
+    return _lib.SegLayerWeights(*[w[n].data_ptr() for n in _lib.LAYER_WEIGHTS])
+
+
+def seg_layer_fwd(lay: Layout, cfg: LayerCfg, w: dict, x, y=None, saved=None, ws=None):
+    """Decoder-layer forward over the packed rows; x [P, H] bf16, w: the bf16
+    weights by name (g1, wq, wk, wv, wo, g2, wg, wu, wd).  Returns (y, saved)."""
+    import torch
+    P, H = x.shape
+    dev = x.device
+    assert x.dtype == torch.bfloat16 and x.is_contiguous()
+    for n in _lib.LAYER_WEIGHTS:
+        assert w[n].dtype == torch.bfloat16 and w[n].is_contiguous(), n
+    if y is None:
+        y = torch.empty_like(x)
+    if saved is None:
+        bf = dict(dtype=torch.bfloat16, device=dev)
+        saved = {"q": torch.empty((P, cfg.hq, cfg.d), **bf), "k": torch.empty((P, cfg.hkv, cfg.d), **bf),
+                 "v": torch.empty((P, cfg.hkv, cfg.d), **bf), "o": torch.empty((P, cfg.hq, cfg.d), **bf),
+                 "lse": torch.empty((cfg.hq, P), dtype=torch.float32, device=dev),
+                 "y1": torch.empty((P, H), **bf),
+                 "rstd1": torch.empty(P, dtype=torch.float32, device=dev),
+                 "rstd2": torch.empty(P, dtype=torch.float32, device=dev)}
+    sv = _lib.SegLayerSaved(*[saved[n].data_ptr() for n in ("q", "k", "v", "o", "lse", "y1", "rstd1",
+                                                             "rstd2")])
+    if ws is None:
+        ws = layer_workspace(lay, cfg, False)
+    check(_lib.lib().seg_layer_fwd(ctypes.byref(lay.c), ctypes.byref(lay.sizes), ctypes.byref(cfg.c()),
+                                   ctypes.byref(_layer_weights(w)), x.data_ptr(), y.data_ptr(),
+                                   ctypes.byref(sv), ws.data_ptr(), ws.numel(), _stream(dev)))
+    return y, saved
+
+
+def seg_layer_bwd(lay: Layout, cfg: LayerCfg, w: dict, x, saved: dict, dy, dx=None, grads=None,
+                  ws=None):
+    """Decoder-layer backward: returns (dx, grads) with fp32 weight gradients by name."""
+    import torch
+    dev = x.device
+    assert dy.dtype == torch.bfloat16 and dy.is_contiguous() and dy.shape == x.shape
+    if dx is None:
+        dx = torch.empty_like(x)
+    if grads is None:
+        grads = {n: torch.empty(w[n].shape, dtype=torch.float32, device=dev) for n in _lib.LAYER_WEIGHTS}
+    sv = _lib.SegLayerSaved(*[saved[n].data_ptr() for n in ("q", "k", "v", "o", "lse", "y1", "rstd1",
+                                                             "rstd2")])
+    g = _lib.SegLayerGrads(*[grads[n].data_ptr() for n in _lib.LAYER_WEIGHTS])
+    if ws is None:
+        ws = layer_workspace(lay, cfg, True)
+    check(_lib.lib().seg_layer_bwd(ctypes.byref(lay.c), ctypes.byref(lay.sizes), ctypes.byref(cfg.c()),
+                                   ctypes.byref(_layer_weights(w)), x.data_ptr(), ctypes.byref(sv),
+                                   dy.data_ptr(), dx.data_ptr(), ctypes.byref(g), ws.data_ptr(),
+                                   ws.numel(), _stream(dev)))
+    return dx, grads

@@ -433,3 +433,59 @@ class Inputs:
     def tgt_torch(self, device="cuda"):
         return uniform_int_torch(self.seed, STREAM["tgt"], 0, self.n_canon, self.cfg.vocab,
                                  device)
+
+
+# ----------------------------------------------------------------------------
+# decoder-layer tensors (random-init weights of a Qwen-style layer)
+
+LAYER_STREAM = {"x": 10, "dy": 11, "g1": 12, "wq": 13, "wk": 14, "wv": 15, "wo": 16, "g2": 17,
+                "wg": 18, "wu": 19, "wd": 20}
+LAYER_WEIGHTS = ("g1", "wq", "wk", "wv", "wo", "g2", "wg", "wu", "wd")
+
+
+def layer_shapes(H, I, hq, hkv, d) -> dict:
+    return {"g1": (H,), "wq": (hq * d, H), "wk": (hkv * d, H), "wv": (hkv * d, H),
+            "wo": (H, hq * d), "g2": (H,), "wg": (I, H), "wu": (I, H), "wd": (H, I)}
+
+
+def _gain_bits(seed, name, n):
+    """Norm gains 1 + 0.1 z, rounded to float32 and then to bf16 (bits)."""
+    z = normal_np(seed, LAYER_STREAM[name], np.arange(n), 1.0, "f32")
+    return bf16_round_np((1.0 + 0.1 * z).astype(np.float32))
+
+
+def layer_weights_np(seed, H, I, hq, hkv, d) -> dict:
+    """bf16 layer weights as float64 values: gains 1 + 0.1 z, projections
+    z / sqrt(fan_in)."""
+    out = {}
+    for n, shp in layer_shapes(H, I, hq, hkv, d).items():
+        if len(shp) == 1:
+            out[n] = bf16_bits_to_f64(_gain_bits(seed, n, shp[0]))
+        else:
+            out[n] = normal_np(seed, LAYER_STREAM[n], np.arange(shp[0] * shp[1]),
+                               1.0 / math.sqrt(shp[1])).reshape(shp)
+    return out
+
+
+def layer_weights_torch(seed, H, I, hq, hkv, d, device="cuda") -> dict:
+    """The same weights as layer_weights_np, as bf16 device tensors."""
+    import torch
+    out = {}
+    for n, shp in layer_shapes(H, I, hq, hkv, d).items():
+        if len(shp) == 1:
+            bits = _gain_bits(seed, n, shp[0]).astype(np.int16)
+            out[n] = torch.from_numpy(bits).view(torch.bfloat16).to(device)
+        else:
+            out[n] = normal_torch(seed, LAYER_STREAM[n], 0, shp[0] * shp[1],
+                                  1.0 / math.sqrt(shp[1]), "bf16", device).view(*shp)
+    return out
+
+
+def layer_rows_np(seed, name, rows, width) -> np.ndarray:
+    """Rows of a [*, width] standard-normal bf16 tensor ("x" or "dy")."""
+    return normal_rows_np(seed, LAYER_STREAM[name], rows, width, 1.0, "bf16")
+
+
+def layer_rows_torch(seed, name, n_rows, width, device="cuda"):
+    return normal_torch(seed, LAYER_STREAM[name], 0, n_rows * width, 1.0, "bf16",
+                        device).view(n_rows, width)

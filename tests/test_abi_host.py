@@ -195,3 +195,51 @@ def test_query_anchored_matches_oracle():
         want = _sizes_oracle(sp, K, D, tile, mode="anchored")
         for k, v in want.items():
             assert got[k] == v, (it, k, got[k], v)
+
+
+def test_layer_sizing_and_argument_checks():
+    """Layer workspace sizing and argument rejection, before any launch."""
+    L = _lib_or_skip()
+    pr = _prob()
+    sz = S.seg_layout_query(pr)
+    lay = _lib.SegLayout()
+    lay.tile, lay.window = 128, 2
+    cfg = S.LayerCfg(256, 512, 4, 2, 64)
+    f = L.seg_layer_workspace_bytes(ctypes.byref(sz), ctypes.byref(cfg.c()), 0)
+    b = L.seg_layer_workspace_bytes(ctypes.byref(sz), ctypes.byref(cfg.c()), 1)
+    assert 0 < f < b
+    # smaller row chunks need less workspace
+    assert sz.packed_tokens >= 8
+    c2 = S.LayerCfg(256, 512, 4, 2, 64, chunk_rows=sz.packed_tokens // 4)
+    assert L.seg_layer_workspace_bytes(ctypes.byref(sz), ctypes.byref(c2.c()), 1) < b
+    assert L.seg_layer_workspace_bytes(ctypes.byref(sz), ctypes.byref(S.LayerCfg(0, 8, 1, 1, 64).c()),
+                                       0) == 0
+    w = _lib.SegLayerWeights(*([1] * 9))
+    sv = _lib.SegLayerSaved(*([1] * 8))
+    g = _lib.SegLayerGrads(*([1] * 9))
+    bad = [(S.LayerCfg(250, 512, 4, 2, 64), _lib.SEG_ERR_UNSUPPORTED),     # hidden % 8
+           (S.LayerCfg(256, 500, 4, 2, 64), _lib.SEG_ERR_UNSUPPORTED),     # inter % 8
+           (S.LayerCfg(16384, 512, 4, 2, 64), _lib.SEG_ERR_UNSUPPORTED),   # hidden too wide
+           (S.LayerCfg(256, 512, 4, 3, 64), _lib.SEG_ERR_UNSUPPORTED),     # hq % hkv
+           (S.LayerCfg(256, 512, 4, 2, 96), _lib.SEG_ERR_UNSUPPORTED),     # head_dim
+           (S.LayerCfg(256, 512, 4, 2, 64, rms_eps=0.0), _lib.SEG_ERR_ARG),
+           (S.LayerCfg(256, 512, 4, 2, 64, rope_base=1.0), _lib.SEG_ERR_ARG),
+           (S.LayerCfg(256, 512, 4, 2, 64, chunk_rows=-1), _lib.SEG_ERR_ARG)]
+    for c, want in bad:
+        st = L.seg_layer_fwd(ctypes.byref(lay), ctypes.byref(sz), ctypes.byref(c.c()), ctypes.byref(w),
+                             1, 1, ctypes.byref(sv), 1, 1 << 40, None)
+        assert st == want, (c, st)
+        st = L.seg_layer_bwd(ctypes.byref(lay), ctypes.byref(sz), ctypes.byref(c.c()), ctypes.byref(w),
+                             1, ctypes.byref(sv), 1, 1, ctypes.byref(g), 1, 1 << 40, None)
+        assert st == want, (c, st)
+    # workspace too small, then a NULL weight
+    st = L.seg_layer_fwd(ctypes.byref(lay), ctypes.byref(sz), ctypes.byref(cfg.c()), ctypes.byref(w),
+                         1, 1, ctypes.byref(sv), 1, f - 1, None)
+    assert st == _lib.SEG_ERR_WORKSPACE
+    st = L.seg_layer_bwd(ctypes.byref(lay), ctypes.byref(sz), ctypes.byref(cfg.c()), ctypes.byref(w),
+                         1, ctypes.byref(sv), 1, 1, ctypes.byref(g), 1, b - 1, None)
+    assert st == _lib.SEG_ERR_WORKSPACE
+    w.wd = None
+    st = L.seg_layer_fwd(ctypes.byref(lay), ctypes.byref(sz), ctypes.byref(cfg.c()), ctypes.byref(w),
+                         1, 1, ctypes.byref(sv), 1, f, None)
+    assert st == _lib.SEG_ERR_ARG and b"NULL" in L.seg_last_error()

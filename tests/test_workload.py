@@ -38,3 +38,17 @@ def test_spans_of_configs():
     lg = WL.make_spans(WL.LONG)
     T = np.diff(lg.step_offsets)
     assert T.min() >= 10 and T.max() <= 50
+
+
+def test_layer_generators_host_and_device_identical():
+    a = WL.layer_weights_np(3, 40, 24, 2, 1, 64)
+    b = WL.layer_weights_torch(3, 40, 24, 2, 1, 64, device="cpu")
+    for n, shp in WL.layer_shapes(40, 24, 2, 1, 64).items():
+        assert a[n].shape == shp and tuple(b[n].shape) == shp
+        assert np.array_equal(a[n], b[n].to(torch.float64).numpy()), n
+    # projections have unit-variance rows after the 1/sqrt(fan_in) scale
+    assert abs(a["wg"].std() * np.sqrt(40) - 1.0) < 0.1
+    assert abs(a["g1"].mean() - 1.0) < 0.1
+    x = WL.layer_rows_np(3, "x", np.array([4, 0, 6]), 40)
+    xt = WL.layer_rows_torch(3, "x", 7, 40, device="cpu")
+    assert np.array_equal(x, xt.to(torch.float64).numpy()[[4, 0, 6]])
