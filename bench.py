@@ -341,6 +341,184 @@ def pmc_driver(cfg_name):
                                       "launches": 3}}), flush=True)
 
 
+LAYER_INTER = 18944   # MLP width of the 7B-class backbone (Qwen2-7B shape)
+LAYER_GROUPS = 4      # trajectory groups (micro-batches) per layer step
+LAYER_SCOPES = ["layout", "ly_norm", "ly_rope", "ly_proj", "ly_mlp", "ly_wgrad", "ly_misc",
+                "attn_prep", "attn_fwd", "attn_delta", "attn_bwd_dkdv", "attn_bwd_dq"]
+
+
+class LayerRun:
+    """One decoder layer (projections, RoPE, segmented attention, SwiGLU MLP)
+    over the batch, forward and backward, in trajectory groups: each group is
+    packed and run on its own (a micro-batch), all groups' inputs resident."""
+
+    def __init__(self, cfg, dev, inter, groups):
+        import numpy as np
+        import torch
+
+        from paper_2607_11185_amd import seg as S
+        from paper_2607_11185_amd import workload as WL
+        self.S, self.cfg, self.dev = S, cfg, dev
+        H, d = cfg.hidden, cfg.head_dim
+        self.lc = S.LayerCfg(H, inter, cfg.hq, cfg.hkv, d, 1e-6, 1e6, 16384)
+        spans = WL.make_spans(cfg)
+        bounds = np.linspace(0, spans.num_traj, groups + 1).round().astype(int)
+        self.w = WL.layer_weights_torch(cfg.seed, H, inter, cfg.hq, cfg.hkv, d, dev)
+        n_canon = int(spans.canon_offsets()[-1])
+        xc = WL.layer_rows_torch(cfg.seed, "x", n_canon, H, dev)
+        coff = spans.canon_offsets()
+        self.groups = []
+        self.P = self.pairs = self.traj_tokens = 0
+        for t0, t1 in zip(bounds[:-1], bounds[1:]):
+            sub = spans.subset(int(t0), int(t1))
+            prob = S.Problem.from_spans(sub, cfg.window, cfg.seg_steps, cfg.max_seg_tokens,
+                                        cfg.buffer_tokens, 128, cfg.mode)
+            sz = S.seg_layout_query(prob)
+            lay = S.seg_build_layout(prob, sz, dev)
+            host = lay.host()
+            src = host["tok_src"].astype(np.int64)
+            src = np.where(src >= 0, src + int(coff[t0]), 0)
+            x = xc[torch.from_numpy(src).to(dev)].contiguous()
+            P = sz.packed_tokens
+            dy = WL.layer_rows_torch(cfg.seed + 1 + len(self.groups), "dy", P, H, dev)
+            self.groups.append({"prob": prob, "lay": lay, "x": x, "dy": dy, "P": P})
+            self.P += P
+            self.pairs += int(host["seg_pairs"].sum())
+            self.traj_tokens += sz.traj_tokens
+        del xc
+        torch.cuda.empty_cache()
+        # outputs, saved activations and workspaces sized for the largest group
+        big = max(self.groups, key=lambda g: g["P"])
+        self.y, self.saved = S.seg_layer_fwd(big["lay"], self.lc, self.w, big["x"])
+        self.dx, self.grads = S.seg_layer_bwd(big["lay"], self.lc, self.w, big["x"], self.saved,
+                                              big["dy"])
+        self.ws = S.layer_workspace(big["lay"], self.lc, True)
+        torch.cuda.synchronize()
+        log(f"[layer {cfg.name}] groups={len(self.groups)} packed={self.P} "
+            f"(largest {big['P']}) pairs/head={self.pairs} inter={inter}")
+
+    def _views(self, P):
+        H, c = self.cfg.hidden, self.cfg
+        sv = {"q": self.saved["q"][:P], "k": self.saved["k"][:P], "v": self.saved["v"][:P],
+              "o": self.saved["o"][:P], "lse": self.saved["lse"].view(-1)[:c.hq * P].view(c.hq, P),
+              "y1": self.saved["y1"][:P], "rstd1": self.saved["rstd1"][:P],
+              "rstd2": self.saved["rstd2"][:P]}
+        return self.y[:P], sv, self.dx[:P]
+
+    def step(self, ev=None):
+        S = self.S
+        rec = (lambda name: ev[name].record()) if ev is not None else (lambda name: None)
+        for gi, g in enumerate(self.groups):
+            rec(f"l{gi}")
+            sz = S.seg_layout_query(g["prob"])
+            S.seg_build_layout(g["prob"], sz, self.dev, out=g["lay"])
+            y, sv, dx = self._views(g["P"])
+            rec(f"f{gi}")
+            S.seg_layer_fwd(g["lay"], self.lc, self.w, g["x"], y=y, saved=sv, ws=self.ws)
+            rec(f"b{gi}")
+            S.seg_layer_bwd(g["lay"], self.lc, self.w, g["x"], sv, g["dy"], dx=dx, grads=self.grads,
+                            ws=self.ws)
+        rec("end")
+
+    def gemm_flop(self):
+        """Algorithmic GEMM FLOP of the step: forward projections and MLP, and
+        twice that for the backward (data and weight gradients)."""
+        c, I = self.cfg, self.lc.inter
+        H, QD, KD = c.hidden, c.hq * c.head_dim, c.hkv * c.head_dim
+        fwd = 2.0 * self.P * H * (QD + 2 * KD) + 2.0 * self.P * QD * H + 6.0 * self.P * H * I
+        return 3.0 * fwd
+
+    def attn_flop(self):
+        c = self.cfg
+        return 12.0 * c.head_dim * self.pairs * c.hq
+
+    def free(self):
+        for k in list(self.__dict__):
+            if k not in ("cfg", "P", "pairs", "traj_tokens", "lc", "S", "dev"):
+                delattr(self, k)
+
+
+def time_layer(run, steps, warmup):
+    import ctypes
+
+    import torch
+
+    from paper_2607_11185_amd import _lib
+    L = _lib.lib()
+    for _ in range(warmup):
+        run.step()
+    torch.cuda.synchronize()
+    G = len(run.groups)
+    names = [f"{p}{i}" for i in range(G) for p in "lfb"] + ["end"]
+    evs = [{n: torch.cuda.Event(enable_timing=True) for n in names} for _ in range(steps)]
+    L.seg_profile_reset()
+    L.seg_profile_enable(1)
+    torch.cuda.synchronize()
+    for i in range(steps):
+        run.step(evs[i])
+    torch.cuda.synchronize()
+    L.seg_profile_enable(0)
+    ph = {"layout": 0.0, "fwd": 0.0, "bwd": 0.0, "step": 0.0}
+    for e in evs:
+        for i in range(G):
+            nxt = e[f"l{i + 1}"] if i + 1 < G else e["end"]
+            ph["layout"] += e[f"l{i}"].elapsed_time(e[f"f{i}"])
+            ph["fwd"] += e[f"f{i}"].elapsed_time(e[f"b{i}"])
+            ph["bwd"] += e[f"b{i}"].elapsed_time(nxt)
+        ph["step"] += e["l0"].elapsed_time(e["end"])
+    ph = {k: v / steps for k, v in ph.items()}
+    scopes = {}
+    for name in LAYER_SCOPES:
+        tot = ctypes.c_double()
+        n = ctypes.c_int64()
+        _lib.check(L.seg_profile_read(name.encode(), ctypes.byref(tot), ctypes.byref(n)))
+        if n.value:
+            scopes[name] = round(tot.value / steps, 3)
+    L.seg_profile_reset()
+    return ph, scopes
+
+
+def layer_bench(cfg, steps, warmup, inter, groups, stepwise=True):
+    """Training step of one full decoder layer around the segmented attention
+    (forward + backward, all weight gradients) over the batch, segmented and
+    step-wise.  One JSON line (not the bench line)."""
+    import torch
+    dev = torch.device("cuda:0")
+    res = {}
+    cfgs = [("segmented", cfg)]
+    if stepwise:
+        cfgs.append(("stepwise", cfg.with_(name=cfg.name + "_stepwise", seg_steps=1,
+                                           mode="sliding")))
+    for label, c in cfgs:
+        run = LayerRun(c, dev, inter, groups)
+        ph, scopes = time_layer(run, steps, warmup)
+        gemm_ms = sum(scopes.get(n, 0.0) for n in ("ly_proj", "ly_mlp", "ly_wgrad"))
+        attn_ms = sum(scopes.get(n, 0.0) for n in ("attn_prep", "attn_fwd", "attn_delta",
+                                                    "attn_bwd_dkdv", "attn_bwd_dq"))
+        flop = run.gemm_flop() + run.attn_flop()
+        res[label] = {
+            "packed_tokens": run.P, "visible_pairs_per_head": run.pairs,
+            "ms_per_step": round(ph["step"], 3),
+            "traj_tokens_per_s": round(run.traj_tokens / (ph["step"] * 1e-3), 1),
+            "layer_tflops": round(flop / ((ph["fwd"] + ph["bwd"]) * 1e-3) / 1e12, 2),
+            "gemm_tflops": round(run.gemm_flop() / (gemm_ms * 1e-3) / 1e12, 2) if gemm_ms else None,
+            "attn_tflops": round(run.attn_flop() / (attn_ms * 1e-3) / 1e12, 2) if attn_ms else None,
+            "phases_ms": {k: round(v, 3) for k, v in ph.items()},
+            "scopes_ms": scopes,
+        }
+        log(f"  {label}: {res[label]}")
+        run.free()
+        del run
+        torch.cuda.empty_cache()
+    out = {"layer": f"{cfg.name}: hidden {cfg.hidden}, MLP {inter}, {cfg.hq}q/{cfg.hkv}kv heads, "
+                    f"d={cfg.head_dim}, RMSNorm + RoPE + SwiGLU, {groups} trajectory groups",
+           "steps": steps, "warmup": warmup, "dtype": "bf16", **res}
+    if stepwise:
+        out["speedup_vs_stepwise"] = round(res["stepwise"]["ms_per_step"] /
+                                           res["segmented"]["ms_per_step"], 3)
+    print(json.dumps(out), flush=True)
+
+
 SWEEP_K = (1, 3, 5, 8, 10, 15)
 
 
@@ -388,6 +566,12 @@ def main():
     ap.add_argument("--pmc-driver", action="store_true",
                     help="one launch of each attention kernel plus a calibration copy, for "
                          "rocprofv3 --pmc counter passes (no timing, no JSON bench line)")
+    ap.add_argument("--layer", action="store_true",
+                    help="training step of one full decoder layer (projections, RoPE, segmented "
+                         "attention, SwiGLU MLP) segmented vs step-wise (one JSON line; not the "
+                         "bench line)")
+    ap.add_argument("--layer-inter", type=int, default=LAYER_INTER)
+    ap.add_argument("--layer-groups", type=int, default=LAYER_GROUPS)
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the segmented path runs on a single MI355X and this "
@@ -402,6 +586,10 @@ def main():
         sys.exit(1)
     if args.pmc_driver:
         pmc_driver(args.config)
+        return
+    if args.layer:
+        layer_bench(WL.CONFIGS[args.config], args.steps, args.warmup, args.layer_inter,
+                    args.layer_groups, not args.no_stepwise)
         return
     if args.sweep:
         sweep(WL.CONFIGS[args.config], args.steps, args.warmup)

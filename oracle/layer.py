@@ -5,9 +5,9 @@ TEST INFRASTRUCTURE ONLY (see the package docstring).
 The paper trains the language model of a vision-language agent on VCS
 segments and keeps the vision encoder fixed during RL (App. E, RL stage), so
 the screenshot tokens enter the language model as given hidden states.  It does
-not spell out the layer, so this follows the Qwen-style decoder layer of the
-backbones it trains (pre-norm RMSNorm, grouped-query attention with rotary
-position embedding, SwiGLU MLP), float64 throughout:
+not spell out the layer, so this follows a generic Qwen-family decoder layer
+(pre-norm RMSNorm, grouped-query attention with rotary position embedding,
+SwiGLU MLP; no biases, no per-head q/k norm), float64 throughout:
 
     a  = rms(x) * g1                    rms(x) = x / sqrt(mean(x^2) + eps)
     q, k, v = a Wq^T, a Wk^T, a Wv^T    (heads of d columns)

@@ -120,6 +120,13 @@ class Spans:
         """[num_traj+1] start of each trajectory in the canonical token order."""
         return np.concatenate([[0], np.cumsum(self.traj_tokens())]).astype(np.int64)
 
+    def subset(self, t0: int, t1: int) -> "Spans":
+        """Trajectories t0 .. t1-1 as a batch of their own."""
+        a, b = int(self.step_offsets[t0]), int(self.step_offsets[t1])
+        return Spans(step_offsets=(self.step_offsets[t0:t1 + 1] - a).astype(np.int32),
+                     prompt_len=self.prompt_len[t0:t1].copy(), img_len=self.img_len[a:b].copy(),
+                     text_len=self.text_len[a:b].copy(), action_len=self.action_len[a:b].copy())
+
 
 def make_spans(cfg: Config, seed: Optional[int] = None) -> Spans:
     """Draw turn counts and text lengths (NumPy PCG64, SeedSequence(seed))."""

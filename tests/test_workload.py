@@ -52,3 +52,11 @@ def test_layer_generators_host_and_device_identical():
     x = WL.layer_rows_np(3, "x", np.array([4, 0, 6]), 40)
     xt = WL.layer_rows_torch(3, "x", 7, 40, device="cpu")
     assert np.array_equal(x, xt.to(torch.float64).numpy()[[4, 0, 6]])
+
+
+def test_spans_subset():
+    sp = WL.make_spans(WL.SMALL)
+    a, b = sp.subset(0, 2), sp.subset(2, 4)
+    assert a.num_traj == 2 and b.num_traj == 2 and a.num_steps + b.num_steps == sp.num_steps
+    assert np.array_equal(np.concatenate([a.traj_tokens(), b.traj_tokens()]), sp.traj_tokens())
+    assert np.array_equal(np.concatenate([a.text_len, b.text_len]), sp.text_len)
