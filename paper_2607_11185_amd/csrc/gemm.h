@@ -1,9 +1,13 @@
-// Shared "NT" GEMM of the libseg translation units (gfx950, bf16 MFMA):
+// Shared "NT" GEMMs of the libseg translation units (gfx950, bf16 MFMA):
 //   C[m][n] = sum_k A[m][k] * B[n][k]     (both operands k-contiguous)
-// 128x128 block tiles, 4 waves of 64x64, K in steps of 32.  The next K step
-// is staged in registers (its global loads are in flight while the current
-// step is multiplied) and written to the other LDS buffer afterwards.  The
-// epilogue is a functor called by every thread with the accumulators.
+// Two block shapes with one epilogue interface (a functor called by every
+// thread with its accumulators and a Tile that says where they sit):
+//  - k_gemm_nt: 128x128 blocks, 4 waves of 64x64, K in steps of 32, the next
+//    step staged in registers; two blocks per CU.  For grids too small to
+//    fill the chip with 256-wide tiles.
+//  - k_gemm_big: 256x256 blocks, 4 waves of 128x128 (one per SIMD, 256
+//    accumulator registers each), K in steps of 64 fetched by direct
+//    buffer->LDS loads into two 64 KB stages; XCD-aware grouped tile order.
 #pragma once
 
 #include "common.h"
@@ -13,14 +17,15 @@ namespace gemm {
 
 constexpr int BM = 128, BN = 128, BK = 32;
 
-// Where a wave's accumulators sit: rows m0 + wm*64 + bm*32 + 8*(r/4) + 4*hh + r%4,
-// columns n0 + wn*64 + bn*32 + col for register r of acc[bm][bn].
+// Where a wave's accumulators sit: rows m0 + wm*wt + bm*32 + 8*(r/4) + 4*hh + r%4,
+// columns n0 + wn*wt + bn*32 + col for register r of acc[bm][bn]; wt is the
+// wave tile (64 or 128), the block is 2x2 waves.
 struct Tile {
-  int m0, n0, M, N, wm, wn, col, hh;
+  int m0, n0, M, N, wm, wn, col, hh, wt;
   __device__ __forceinline__ int row(int bm, int r) const {
-    return m0 + wm * 64 + bm * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+    return m0 + wm * wt + bm * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
   }
-  __device__ __forceinline__ int column(int bn) const { return n0 + wn * 64 + bn * 32 + col; }
+  __device__ __forceinline__ int column(int bn) const { return n0 + wn * wt + bn * 32 + col; }
 };
 
 // C = scale * A B^T stored as TO (leading dimension ldc)
@@ -29,11 +34,12 @@ struct EpiStore {
   TO *c;
   long ldc;
   float scale;
-  __device__ __forceinline__ void operator()(const f32x16 (&acc)[2][2], const Tile &t) const {
+  template <int T>
+  __device__ __forceinline__ void operator()(const f32x16 (&acc)[T][T], const Tile &t) const {
 #pragma unroll
-    for (int bm = 0; bm < 2; ++bm)
+    for (int bm = 0; bm < T; ++bm)
 #pragma unroll
-      for (int bn = 0; bn < 2; ++bn) {
+      for (int bn = 0; bn < T; ++bn) {
         const int n = t.column(bn);
         if (n >= t.N) continue;
 #pragma unroll
@@ -52,11 +58,12 @@ struct EpiResid {
   const unsigned short *r;
   long ldr;
   float scale;
-  __device__ __forceinline__ void operator()(const f32x16 (&acc)[2][2], const Tile &t) const {
+  template <int T>
+  __device__ __forceinline__ void operator()(const f32x16 (&acc)[T][T], const Tile &t) const {
 #pragma unroll
-    for (int bm = 0; bm < 2; ++bm)
+    for (int bm = 0; bm < T; ++bm)
 #pragma unroll
-      for (int bn = 0; bn < 2; ++bn) {
+      for (int bn = 0; bn < T; ++bn) {
         const int n = t.column(bn);
         if (n >= t.N) continue;
 #pragma unroll
@@ -74,11 +81,12 @@ struct EpiAccum {
   float *c;
   long ldc;
   float scale;
-  __device__ __forceinline__ void operator()(const f32x16 (&acc)[2][2], const Tile &t) const {
+  template <int T>
+  __device__ __forceinline__ void operator()(const f32x16 (&acc)[T][T], const Tile &t) const {
 #pragma unroll
-    for (int bm = 0; bm < 2; ++bm)
+    for (int bm = 0; bm < T; ++bm)
 #pragma unroll
-      for (int bn = 0; bn < 2; ++bn) {
+      for (int bn = 0; bn < T; ++bn) {
         const int n = t.column(bn);
         if (n >= t.N) continue;
 #pragma unroll
@@ -160,10 +168,223 @@ __global__ void __launch_bounds__(256, 2) k_gemm_nt(const unsigned short *__rest
     if (more) stash(buf ^ 1);
     __syncthreads();
   }
-  ep(acc, Tile{m0, n0, M, N, wm, wn, col, hh});
+  ep(acc, Tile{m0, n0, M, N, wm, wn, col, hh, 64});
 }
 
 inline dim3 grid(int M, int N) { return dim3((unsigned)((N + BN - 1) / BN), (unsigned)((M + BM - 1) / BM)); }
+
+// ---------------------------------------------------------------- 256x256
+
+constexpr int BIG = 256, BKB = 64;
+constexpr int BIG_STAGE = 2 * BIG * BKB;  // bf16 elements of one stage (A then B): 64 KB
+
+// Raw buffer resource over [base, base + bytes): loads at or past the end
+// return zeros.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t gemm_rsrc(const void *base, long bytes) {
+  const long lim = bytes < 0x7fffffffL ? bytes : 0x7fffffffL;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)lim, 0x00020000);
+}
+
+// LDS layout of a 256 x 64 operand tile: row-major, 128 B per row, 16-byte
+// chunk c of row r stored in slot c ^ ((r >> 1) & 7).  Sixteen consecutive
+// rows then hit sixteen distinct 16-byte slots of the 64 banks (row parity
+// picks the half of the 256-byte bank line), so a fragment read of 32 rows x
+// 16 bytes is conflict-free.  A direct load writes 64 lanes x 16 bytes
+// = 8 rows in slot order; each lane fetches the chunk that belongs there.
+struct BigFill {
+  int voff[8];   // byte offset of the lane's chunk in each of its 8 row groups
+  int kchunk;    // the lane's logical k chunk (0..7)
+  __device__ __forceinline__ void init(int wave, int lane, long ld) {
+    const int rr = lane >> 3, slot = lane & 7;
+    // (row >> 1) & 7 is the same for all 8 row groups (they start at multiples of 8)
+    kchunk = slot ^ (((wave * 8 + rr) >> 1) & 7);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int row = (j * 4 + wave) * 8 + rr;
+      voff[j] = (int)(row * ld * 2) + kchunk * 16;
+    }
+  }
+  // loads the 64-column K step starting at k0 (chunks at or past K read
+  // zero; so does a whole step past the end); wave is wave-uniform
+  __device__ __forceinline__ void issue(unsigned short *__restrict__ tile,
+                                        __amdgpu_buffer_rsrc_t rs, int k0, int K, int wave) const {
+#if defined(__HIP_DEVICE_COMPILE__)
+    const int add = k0 + kchunk * 8 < K ? k0 * 2 : 0x40000000;
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rs, (__attribute__((address_space(3))) void *)(tile + (j * 4 + wave) * 8 * BKB), 16,
+          voff[j] + add, 0, 0, 0);
+#endif
+  }
+};
+
+// Tile order: a 1-D grid of 8 * ceil(T / 8) blocks for T tiles.  Block b runs
+// on XCD b % 8; XCD x takes the contiguous tile range [x*C, (x+1)*C) so its
+// concurrent blocks share an L2, and tiles are ordered in groups of 8 M-tiles
+// (column by column inside a group) so those blocks reuse A and B rows.
+__device__ __forceinline__ bool big_tile(int nM, int nN, int &mt, int &nt) {
+  const int total = nM * nN;
+  const int per = (total + 7) / 8;
+  const int idx = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+  if (idx >= total) return false;
+  const int G = 8;
+  const int group = idx / (G * nN);
+  const int first = group * G;
+  const int gs = nM - first < G ? nM - first : G;
+  const int in = idx - group * G * nN;
+  mt = first + in % gs;
+  nt = in / gs;
+  return true;
+}
+
+inline unsigned big_blocks(int M, int N) {
+  const long t = (long)((M + BIG - 1) / BIG) * ((N + BIG - 1) / BIG);
+  return (unsigned)((t + 7) / 8 * 8);
+}
+
+// Operand fragments of one 16-wide k slice: rows (w*128 + i*32 + col) of A and
+// B, 16 bytes each.
+struct BigFrags {
+  bf16x8 a[4], b[4];
+};
+
+__device__ __forceinline__ void big_load(BigFrags &f, const char *pa, const char *pb, int sw) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f.a[i] = *reinterpret_cast<const bf16x8 *>(pa + i * 32 * 128 + sw);
+    f.b[i] = *reinterpret_cast<const bf16x8 *>(pb + i * 32 * 128 + sw);
+  }
+}
+
+__device__ __forceinline__ void big_mma(f32x16 (&acc)[4][4], const BigFrags &f) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(f.a[i], f.b[j], acc[i][j]);
+}
+
+// Scheduling of one slice: the eight fragment reads of the next slice are
+// spread over the first eight products of this one, so their LDS latency
+// hides under the MFMA pipe (one wave per SIMD has no other wave to cover it).
+// The first slice of a step also carries the sixteen direct loads of the
+// next step.
+__device__ __forceinline__ void big_interleave(bool with_loads) {
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    if (i < 8) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+    if (with_loads) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // one global load
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+  }
+}
+
+// First three slices of a K step: issue the next step's direct loads (past
+// the end of K they read zeros into the idle buffer), then multiply slices
+// 0-2 of the current stage while reading slices 1-3.  f0 holds slice 0 on
+// entry; f1 holds slice 3 on exit.
+__device__ __forceinline__ void big_step(const unsigned short *__restrict__ rA,
+                                         const unsigned short *__restrict__ rB,
+                                         unsigned short *__restrict__ wA,
+                                         unsigned short *__restrict__ wB, const BigFill &fa,
+                                         const BigFill &fb, __amdgpu_buffer_rsrc_t ra,
+                                         __amdgpu_buffer_rsrc_t rb, int k_next, int K, int wave,
+                                         int offA, int offB, const int (&sw)[4], BigFrags &f0,
+                                         BigFrags &f1, f32x16 (&acc)[4][4]) {
+  fa.issue(wA, ra, k_next, K, wave);
+  fb.issue(wB, rb, k_next, K, wave);
+  const char *pa = reinterpret_cast<const char *>(rA) + offA;
+  const char *pb = reinterpret_cast<const char *>(rB) + offB;
+  big_load(f1, pa, pb, sw[1]);
+  big_mma(acc, f0);
+  big_interleave(true);
+  big_load(f0, pa, pb, sw[2]);
+  big_mma(acc, f1);
+  big_interleave(false);
+  big_load(f1, pa, pb, sw[3]);
+  big_mma(acc, f0);
+  big_interleave(false);
+}
+
+// lda, ldb and K must be multiples of 8 and 256 * ld * 2 < 2^30; rows beyond
+// M / N and chunks beyond K read as zero.  Grid: big_blocks(M, N) x 256.
+template <class Epi>
+__global__ void __launch_bounds__(256, 1) k_gemm_big(const unsigned short *__restrict__ A, long lda,
+                                                     const unsigned short *__restrict__ B, long ldb,
+                                                     int M, int N, int K, Epi ep) {
+  __shared__ __attribute__((aligned(1024))) unsigned short lds[2 * BIG_STAGE];
+  const int nM = (M + BIG - 1) / BIG, nN = (N + BIG - 1) / BIG;
+  int mt, nt;
+  if (!big_tile(nM, nN, mt, nt)) return;
+  const int m0 = mt * BIG, n0 = nt * BIG;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1, col = lane & 31, hh = lane >> 5;
+
+  // each resource covers only the block's own rows (< 2^30 bytes), so the
+  // offset of a chunk past K (+2^30) is out of range and reads zero
+  const __amdgpu_buffer_rsrc_t ra =
+      gemm_rsrc(A + (long)m0 * lda, (long)(M - m0 < BIG ? M - m0 : BIG) * lda * 2);
+  const __amdgpu_buffer_rsrc_t rb =
+      gemm_rsrc(B + (long)n0 * ldb, (long)(N - n0 < BIG ? N - n0 : BIG) * ldb * 2);
+  BigFill fa, fb;
+  fa.init(wave, lane, lda);
+  fb.init(wave, lane, ldb);
+
+  // fragment reads: row (w*128 + i*32 + col), logical chunk 2*kk + hh
+  const int sx = (col >> 1) & 7;
+  int sw[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) sw[kk] = ((2 * kk + hh) ^ sx) * 16;
+  const int offA = (wm * 128 + col) * 128, offB = (wn * 128 + col) * 128;
+
+  f32x16 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
+
+  unsigned short *s0 = lds, *s1 = lds + BIG_STAGE;
+  const int nk = (K + BKB - 1) / BKB;
+  fa.issue(s0, ra, 0, K, wave);
+  fb.issue(s0 + BIG * BKB, rb, 0, K, wave);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  BigFrags f0, f1;
+  big_load(f0, reinterpret_cast<const char *>(s0) + offA,
+           reinterpret_cast<const char *>(s0 + BIG * BKB) + offB, sw[0]);
+  for (int kt = 0; kt < nk; ++kt) {
+    unsigned short *cur = (kt & 1) ? s1 : s0;
+    unsigned short *nxt = (kt & 1) ? s0 : s1;
+    big_step(cur, cur + BIG * BKB, nxt, nxt + BIG * BKB, fa, fb, ra, rb, (kt + 1) * BKB, K, wave,
+             offA, offB, sw, f0, f1, acc);
+    // every wave is done reading this stage and the next one has landed; the
+    // last slice's products then cover the reads of the next stage's first
+    // slice (after the last step they read the zero-filled idle buffer)
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    big_load(f0, reinterpret_cast<const char *>(nxt) + offA,
+             reinterpret_cast<const char *>(nxt + BIG * BKB) + offB, sw[0]);
+    big_mma(acc, f1);
+    big_interleave(false);
+  }
+  ep(acc, Tile{m0, n0, M, N, wm, wn, col, hh, 128});
+}
+
+// Block shape for a problem: the 256-wide tiles unless they would leave more
+// than a quarter of the CUs idle in the first wave.
+inline bool gemm_use_big(int M, int N) {
+  return (long)((M + BIG - 1) / BIG) * ((N + BIG - 1) / BIG) >= 192;
+}
+
+template <class Epi>
+inline void gemm_launch(const unsigned short *A, long lda, const unsigned short *B, long ldb, int M,
+                        int N, int K, const Epi &ep, hipStream_t st) {
+  if (M <= 0 || N <= 0) return;
+  if (gemm_use_big(M, N))
+    k_gemm_big<Epi><<<big_blocks(M, N), 256, 0, st>>>(A, lda, B, ldb, M, N, K, ep);
+  else
+    k_gemm_nt<Epi><<<grid(M, N), 256, 0, st>>>(A, lda, B, ldb, M, N, K, ep);
+}
 
 // y[c][r] = x[r][c] for a [rows][cols] matrix (ldx), output [cols][ldy]; x is
 // bf16 bits or fp32 (rounded); optional row gather; zero for r >= rows up to

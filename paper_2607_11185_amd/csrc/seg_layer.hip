@@ -30,11 +30,12 @@ namespace {
 using gemm::EpiAccum;
 using gemm::EpiResid;
 using gemm::EpiStore;
-using gemm::k_gemm_nt;
 using gemm::k_transpose2d;
 
 constexpr int MAX_CH = 16;   // hidden <= 8 * 64 * MAX_CH
 constexpr int RMS_ROWS = 32; // rows per block of the norm backward
+constexpr int DEFAULT_CHUNK = 16384;     // rows per chunk when chunk_rows = 0
+constexpr int MAX_CHUNK = 1 << 20;       // GEMM rows are addressed with 32-bit offsets
 
 // ------------------------------------------------------------------ kernels
 
@@ -287,7 +288,7 @@ Dims dims_of(const seg_sizes &sz, const seg_layer_cfg &c) {
   m.d = c.d;
   m.QD = c.hq * c.d;
   m.KD = c.hkv * c.d;
-  long C = c.chunk_rows > 0 ? c.chunk_rows : m.P;
+  long C = c.chunk_rows > 0 ? c.chunk_rows : DEFAULT_CHUNK;
   C = std::max<long>(1, std::min<long>(C, std::max<long>(m.P, 1)));
   m.C = (int)C;
   m.Cp = (int)((C + 31) / 32 * 32);
@@ -357,6 +358,9 @@ void check_layer(const seg_layout *L, const seg_sizes *sz, const seg_layer_cfg *
   SEG_CHECK(std::isfinite(c->rope_base) && c->rope_base > 1.f, SEG_ERR_ARG,
             "rope_base must be > 1");
   SEG_CHECK(c->chunk_rows >= 0, SEG_ERR_ARG, "chunk_rows must be >= 0");
+  SEG_CHECK(c->chunk_rows <= MAX_CHUNK && c->inter <= MAX_CHUNK && (long)c->hq * c->d <= MAX_CHUNK,
+            SEG_ERR_UNSUPPORTED, "chunk_rows %d, inter %d or hq*d above %d", c->chunk_rows,
+            c->inter, MAX_CHUNK);
   SEG_CHECK(w->g1 && w->wq && w->wk && w->wv && w->wo && w->g2 && w->wg && w->wu && w->wd,
             SEG_ERR_ARG, "a weight pointer is NULL");
   SEG_CHECK((long)std::max<long>(sz->packed_tokens, 1) * std::max(c->hidden, c->inter) < (1L << 40),
@@ -369,8 +373,7 @@ void check_layer(const seg_layout *L, const seg_sizes *sz, const seg_layer_cfg *
 template <class Epi>
 void gemm_nt(const unsigned short *A, long lda, const unsigned short *B, long ldb, int M, int N, int K,
              const Epi &ep, hipStream_t st) {
-  if (M <= 0 || N <= 0) return;
-  k_gemm_nt<Epi><<<gemm::grid(M, N), 256, 0, st>>>(A, lda, B, ldb, M, N, K, ep);
+  gemm::gemm_launch(A, lda, B, ldb, M, N, K, ep, st);
   SEG_LAUNCH_CHECK();
 }
 

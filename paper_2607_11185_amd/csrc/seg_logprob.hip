@@ -22,8 +22,6 @@
 namespace seg {
 namespace {
 
-using gemm::BM;
-using gemm::BN;
 using gemm::EpiStore;
 using gemm::k_gemm_nt;
 using gemm::k_transpose2d;
@@ -35,23 +33,25 @@ constexpr float LN2 = 0.6931471805599453f;
 struct EpiLogits {
   float *zt;        // [M][ldz] fp32
   long ldz;
-  float2 *stats;    // [M/BM tiles][N]: (max, sum exp(z - max)) in log2 units
+  float2 *stats;    // [ceil(M/128) slabs][N]: (max, sum exp(z - max)) in log2 units
   int nrows;        // N
   const int32_t *target;  // [N]
   float *ztgt;      // [N]
   float scale;
-  __device__ __forceinline__ void operator()(const f32x16 (&acc)[2][2], const gemm::Tile &t) const {
-    __shared__ float2 sStat[2][BN];
-    const int tid = threadIdx.x;
-    // accumulator lane holds one row n
+  // for the 256-wide tiles: a wave covers one 128-row slab of M; the two lane
+  // halves of a column are combined by a shuffle
+  template <int T>
+  __device__ __forceinline__ void operator()(const f32x16 (&acc)[T][T], const gemm::Tile &t) const {
+    static_assert(T == 4, "logits epilogue expects 128-row wave tiles");
+    const int slab_row = t.m0 + t.wm * t.wt;
 #pragma unroll
-    for (int bn = 0; bn < 2; ++bn) {
+    for (int bn = 0; bn < T; ++bn) {
       const int n = t.column(bn);
       const bool nok = n < t.N;
       const int tgt = nok ? target[n] : -1;
       float mx = -INFINITY;
 #pragma unroll
-      for (int bm = 0; bm < 2; ++bm)
+      for (int bm = 0; bm < T; ++bm)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int m = t.row(bm, r);
@@ -66,7 +66,7 @@ struct EpiLogits {
       float sm = 0.f;
       if (mx != -INFINITY) {
 #pragma unroll
-        for (int bm = 0; bm < 2; ++bm)
+        for (int bm = 0; bm < T; ++bm)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int m = t.row(bm, r);
@@ -74,18 +74,8 @@ struct EpiLogits {
           }
       }
       sm += __shfl_xor(sm, 32, 64);
-      if (t.hh == 0) sStat[t.wm][t.wn * 64 + bn * 32 + t.col] = make_float2(mx, sm);
-    }
-    __syncthreads();
-    if (tid < BN && t.n0 + tid < t.N) {
-      const float2 a = sStat[0][tid], b = sStat[1][tid];
-      const float mx = fmaxf(a.x, b.x);
-      float sm = 0.f;
-      if (mx != -INFINITY) {
-        if (a.x != -INFINITY) sm += a.y * exp2f(a.x - mx);
-        if (b.x != -INFINITY) sm += b.y * exp2f(b.x - mx);
-      }
-      stats[(long)blockIdx.y * nrows + t.n0 + tid] = make_float2(mx, sm);
+      if (t.hh == 0 && nok && slab_row < t.M)
+        stats[(long)(slab_row / 128) * nrows + n] = make_float2(mx, sm);
     }
   }
 };
@@ -230,7 +220,7 @@ LpWs lp_ws(int rows, int hidden, int vocab, seg_dtype dt) {
   LpWs w{};
   w.Rp = (rows + 31) / 32 * 32;
   w.Vp = (vocab + 31) / 32 * 32;
-  w.ntiles = (vocab + BM - 1) / BM;
+  w.ntiles = (vocab + 127) / 128;  // 128-row slabs of the logits epilogue
   size_t off = 0;
   auto take = [&](size_t bytes) {
     size_t o = off;
@@ -301,9 +291,9 @@ void logprob_impl(int rows, int H, int V, const TI *h, const int32_t *row_index,
   SEG_HIP(hipMemsetAsync(ztgt, 0xff, sizeof(float) * Rp, st));
   {
     EpiLogits e{zt, Rp, stats, rows, target, ztgt, cfg.logit_scale};
-    dim3 grid((rows + BN - 1) / BN, (V + BM - 1) / BM);
     ProfScope prof("logits", st);
-    k_gemm_nt<EpiLogits><<<grid, 256, 0, st>>>(wb, H, hb, H, V, rows, H, e);
+    gemm::k_gemm_big<EpiLogits><<<gemm::big_blocks(V, rows), 256, 0, st>>>(wb, H, hb, H, V, rows,
+                                                                          H, e);
     SEG_LAUNCH_CHECK();
   }
   // 2. per-row loss
@@ -333,17 +323,15 @@ void logprob_impl(int rows, int H, int V, const TI *h, const int32_t *row_index,
   // 4. dH = s * dz W  (M = rows, N = H, K = Vp)
   {
     EpiStore<TO> e{static_cast<TO *>(dh), H, cfg.logit_scale};
-    dim3 grid((H + BN - 1) / BN, (rows + BM - 1) / BM);
     ProfScope prof("dh", st);
-    k_gemm_nt<EpiStore<TO>><<<grid, 256, 0, st>>>(dz, Vp, wt, Vp, rows, H, Vp, e);
+    gemm::gemm_launch(dz, Vp, wt, Vp, rows, H, Vp, e, st);
     SEG_LAUNCH_CHECK();
   }
   //    dW = s * dz^T h  (M = V, N = H, K = Rp)
   {
     EpiStore<float> e{dw, H, cfg.logit_scale};
-    dim3 grid((H + BN - 1) / BN, (V + BM - 1) / BM);
     ProfScope prof("dw", st);
-    k_gemm_nt<EpiStore<float>><<<grid, 256, 0, st>>>(dzt, Rp, ht, Rp, V, H, Rp, e);
+    gemm::gemm_launch(dzt, Rp, ht, Rp, V, H, Rp, e, st);
     SEG_LAUNCH_CHECK();
   }
 }
@@ -374,6 +362,10 @@ extern "C" seg_status seg_logprob_loss(int32_t rows, int32_t hidden, int32_t voc
     SEG_CHECK(rows >= 0 && hidden >= 1 && vocab >= 1 && num_traj >= 0, SEG_ERR_ARG,
               "bad sizes rows=%d hidden=%d vocab=%d num_traj=%d", rows, hidden, vocab, num_traj);
     SEG_CHECK(hidden % 8 == 0, SEG_ERR_UNSUPPORTED, "hidden %d must be a multiple of 8", hidden);
+    // GEMM operand rows (hidden, padded vocab, padded rows) are addressed with
+    // 32-bit offsets inside a 256-row block
+    SEG_CHECK(hidden <= (1 << 20) && vocab <= (1 << 20) - 256 && rows <= (1 << 20) - 256,
+              SEG_ERR_CAPACITY, "rows %d, hidden %d or vocab %d above 2^20", rows, hidden, vocab);
     SEG_CHECK(std::isfinite(cfg->eps_low) && std::isfinite(cfg->eps_high) &&
                   std::isfinite(cfg->loss_scale) && std::isfinite(cfg->logit_scale) &&
                   std::isfinite(cfg->dual_clip_c) && std::isfinite(cfg->kl_coef),
