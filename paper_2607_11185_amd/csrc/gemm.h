@@ -370,6 +370,173 @@ __global__ void __launch_bounds__(256, 1) k_gemm_big(const unsigned short *__res
   ep(acc, Tile{m0, n0, M, N, wm, wn, col, hh, 128});
 }
 
+// ------------------------------------------------- 256x256, transposed operands
+// C[m][n] = sum_k At[k][m] * Bt[k][n] with At [K][lda], Bt [K][ldb] row-major
+// (the weight gradients W^T-style: both operands run along the rows of a
+// chunk).  Tiles hold 64 k-rows x 256 columns (512 B per row); 16-byte chunk
+// c of row r sits in slot c ^ 4*(r & 3), so a 32-lane transpose read (4 rows x
+// 64 bytes) hits 16 distinct slots of the 64 banks.  Fragments come from
+// ds_read_b64_tr_b16 pairs: lane l gets column (l % 32) of rows
+// {4h..4h+3, 8+4h..8+4h+3} (h = l / 32) of the slice; A and B use the same
+// row order, so every product pairs equal k.
+
+typedef short gemm_v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) gemm_v4i16 gemm_lds_v4i16;
+
+struct BigFillT {
+  int voff[8];  // byte offset of the lane's chunk in each of its 8 row pairs
+  __device__ __forceinline__ void init(int wave, int lane, long ld) {
+    const int rr = lane >> 5, p = lane & 31;
+    // op j of a wave covers rows 2*(4j + wave) + {0, 1}; row & 3 = (2*wave + rr) & 3
+    const int c = p ^ (4 * ((2 * wave + rr) & 3));
+#pragma unroll
+    for (int j = 0; j < 8; ++j) voff[j] = (int)((2 * (j * 4 + wave) + rr) * ld * 2) + c * 16;
+  }
+  // rs covers the step's rows (from k0) of the block's columns
+  __device__ __forceinline__ void issue(unsigned short *__restrict__ tile,
+                                        __amdgpu_buffer_rsrc_t rs, int wave) const {
+#if defined(__HIP_DEVICE_COMPILE__)
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rs, (__attribute__((address_space(3))) void *)(tile + (j * 4 + wave) * 2 * BIG), 16,
+          voff[j], 0, 0, 0);
+#endif
+  }
+};
+
+// resource over rows [k0, min(K, k0 + 64)) of columns [c0, C) of a [K][ld]
+// matrix (zero rows past K; the last row stops at column C)
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tn_rsrc(const unsigned short *X, long ld, int k0,
+                                                         int K, int c0, int C) {
+  const int rows = K - k0 < BKB ? K - k0 : BKB;
+  const long bytes = rows > 0 ? ((long)(rows - 1) * ld + (C - c0)) * 2 : 0;
+  return gemm_rsrc(X + (long)k0 * ld + c0, bytes);
+}
+
+__device__ __forceinline__ bf16x8 tr_frag(const char *p) {
+  const gemm_v4i16 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((gemm_lds_v4i16 *)p);
+  const gemm_v4i16 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((gemm_lds_v4i16 *)(p + 8 * 512));
+  const bf16x4 a4 = __builtin_bit_cast(bf16x4, a), b4 = __builtin_bit_cast(bf16x4, b);
+  bf16x8 r;
+  r[0] = a4[0]; r[1] = a4[1]; r[2] = a4[2]; r[3] = a4[3];
+  r[4] = b4[0]; r[5] = b4[1]; r[6] = b4[2]; r[7] = b4[3];
+  return r;
+}
+
+// slice kk of the stage: rows 16*kk.. ; oa/ob: per-lane byte offsets of the
+// four 32-column blocks (row part included)
+__device__ __forceinline__ void big_load_tn(BigFrags &f, const char *pa, const char *pb,
+                                            const int (&oa)[4], const int (&ob)[4], int kk) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f.a[i] = tr_frag(pa + kk * 16 * 512 + oa[i]);
+    f.b[i] = tr_frag(pb + kk * 16 * 512 + ob[i]);
+  }
+}
+
+__device__ __forceinline__ void big_interleave_tn(bool with_loads) {
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS transpose read
+    if (with_loads) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // one global load
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+  }
+}
+
+__device__ __forceinline__ void big_step_tn(const unsigned short *__restrict__ rA,
+                                            const unsigned short *__restrict__ rB,
+                                            unsigned short *__restrict__ wA,
+                                            unsigned short *__restrict__ wB, const BigFillT &fa,
+                                            const BigFillT &fb, __amdgpu_buffer_rsrc_t ra,
+                                            __amdgpu_buffer_rsrc_t rb, int wave, const int (&oa)[4],
+                                            const int (&ob)[4], BigFrags &f0, BigFrags &f1,
+                                            f32x16 (&acc)[4][4]) {
+  fa.issue(wA, ra, wave);
+  fb.issue(wB, rb, wave);
+  const char *pa = reinterpret_cast<const char *>(rA);
+  const char *pb = reinterpret_cast<const char *>(rB);
+  big_load_tn(f1, pa, pb, oa, ob, 1);
+  big_mma(acc, f0);
+  big_interleave_tn(true);
+  big_load_tn(f0, pa, pb, oa, ob, 2);
+  big_mma(acc, f1);
+  big_interleave_tn(false);
+  big_load_tn(f1, pa, pb, oa, ob, 3);
+  big_mma(acc, f0);
+  big_interleave_tn(false);
+}
+
+// lda, ldb multiples of 8, 64 * ld * 2 < 2^30; K >= 0 rows (rows past K read
+// as zero); columns past M / N are computed from whatever the rows hold there
+// and dropped by the epilogue.  Grid: big_blocks(M, N) x 256.
+template <class Epi>
+__global__ void __launch_bounds__(256, 1) k_gemm_big_tn(const unsigned short *__restrict__ At,
+                                                        long lda,
+                                                        const unsigned short *__restrict__ Bt,
+                                                        long ldb, int M, int N, int K, Epi ep) {
+  __shared__ __attribute__((aligned(1024))) unsigned short lds[2 * BIG_STAGE];
+  const int nM = (M + BIG - 1) / BIG, nN = (N + BIG - 1) / BIG;
+  int mt, nt;
+  if (!big_tile(nM, nN, mt, nt)) return;
+  const int m0 = mt * BIG, n0 = nt * BIG;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1, col = lane & 31, hh = lane >> 5;
+
+  BigFillT fa, fb;
+  fa.init(wave, lane, lda);
+  fb.init(wave, lane, ldb);
+  // transpose-read offsets: row 4*hh + (lane%16)/4, column
+  // w*128 + 32*i + 16*((lane/16)%2) + 4*(lane%4)
+  const int l16 = lane & 15, r = 4 * hh + (l16 >> 2), sx = 4 * (r & 3);
+  int oa[4], ob[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int ca = wm * 128 + 32 * i + 16 * ((lane >> 4) & 1) + 4 * (l16 & 3);
+    const int cb = wn * 128 + 32 * i + 16 * ((lane >> 4) & 1) + 4 * (l16 & 3);
+    oa[i] = r * 512 + (((ca >> 3) ^ sx) << 4) + (ca & 7) * 2;
+    ob[i] = r * 512 + (((cb >> 3) ^ sx) << 4) + (cb & 7) * 2;
+  }
+
+  f32x16 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
+
+  unsigned short *s0 = lds, *s1 = lds + BIG_STAGE;
+  const int nk = (K + BKB - 1) / BKB;
+  fa.issue(s0, tn_rsrc(At, lda, 0, K, m0, M), wave);
+  fb.issue(s0 + BIG * BKB, tn_rsrc(Bt, ldb, 0, K, n0, N), wave);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  BigFrags f0, f1;
+  big_load_tn(f0, reinterpret_cast<const char *>(s0), reinterpret_cast<const char *>(s0 + BIG * BKB),
+              oa, ob, 0);
+  for (int kt = 0; kt < nk; ++kt) {
+    unsigned short *cur = (kt & 1) ? s1 : s0;
+    unsigned short *nxt = (kt & 1) ? s0 : s1;
+    const int k1 = (kt + 1) * BKB;
+    big_step_tn(cur, cur + BIG * BKB, nxt, nxt + BIG * BKB, fa, fb, tn_rsrc(At, lda, k1, K, m0, M),
+                tn_rsrc(Bt, ldb, k1, K, n0, N), wave, oa, ob, f0, f1, acc);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    big_load_tn(f0, reinterpret_cast<const char *>(nxt),
+                reinterpret_cast<const char *>(nxt + BIG * BKB), oa, ob, 0);
+    big_mma(acc, f1);
+    big_interleave_tn(false);
+  }
+  ep(acc, Tile{m0, n0, M, N, wm, wn, col, hh, 128});
+}
+
+template <class Epi>
+inline void gemm_launch_tn(const unsigned short *At, long lda, const unsigned short *Bt, long ldb,
+                           int M, int N, int K, const Epi &ep, hipStream_t st) {
+  if (M <= 0 || N <= 0) return;
+  k_gemm_big_tn<Epi><<<big_blocks(M, N), 256, 0, st>>>(At, lda, Bt, ldb, M, N, K, ep);
+}
+
 // Block shape for a problem: the 256-wide tiles unless they would leave more
 // than a quarter of the CUs idle in the first wave.
 inline bool gemm_use_big(int M, int N) {

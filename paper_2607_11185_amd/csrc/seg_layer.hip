@@ -5,10 +5,11 @@
 // token's row inside its segment as position, the segmented attention of
 // seg_attn.hip, output projection, RMSNorm and a SwiGLU MLP, with residual
 // connections; forward and backward on gfx950.  Projections and the MLP run
-// over row chunks with the shared NT GEMM (gemm.h); transposed operands are
-// materialised per chunk.  Weight gradients are summed chunk after chunk and
-// the norm-weight gradients through fixed-order partial sums, so results are
-// bitwise reproducible.
+// over row chunks with the shared GEMMs (gemm.h): data products with the NT
+// kernel (weights transposed once per call), weight gradients with the
+// transposed-operand kernel straight from the chunk's row-major activations.
+// Weight gradients are summed chunk after chunk and the norm-weight gradients
+// through fixed-order partial sums, so results are bitwise reproducible.
 #include <cmath>
 
 #include "common.h"
@@ -177,13 +178,29 @@ __global__ void __launch_bounds__(256) k_rms_bwd(const unsigned short *__restric
   }
 }
 
-// out[h] += sum over parts p (in order) of part[p][h]
-__global__ void k_colsum_add(const float *__restrict__ part, int nparts, int H,
-                             float *__restrict__ out) {
+// Column sums of part[nparts][H] in a fixed order, in two passes: block
+// (x, y) sums parts [y*per, (y+1)*per) of 256 columns into part2[y][H], then
+// out[h] += sum over y (in order) of part2[y][h].
+constexpr int COLSUM_SPLIT = 16;
+
+__global__ void __launch_bounds__(256) k_colsum_part(const float *__restrict__ part, int nparts,
+                                                     int H, float *__restrict__ part2) {
+  const int h = blockIdx.x * 256 + threadIdx.x;
+  if (h >= H) return;
+  const int per = (nparts + COLSUM_SPLIT - 1) / COLSUM_SPLIT;
+  const int p0 = blockIdx.y * per, p1 = min(nparts, p0 + per);
+  float s = 0.f;
+#pragma unroll 8
+  for (int p = p0; p < p1; ++p) s += part[(long)p * H + h];
+  part2[(long)blockIdx.y * H + h] = s;
+}
+
+__global__ void k_colsum_add(const float *__restrict__ part2, int H, float *__restrict__ out) {
   const int h = blockIdx.x * blockDim.x + threadIdx.x;
   if (h >= H) return;
   float s = 0.f;
-  for (int p = 0; p < nparts; ++p) s += part[(long)p * H + h];
+#pragma unroll
+  for (int y = 0; y < COLSUM_SPLIT; ++y) s += part2[(long)y * H + h];
   out[h] += s;
 }
 
@@ -275,7 +292,7 @@ int blocks_for(long n, int per = 256) { return (int)std::max<long>(1, std::min<l
 
 struct Dims {
   long P;
-  int H, I, hq, hkv, d, C, Cp, QD, KD;
+  int H, I, hq, hkv, d, C, QD, KD;
 };
 
 Dims dims_of(const seg_sizes &sz, const seg_layer_cfg &c) {
@@ -291,14 +308,13 @@ Dims dims_of(const seg_sizes &sz, const seg_layer_cfg &c) {
   long C = c.chunk_rows > 0 ? c.chunk_rows : DEFAULT_CHUNK;
   C = std::max<long>(1, std::min<long>(C, std::max<long>(m.P, 1)));
   m.C = (int)C;
-  m.Cp = (int)((C + 31) / 32 * 32);
   return m;
 }
 
 struct LayerWs {
   size_t pos, a, g, u, m, attn;                                  // forward
   size_t wdT, wgT, wuT, woT, wqT, wkT, wvT, dy1, dO, dq, dk, dv;  // backward
-  size_t dm, dg, du, dbf, tA, tB, part;
+  size_t dm, dg, du, dbf, part;
   size_t total;
 };
 
@@ -335,10 +351,7 @@ LayerWs layer_ws(const seg_sizes &sz, const seg_layer_cfg &c, int bwd) {
     w.dg = take(C * I * 2);
     w.du = take(C * I * 2);
     w.dbf = take(C * H * 4);
-    const size_t wide = std::max<size_t>({H, I, (size_t)m.QD});
-    w.tA = take(wide * m.Cp * 2);
-    w.tB = take(wide * m.Cp * 2);
-    w.part = take(((C + RMS_ROWS - 1) / RMS_ROWS) * 4 * H * 4);
+    w.part = take((((C + RMS_ROWS - 1) / RMS_ROWS) * 4 + COLSUM_SPLIT) * H * 4);
   }
   w.total = std::max<size_t>(off, 256);
   return w;
@@ -377,6 +390,14 @@ void gemm_nt(const unsigned short *A, long lda, const unsigned short *B, long ld
   SEG_LAUNCH_CHECK();
 }
 
+// C[M][N] (+)= At^T Bt over K rows; At [K][lda], Bt [K][ldb]
+template <class Epi>
+void gemm_tn(const unsigned short *At, long lda, const unsigned short *Bt, long ldb, int M, int N,
+             int K, const Epi &ep, hipStream_t st) {
+  gemm::gemm_launch_tn(At, lda, Bt, ldb, M, N, K, ep, st);
+  SEG_LAUNCH_CHECK();
+}
+
 void transpose(const unsigned short *x, long ldx, int rows, int cols, int pad_rows,
                unsigned short *y, hipStream_t st) {
   k_transpose2d<unsigned short><<<gemm::grid64(cols, pad_rows), 256, 0, st>>>(
@@ -396,7 +417,10 @@ void rms_bwd(const unsigned short *x, const void *g, const float *rstd, const fl
   const int nb = (rows + RMS_ROWS - 1) / RMS_ROWS;
   k_rms_bwd<<<nb, 256, 0, st>>>(x, H, CUS(g), rstd, dy, H, rows, H, pos, resid, H, out, H, part);
   SEG_LAUNCH_CHECK();
-  k_colsum_add<<<(H + 255) / 256, 256, 0, st>>>(part, nb * 4, H, dgrad);
+  float *part2 = part + (long)nb * 4 * H;
+  k_colsum_part<<<dim3((H + 255) / 256, COLSUM_SPLIT), 256, 0, st>>>(part, nb * 4, H, part2);
+  SEG_LAUNCH_CHECK();
+  k_colsum_add<<<(H + 255) / 256, 256, 0, st>>>(part2, H, dgrad);
   SEG_LAUNCH_CHECK();
 }
 
@@ -480,7 +504,7 @@ void layer_bwd_impl(const seg_layout *L, const seg_sizes *sz, const seg_layer_cf
                     char *base, const LayerWs &W, size_t ws_bytes, hipStream_t st) {
   const Dims m = dims_of(*sz, c);
   const long P = m.P;
-  const int H = m.H, I = m.I, Cp = m.Cp;
+  const int H = m.H, I = m.I;
   int32_t *pos = reinterpret_cast<int32_t *>(base + W.pos);
   unsigned short *a = US(base + W.a), *gb = US(base + W.g), *ub = US(base + W.u), *mb = US(base + W.m);
   unsigned short *wdT = US(base + W.wdT), *wgT = US(base + W.wgT), *wuT = US(base + W.wuT);
@@ -489,7 +513,6 @@ void layer_bwd_impl(const seg_layout *L, const seg_sizes *sz, const seg_layer_cf
   unsigned short *dy1 = US(base + W.dy1), *dO = US(base + W.dO), *dq = US(base + W.dq),
                  *dk = US(base + W.dk), *dv = US(base + W.dv);
   unsigned short *dm = US(base + W.dm), *dgb = US(base + W.dg), *dub = US(base + W.du);
-  unsigned short *tA = US(base + W.tA), *tB = US(base + W.tB);
   float *dbf = reinterpret_cast<float *>(base + W.dbf);
   float *part = reinterpret_cast<float *>(base + W.part);
   const unsigned short *q = CUS(sv.q), *k = CUS(sv.k), *v = CUS(sv.v), *o = CUS(sv.o),
@@ -541,23 +564,16 @@ void layer_bwd_impl(const seg_layout *L, const seg_sizes *sz, const seg_layer_cf
     }
     {
       ProfScope prof("ly_wgrad", st);
-      transpose(dy1c, H, cr, H, Cp, tA, st);  // dy^T [H, Cp]
-      transpose(mb, I, cr, I, Cp, tB, st);    // m^T [I, Cp]
-      gemm_nt(tA, Cp, tB, Cp, H, I, Cp, EpiAccum{gr.wd, I, 1.f}, st);
-      transpose(a, H, cr, H, Cp, tB, st);     // b^T [H, Cp]
-      transpose(dgb, I, cr, I, Cp, tA, st);   // dg^T [I, Cp]
-      gemm_nt(tA, Cp, tB, Cp, I, H, Cp, EpiAccum{gr.wg, H, 1.f}, st);
-      transpose(dub, I, cr, I, Cp, tA, st);   // du^T [I, Cp]
-      gemm_nt(tA, Cp, tB, Cp, I, H, Cp, EpiAccum{gr.wu, H, 1.f}, st);
+      gemm_tn(dy1c, H, mb, I, H, I, cr, EpiAccum{gr.wd, I, 1.f}, st);  // dWd += dy^T m
+      gemm_tn(dgb, I, a, H, I, H, cr, EpiAccum{gr.wg, H, 1.f}, st);    // dWg += dg^T b
+      gemm_tn(dub, I, a, H, I, H, cr, EpiAccum{gr.wu, H, 1.f}, st);    // dWu += du^T b
     }
     {
       ProfScope prof("ly_norm", st);
       rms_bwd(y1 + r0 * H, w.g2, sv.rstd2 + r0, dbf, cr, H, pos + r0, dy1c, dy1c, part, gr.g2, st);
     }
     ProfScope prof("ly_proj", st);
-    transpose(dy1c, H, cr, H, Cp, tA, st);                       // dy1^T [H, Cp]
-    transpose(o + r0 * m.QD, m.QD, cr, m.QD, Cp, tB, st);        // o^T [QD, Cp]
-    gemm_nt(tA, Cp, tB, Cp, H, m.QD, Cp, EpiAccum{gr.wo, m.QD, 1.f}, st);
+    gemm_tn(dy1c, H, o + r0 * m.QD, m.QD, H, m.QD, cr, EpiAccum{gr.wo, m.QD, 1.f}, st);  // dWo
     gemm_nt(dy1c, H, woT, H, cr, m.QD, H, EpiStore<unsigned short>{dO + r0 * m.QD, m.QD, 1.f}, st);
   }
   check_status(seg_attn_bwd(L, sz, SEG_BF16, m.hq, m.hkv, m.d, 1.f / std::sqrt((float)m.d), q, k, v,
@@ -588,13 +604,9 @@ void layer_bwd_impl(const seg_layout *L, const seg_sizes *sz, const seg_layer_cf
     }
     {
       ProfScope prof("ly_wgrad", st);
-      transpose(a, H, cr, H, Cp, tB, st);  // a^T [H, Cp]
-      transpose(dq + r0 * m.QD, m.QD, cr, m.QD, Cp, tA, st);
-      gemm_nt(tA, Cp, tB, Cp, m.QD, H, Cp, EpiAccum{gr.wq, H, 1.f}, st);
-      transpose(dk + r0 * m.KD, m.KD, cr, m.KD, Cp, tA, st);
-      gemm_nt(tA, Cp, tB, Cp, m.KD, H, Cp, EpiAccum{gr.wk, H, 1.f}, st);
-      transpose(dv + r0 * m.KD, m.KD, cr, m.KD, Cp, tA, st);
-      gemm_nt(tA, Cp, tB, Cp, m.KD, H, Cp, EpiAccum{gr.wv, H, 1.f}, st);
+      gemm_tn(dq + r0 * m.QD, m.QD, a, H, m.QD, H, cr, EpiAccum{gr.wq, H, 1.f}, st);  // dWq += dq^T a
+      gemm_tn(dk + r0 * m.KD, m.KD, a, H, m.KD, H, cr, EpiAccum{gr.wk, H, 1.f}, st);
+      gemm_tn(dv + r0 * m.KD, m.KD, a, H, m.KD, H, cr, EpiAccum{gr.wv, H, 1.f}, st);
     }
     ProfScope prof("ly_norm", st);
     rms_bwd(x + r0 * H, w.g1, sv.rstd1 + r0, dbf, cr, H, pos + r0, dy1 + r0 * H, dx + r0 * H, part,
