@@ -28,6 +28,40 @@ struct Tile {
   __device__ __forceinline__ int column(int bn) const { return n0 + wn * wt + bn * 32 + col; }
 };
 
+// Raw buffer resource over [base, base + bytes): loads at or past the end
+// return zeros.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t gemm_rsrc(const void *base, long bytes) {
+  const long lim = bytes < 0x7fffffffL ? bytes : 0x7fffffffL;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)lim, 0x00020000);
+}
+
+// Epilogue stores go through a buffer resource that starts at the block's
+// corner (m0, n0) of C and spans its rows (at most 2*wt): a row past M has a
+// byte offset past the resource and its store is dropped by the hardware;
+// columns past N are masked per 32-column group.  A lane's offset is one register plus, per accumulator
+// row, a wave-uniform row offset; the 32-column group is an immediate.
+// ldc * (2*wt) * sizeof(element) must stay below 2^31.
+struct EpiRows {
+  __amdgpu_buffer_rsrc_t rs;
+  int lane;  // byte offset of the lane's first row and column
+  int rowb;  // bytes per row
+  __device__ __forceinline__ EpiRows(const void *base, long ld, int esz, const Tile &t) {
+    const int rows = t.M - t.m0 < 2 * t.wt ? t.M - t.m0 : 2 * t.wt;
+    rs = gemm_rsrc(static_cast<const char *>(base) + ((long)t.m0 * ld + t.n0) * esz,
+                   (long)rows * ld * esz);
+    rowb = (int)(ld * esz);
+    lane = (t.wm * t.wt + 4 * t.hh) * rowb + (t.wn * t.wt + t.col) * esz;
+  }
+  // byte offset of accumulator register r of row block bm, column group bn
+  __device__ __forceinline__ int at(int bm, int bn, int r, int esz) const {
+    return lane + (bm * 32 + 8 * (r >> 2) + (r & 3)) * rowb + bn * 32 * esz;
+  }
+};
+
+__device__ __forceinline__ void buf_store_bf16(__amdgpu_buffer_rsrc_t rs, int off, float v) {
+  __builtin_amdgcn_raw_buffer_store_b16(f2bf_bits(v), rs, off, 0, 0);
+}
+
 // C = scale * A B^T stored as TO (leading dimension ldc)
 template <class TO>
 struct EpiStore {
@@ -36,18 +70,20 @@ struct EpiStore {
   float scale;
   template <int T>
   __device__ __forceinline__ void operator()(const f32x16 (&acc)[T][T], const Tile &t) const {
+    const EpiRows o(c, ldc, (int)sizeof(TO), t);
 #pragma unroll
-    for (int bm = 0; bm < T; ++bm)
+    for (int bn = 0; bn < T; ++bn) {
+      if (t.column(bn) >= t.N) continue;
 #pragma unroll
-      for (int bn = 0; bn < T; ++bn) {
-        const int n = t.column(bn);
-        if (n >= t.N) continue;
+      for (int bm = 0; bm < T; ++bm)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int m = t.row(bm, r);
-          if (m < t.M) store_val(c, (long)m * ldc + n, acc[bm][bn][r] * scale);
+          const float v = acc[bm][bn][r] * scale;
+          const int off = o.at(bm, bn, r, (int)sizeof(TO));
+          if constexpr (sizeof(TO) == 2) buf_store_bf16(o.rs, off, v);
+          else __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), o.rs, off, 0, 0);
         }
-      }
+    }
   }
 };
 
@@ -60,19 +96,18 @@ struct EpiResid {
   float scale;
   template <int T>
   __device__ __forceinline__ void operator()(const f32x16 (&acc)[T][T], const Tile &t) const {
+    const EpiRows o(c, ldc, 2, t), i(r, ldr, 2, t);
 #pragma unroll
-    for (int bm = 0; bm < T; ++bm)
+    for (int bn = 0; bn < T; ++bn) {
+      if (t.column(bn) >= t.N) continue;
 #pragma unroll
-      for (int bn = 0; bn < T; ++bn) {
-        const int n = t.column(bn);
-        if (n >= t.N) continue;
+      for (int bm = 0; bm < T; ++bm)
 #pragma unroll
         for (int rr = 0; rr < 16; ++rr) {
-          const int m = t.row(bm, rr);
-          if (m < t.M)
-            c[(long)m * ldc + n] = f2bf_bits(bf_bits2f(r[(long)m * ldr + n]) + acc[bm][bn][rr] * scale);
+          const unsigned short x = __builtin_amdgcn_raw_buffer_load_b16(i.rs, i.at(bm, bn, rr, 2), 0, 0);
+          buf_store_bf16(o.rs, o.at(bm, bn, rr, 2), bf_bits2f(x) + acc[bm][bn][rr] * scale);
         }
-      }
+    }
   }
 };
 
@@ -83,18 +118,20 @@ struct EpiAccum {
   float scale;
   template <int T>
   __device__ __forceinline__ void operator()(const f32x16 (&acc)[T][T], const Tile &t) const {
+    const EpiRows o(c, ldc, 4, t);
 #pragma unroll
-    for (int bm = 0; bm < T; ++bm)
+    for (int bn = 0; bn < T; ++bn) {
+      if (t.column(bn) >= t.N) continue;
 #pragma unroll
-      for (int bn = 0; bn < T; ++bn) {
-        const int n = t.column(bn);
-        if (n >= t.N) continue;
+      for (int bm = 0; bm < T; ++bm)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int m = t.row(bm, r);
-          if (m < t.M) c[(long)m * ldc + n] += acc[bm][bn][r] * scale;
+          const int off = o.at(bm, bn, r, 4);
+          const float x = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(o.rs, off, 0, 0));
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, x + acc[bm][bn][r] * scale),
+                                                o.rs, off, 0, 0);
         }
-      }
+    }
   }
 };
 
@@ -178,12 +215,6 @@ inline dim3 grid(int M, int N) { return dim3((unsigned)((N + BN - 1) / BN), (uns
 constexpr int BIG = 256, BKB = 64;
 constexpr int BIG_STAGE = 2 * BIG * BKB;  // bf16 elements of one stage (A then B): 64 KB
 
-// Raw buffer resource over [base, base + bytes): loads at or past the end
-// return zeros.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t gemm_rsrc(const void *base, long bytes) {
-  const long lim = bytes < 0x7fffffffL ? bytes : 0x7fffffffL;
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)lim, 0x00020000);
-}
 
 // LDS layout of a 256 x 64 operand tile: row-major, 128 B per row, 16-byte
 // chunk c of row r stored in slot c ^ ((r >> 1) & 7).  Sixteen consecutive
