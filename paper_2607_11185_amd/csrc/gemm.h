@@ -254,11 +254,12 @@ struct BigFill {
 // on XCD b % 8; XCD x takes the contiguous tile range [x*C, (x+1)*C) so its
 // concurrent blocks share an L2, and tiles are ordered in groups of 8 M-tiles
 // (column by column inside a group) so those blocks reuse A and B rows.
-__device__ __forceinline__ bool big_tile(int nM, int nN, int &mt, int &nt) {
-  const int total = nM * nN;
+__device__ __forceinline__ int big_index(int total) {
   const int per = (total + 7) / 8;
-  const int idx = (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
-  if (idx >= total) return false;
+  return (int)(blockIdx.x & 7) * per + (int)(blockIdx.x >> 3);
+}
+
+__device__ __forceinline__ void big_tile_of(int idx, int nM, int nN, int &mt, int &nt) {
   const int G = 8;
   const int group = idx / (G * nN);
   const int first = group * G;
@@ -266,6 +267,12 @@ __device__ __forceinline__ bool big_tile(int nM, int nN, int &mt, int &nt) {
   const int in = idx - group * G * nN;
   mt = first + in % gs;
   nt = in / gs;
+}
+
+__device__ __forceinline__ bool big_tile(int nM, int nN, int &mt, int &nt) {
+  const int idx = big_index(nM * nN);
+  if (idx >= nM * nN) return false;
+  big_tile_of(idx, nM, nN, mt, nt);
   return true;
 }
 
@@ -296,14 +303,14 @@ __device__ __forceinline__ void big_mma(f32x16 (&acc)[4][4], const BigFrags &f) 
 }
 
 // Scheduling of one slice: the eight fragment reads of the next slice are
-// spread over the first eight products of this one, so their LDS latency
+// spread over the sixteen products of this one (one per two), so their LDS latency
 // hides under the MFMA pipe (one wave per SIMD has no other wave to cover it).
 // The first slice of a step also carries the sixteen direct loads of the
 // next step.
 __device__ __forceinline__ void big_interleave(bool with_loads) {
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
-    if (i < 8) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+    if (i % 2 == 0) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
     if (with_loads) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // one global load
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
   }
@@ -498,18 +505,46 @@ __device__ __forceinline__ void big_step_tn(const unsigned short *__restrict__ r
   big_interleave_tn(false);
 }
 
+// Up to three transposed-operand problems over the same K rows, run by one
+// launch (their tiles in sequence), so a short last wave of one problem is
+// filled by the next.  Each: C_p[M_p][N_p] (+)= At_p^T Bt_p.
+template <class Epi, int NP>
+struct TnGroup {
+  const unsigned short *At[NP], *Bt[NP];
+  long lda[NP], ldb[NP];
+  int M[NP], N[NP];
+  Epi ep[NP];
+  int start[NP + 1];  // first tile of each problem; start[NP] = all tiles
+};
+
 // lda, ldb multiples of 8, 64 * ld * 2 < 2^30; K >= 0 rows (rows past K read
 // as zero); columns past M / N are computed from whatever the rows hold there
-// and dropped by the epilogue.  Grid: big_blocks(M, N) x 256.
-template <class Epi>
-__global__ void __launch_bounds__(256, 1) k_gemm_big_tn(const unsigned short *__restrict__ At,
-                                                        long lda,
-                                                        const unsigned short *__restrict__ Bt,
-                                                        long ldb, int M, int N, int K, Epi ep) {
+// and dropped by the epilogue.  Grid: 8 * ceil(tiles / 8) x 256.
+template <class Epi, int NP>
+__global__ void __launch_bounds__(256, 1) k_gemm_big_tn(const TnGroup<Epi, NP> g, int K) {
   __shared__ __attribute__((aligned(1024))) unsigned short lds[2 * BIG_STAGE];
-  const int nM = (M + BIG - 1) / BIG, nN = (N + BIG - 1) / BIG;
+  const int idx = big_index(g.start[NP]);
+  if (idx >= g.start[NP]) return;
+  // the problem's fields by unrolled selects (no dynamic indexing of the
+  // kernel argument, which would copy it to scratch)
+  const unsigned short *At = g.At[0], *Bt = g.Bt[0];
+  long lda = g.lda[0], ldb = g.ldb[0];
+  int M = g.M[0], N = g.N[0], first = 0;
+  Epi ep = g.ep[0];
+#pragma unroll
+  for (int q = 1; q < NP; ++q)
+    if (idx >= g.start[q]) {
+      At = g.At[q];
+      Bt = g.Bt[q];
+      lda = g.lda[q];
+      ldb = g.ldb[q];
+      M = g.M[q];
+      N = g.N[q];
+      first = g.start[q];
+      ep = g.ep[q];
+    }
   int mt, nt;
-  if (!big_tile(nM, nN, mt, nt)) return;
+  big_tile_of(idx - first, (M + BIG - 1) / BIG, (N + BIG - 1) / BIG, mt, nt);
   const int m0 = mt * BIG, n0 = nt * BIG;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -561,11 +596,30 @@ __global__ void __launch_bounds__(256, 1) k_gemm_big_tn(const unsigned short *__
   ep(acc, Tile{m0, n0, M, N, wm, wn, col, hh, 128});
 }
 
+inline int big_tiles(int M, int N) {
+  return M <= 0 || N <= 0 ? 0 : ((M + BIG - 1) / BIG) * ((N + BIG - 1) / BIG);
+}
+
+template <class Epi, int NP>
+inline void gemm_launch_tn(TnGroup<Epi, NP> g, int K, hipStream_t st) {
+  g.start[0] = 0;
+  for (int q = 0; q < NP; ++q) g.start[q + 1] = g.start[q] + big_tiles(g.M[q], g.N[q]);
+  if (g.start[NP] == 0) return;
+  k_gemm_big_tn<Epi, NP><<<(unsigned)((g.start[NP] + 7) / 8 * 8), 256, 0, st>>>(g, K);
+}
+
 template <class Epi>
 inline void gemm_launch_tn(const unsigned short *At, long lda, const unsigned short *Bt, long ldb,
                            int M, int N, int K, const Epi &ep, hipStream_t st) {
-  if (M <= 0 || N <= 0) return;
-  k_gemm_big_tn<Epi><<<big_blocks(M, N), 256, 0, st>>>(At, lda, Bt, ldb, M, N, K, ep);
+  TnGroup<Epi, 1> g{};
+  g.At[0] = At;
+  g.Bt[0] = Bt;
+  g.lda[0] = lda;
+  g.ldb[0] = ldb;
+  g.M[0] = M;
+  g.N[0] = N;
+  g.ep[0] = ep;
+  gemm_launch_tn(g, K, st);
 }
 
 // Block shape for a problem: the 256-wide tiles unless they would leave more

@@ -35,7 +35,7 @@ using gemm::k_transpose2d;
 
 constexpr int MAX_CH = 16;   // hidden <= 8 * 64 * MAX_CH
 constexpr int RMS_ROWS = 32; // rows per block of the norm backward
-constexpr int DEFAULT_CHUNK = 16384;     // rows per chunk when chunk_rows = 0
+constexpr int DEFAULT_CHUNK = 32768;     // rows per chunk when chunk_rows = 0
 constexpr int MAX_CHUNK = 1 << 20;       // GEMM rows are addressed with 32-bit offsets
 
 // ------------------------------------------------------------------ kernels
@@ -237,23 +237,72 @@ __global__ void __launch_bounds__(256) k_rope(unsigned short *__restrict__ x, lo
 
 __device__ __forceinline__ float sigmoidf_(float g) { return 1.f / (1.f + __expf(-g)); }
 
-// m = silu(g) * u (8 elements per thread)
-__global__ void k_swiglu_fwd(const unsigned short *__restrict__ g, const unsigned short *__restrict__ u,
-                             unsigned short *__restrict__ m, long n8) {
-  for (long c = (long)blockIdx.x * blockDim.x + threadIdx.x; c < n8; c += (long)gridDim.x * blockDim.x) {
-    const u16x8 gv = *reinterpret_cast<const u16x8 *>(g + c * 8);
-    const u16x8 uv = *reinterpret_cast<const u16x8 *>(u + c * 8);
-    u16x8 o;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const float gf = bf_bits2f(gv[j]);
-      o[j] = f2bf_bits(gf * sigmoidf_(gf) * bf_bits2f(uv[j]));
-    }
-    *reinterpret_cast<u16x8 *>(m + c * 8) = o;
+// Gate and up projections side by side: block j of 128 rows of wgu holds
+// wg rows 64j..64j+63 then wu rows 64j..64j+63 (zero rows past I), so one
+// GEMM against wgu gives, in each 128-column wave tile, the gate and up
+// values of the same 64 features.  Grid-stride over 16-byte chunks.
+constexpr int GU_BLOCK = 64;
+
+__global__ void k_interleave_gu(const unsigned short *__restrict__ wg,
+                                const unsigned short *__restrict__ wu, int I, int H, long rows2,
+                                unsigned short *__restrict__ wgu) {
+  const long h8 = H / 8, n = rows2 * h8;
+  for (long c = (long)blockIdx.x * blockDim.x + threadIdx.x; c < n; c += (long)gridDim.x * blockDim.x) {
+    const long R = c / h8, k = (c - R * h8) * 8;
+    const long j = R / (2 * GU_BLOCK), w = R % (2 * GU_BLOCK);
+    const long f = j * GU_BLOCK + (w % GU_BLOCK);
+    u16x8 v = u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+    if (f < I) v = *reinterpret_cast<const u16x8 *>((w < GU_BLOCK ? wg : wu) + f * H + k);
+    *reinterpret_cast<u16x8 *>(wgu + R * H + k) = v;
   }
 }
 
-// dg = dm * u * silu'(g), du = dm * silu(g), silu'(g) = s (1 + g (1 - s)), s = sigmoid(g)
+// Epilogue of the GEMM against wgu (256-wide tiles): m = silu(g) * u for the
+// wave's 64 features, in fp32 from the accumulators (acc[.][0..1] hold the
+// gate, acc[.][2..3] the up values of the same rows and features); with g and
+// u set, also stores the gate and up values (the backward's recompute).
+// Outputs are [rows][ld] bf16 at feature columns.
+struct EpiSwiGLU {
+  unsigned short *m, *g, *u;
+  long ld;
+  int I;
+  template <int T>
+  __device__ __forceinline__ void operator()(const f32x16 (&acc)[T][T], const gemm::Tile &t) const {
+    static_assert(T == 4, "SwiGLU epilogue expects 128-column wave tiles");
+    const int f0 = (t.n0 + t.wn * t.wt) / 2;  // first feature of the wave
+    const int rows = t.M - t.m0 < 2 * t.wt ? t.M - t.m0 : 2 * t.wt;
+    const long base = (long)t.m0 * ld + f0;
+    const long span = (long)rows * ld * 2 - (long)f0 * 2;
+    const __amdgpu_buffer_rsrc_t rm = gemm::gemm_rsrc(m + base, span);
+    __amdgpu_buffer_rsrc_t rg = rm, ru = rm;
+    if (g) {
+      rg = gemm::gemm_rsrc(g + base, span);
+      ru = gemm::gemm_rsrc(u + base, span);
+    }
+    const int rowb = (int)(ld * 2);
+    const int lane = (t.wm * t.wt + 4 * t.hh) * rowb + t.col * 2;
+#pragma unroll
+    for (int bn = 0; bn < 2; ++bn) {
+      if (f0 + bn * 32 + t.col >= I) continue;
+#pragma unroll
+      for (int bm = 0; bm < T; ++bm)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float gv = acc[bm][bn][r], uv = acc[bm][bn + 2][r];
+          const int off = lane + (bm * 32 + 8 * (r >> 2) + (r & 3)) * rowb + bn * 64;
+          __builtin_amdgcn_raw_buffer_store_b16(f2bf_bits(gv * sigmoidf_(gv) * uv), rm, off, 0, 0);
+          if (g) {
+            __builtin_amdgcn_raw_buffer_store_b16(f2bf_bits(gv), rg, off, 0, 0);
+            __builtin_amdgcn_raw_buffer_store_b16(f2bf_bits(uv), ru, off, 0, 0);
+          }
+        }
+    }
+  }
+};
+
+// dg = dm * u * silu'(g), du = dm * silu(g), silu'(g) = s (1 + g (1 - s)),
+// s = sigmoid(g) (8 elements per thread).  A streaming kernel: folded into the
+// dm GEMM's epilogue its loads of g and u stall the one wave per SIMD.
 __global__ void k_swiglu_bwd(const unsigned short *__restrict__ g, const unsigned short *__restrict__ u,
                              const unsigned short *__restrict__ dm, unsigned short *__restrict__ dg,
                              unsigned short *__restrict__ du, long n8) {
@@ -312,9 +361,9 @@ Dims dims_of(const seg_sizes &sz, const seg_layer_cfg &c) {
 }
 
 struct LayerWs {
-  size_t pos, a, g, u, m, attn;                                  // forward
+  size_t pos, a, m, wgu, attn;                                   // forward
   size_t wdT, wgT, wuT, woT, wqT, wkT, wvT, dy1, dO, dq, dk, dv;  // backward
-  size_t dm, dg, du, dbf, part;
+  size_t g, u, dm, dg, du, dbf, part;
   size_t total;
 };
 
@@ -328,11 +377,11 @@ LayerWs layer_ws(const seg_sizes &sz, const seg_layer_cfg &c, int bwd) {
     return o;
   };
   const size_t P = std::max<long>(m.P, 1), C = m.C, H = m.H, I = m.I;
+  const size_t Ip = (I + GU_BLOCK - 1) / GU_BLOCK * GU_BLOCK;
   w.pos = take(P * 4);
   w.a = take(C * H * 2);
-  w.g = take(C * I * 2);
-  w.u = take(C * I * 2);
   w.m = take(C * I * 2);
+  w.wgu = take(2 * Ip * H * 2);
   w.attn = take(seg_attn_workspace_bytes(&sz, SEG_BF16, c.hq, c.hkv, c.d, bwd));
   if (bwd) {
     w.wdT = take(I * H * 2);
@@ -347,6 +396,8 @@ LayerWs layer_ws(const seg_sizes &sz, const seg_layer_cfg &c, int bwd) {
     w.dq = take(P * m.QD * 2);
     w.dk = take(P * m.KD * 2);
     w.dv = take(P * m.KD * 2);
+    w.g = take(C * I * 2);
+    w.u = take(C * I * 2);
     w.dm = take(C * I * 2);
     w.dg = take(C * I * 2);
     w.du = take(C * I * 2);
@@ -387,6 +438,23 @@ template <class Epi>
 void gemm_nt(const unsigned short *A, long lda, const unsigned short *B, long ldb, int M, int N, int K,
              const Epi &ep, hipStream_t st) {
   gemm::gemm_launch(A, lda, B, ldb, M, N, K, ep, st);
+  SEG_LAUNCH_CHECK();
+}
+
+void build_wgu(const seg_layer_weights &w, int I, int H, unsigned short *wgu, hipStream_t st) {
+  const long rows2 = 2L * ((I + GU_BLOCK - 1) / GU_BLOCK * GU_BLOCK);
+  k_interleave_gu<<<blocks_for(rows2 * (H / 8)), 256, 0, st>>>(CUS(w.wg), CUS(w.wu), I, H, rows2, wgu);
+  SEG_LAUNCH_CHECK();
+}
+
+// rows x [gate | up] of a chunk against the interleaved weights, consumed by
+// the SwiGLU epilogue (always the 256-wide tiles: it pairs the two 64-column
+// halves of a 128-column wave tile)
+void gate_up(const unsigned short *a, const unsigned short *wgu, int rows, int H, int I,
+             const EpiSwiGLU &ep, hipStream_t st) {
+  const int N = 2 * ((I + GU_BLOCK - 1) / GU_BLOCK * GU_BLOCK);
+  if (rows <= 0) return;
+  gemm::k_gemm_big<EpiSwiGLU><<<gemm::big_blocks(rows, N), 256, 0, st>>>(a, H, wgu, H, rows, N, H, ep);
   SEG_LAUNCH_CHECK();
 }
 
@@ -448,11 +516,12 @@ void layer_fwd_impl(const seg_layout *L, const seg_sizes *sz, const seg_layer_cf
   const long P = m.P;
   const int H = m.H, I = m.I;
   int32_t *pos = reinterpret_cast<int32_t *>(base + W.pos);
-  unsigned short *a = US(base + W.a), *gb = US(base + W.g), *ub = US(base + W.u), *mb = US(base + W.m);
+  unsigned short *a = US(base + W.a), *mb = US(base + W.m), *wgu = US(base + W.wgu);
   unsigned short *q = US(sv.q), *k = US(sv.k), *v = US(sv.v), *o = US(sv.o), *y1 = US(sv.y1);
   {
     ProfScope prof("ly_misc", st);
     positions(L, sz, P, pos, st);
+    build_wgu(w, I, H, wgu, st);
   }
   for (long r0 = 0; r0 < P; r0 += m.C) {
     const int cr = (int)std::min<long>(m.C, P - r0);
@@ -489,11 +558,7 @@ void layer_fwd_impl(const seg_layout *L, const seg_sizes *sz, const seg_layer_cf
       rms_fwd(y1 + r0 * H, H, w.g2, c.rms_eps, cr, H, pos + r0, a, sv.rstd2 + r0, st);
     }
     ProfScope prof("ly_mlp", st);
-    gemm_nt(a, H, CUS(w.wg), H, cr, I, H, EpiStore<unsigned short>{gb, I, 1.f}, st);
-    gemm_nt(a, H, CUS(w.wu), H, cr, I, H, EpiStore<unsigned short>{ub, I, 1.f}, st);
-    const long n8 = (long)cr * I / 8;
-    k_swiglu_fwd<<<blocks_for(n8), 256, 0, st>>>(gb, ub, mb, n8);
-    SEG_LAUNCH_CHECK();
+    gate_up(a, wgu, cr, H, I, EpiSwiGLU{mb, nullptr, nullptr, I, I}, st);
     gemm_nt(mb, I, CUS(w.wd), I, cr, H, I, EpiResid{y + r0 * H, H, y1 + r0 * H, H, 1.f}, st);
   }
 }
@@ -506,7 +571,8 @@ void layer_bwd_impl(const seg_layout *L, const seg_sizes *sz, const seg_layer_cf
   const long P = m.P;
   const int H = m.H, I = m.I;
   int32_t *pos = reinterpret_cast<int32_t *>(base + W.pos);
-  unsigned short *a = US(base + W.a), *gb = US(base + W.g), *ub = US(base + W.u), *mb = US(base + W.m);
+  unsigned short *a = US(base + W.a), *gb = US(base + W.g), *ub = US(base + W.u), *mb = US(base + W.m),
+                 *wgu = US(base + W.wgu);
   unsigned short *wdT = US(base + W.wdT), *wgT = US(base + W.wgT), *wuT = US(base + W.wuT);
   unsigned short *woT = US(base + W.woT), *wqT = US(base + W.wqT), *wkT = US(base + W.wkT),
                  *wvT = US(base + W.wvT);
@@ -529,6 +595,7 @@ void layer_bwd_impl(const seg_layout *L, const seg_sizes *sz, const seg_layer_cf
     SEG_HIP(hipMemsetAsync(gr.wu, 0, sizeof(float) * (size_t)I * H, st));
     SEG_HIP(hipMemsetAsync(gr.wd, 0, sizeof(float) * (size_t)H * I, st));
     positions(L, sz, P, pos, st);
+    build_wgu(w, I, H, wgu, st);
     // transposed weights (k-contiguous operands of the data-gradient GEMMs)
     transpose(CUS(w.wd), I, H, I, H, wdT, st);        // wd [H, I] -> [I, H]
     transpose(CUS(w.wg), H, I, H, I, wgT, st);        // wg [I, H] -> [H, I]
@@ -551,22 +618,23 @@ void layer_bwd_impl(const seg_layout *L, const seg_sizes *sz, const seg_layer_cf
     }
     {
       ProfScope prof("ly_mlp", st);
-      gemm_nt(a, H, CUS(w.wg), H, cr, I, H, EpiStore<unsigned short>{gb, I, 1.f}, st);
-      gemm_nt(a, H, CUS(w.wu), H, cr, I, H, EpiStore<unsigned short>{ub, I, 1.f}, st);
-      const long n8 = (long)cr * I / 8;
-      k_swiglu_fwd<<<blocks_for(n8), 256, 0, st>>>(gb, ub, mb, n8);
-      SEG_LAUNCH_CHECK();
+      gate_up(a, wgu, cr, H, I, EpiSwiGLU{mb, gb, ub, I, I}, st);  // m, g, u
       gemm_nt(dy1c, H, wdT, H, cr, I, H, EpiStore<unsigned short>{dm, I, 1.f}, st);  // dm = dy wd
+      const long n8 = (long)cr * I / 8;
       k_swiglu_bwd<<<blocks_for(n8), 256, 0, st>>>(gb, ub, dm, dgb, dub, n8);
       SEG_LAUNCH_CHECK();
       gemm_nt(dgb, I, wgT, I, cr, H, I, EpiStore<float>{dbf, H, 1.f}, st);  // db = dg wg + du wu
       gemm_nt(dub, I, wuT, I, cr, H, I, EpiAccum{dbf, H, 1.f}, st);
     }
     {
+      // dWd += dy^T m, dWg += dg^T b, dWu += du^T b in one launch
       ProfScope prof("ly_wgrad", st);
-      gemm_tn(dy1c, H, mb, I, H, I, cr, EpiAccum{gr.wd, I, 1.f}, st);  // dWd += dy^T m
-      gemm_tn(dgb, I, a, H, I, H, cr, EpiAccum{gr.wg, H, 1.f}, st);    // dWg += dg^T b
-      gemm_tn(dub, I, a, H, I, H, cr, EpiAccum{gr.wu, H, 1.f}, st);    // dWu += du^T b
+      gemm::TnGroup<EpiAccum, 3> g{{dy1c, dgb, dub}, {mb, a, a}, {H, I, I}, {I, H, H}, {H, I, I},
+                                   {I, H, H},
+                                   {EpiAccum{gr.wd, I, 1.f}, EpiAccum{gr.wg, H, 1.f},
+                                    EpiAccum{gr.wu, H, 1.f}}, {}};
+      gemm::gemm_launch_tn(g, cr, st);
+      SEG_LAUNCH_CHECK();
     }
     {
       ProfScope prof("ly_norm", st);
@@ -603,10 +671,14 @@ void layer_bwd_impl(const seg_layout *L, const seg_sizes *sz, const seg_layer_cf
       gemm_nt(dv + r0 * m.KD, m.KD, wvT, m.KD, cr, H, m.KD, EpiAccum{dbf, H, 1.f}, st);
     }
     {
+      // dWq += dq^T a, dWk += dk^T a, dWv += dv^T a in one launch
       ProfScope prof("ly_wgrad", st);
-      gemm_tn(dq + r0 * m.QD, m.QD, a, H, m.QD, H, cr, EpiAccum{gr.wq, H, 1.f}, st);  // dWq += dq^T a
-      gemm_tn(dk + r0 * m.KD, m.KD, a, H, m.KD, H, cr, EpiAccum{gr.wk, H, 1.f}, st);
-      gemm_tn(dv + r0 * m.KD, m.KD, a, H, m.KD, H, cr, EpiAccum{gr.wv, H, 1.f}, st);
+      gemm::TnGroup<EpiAccum, 3> g{{dq + r0 * m.QD, dk + r0 * m.KD, dv + r0 * m.KD}, {a, a, a},
+                                   {m.QD, m.KD, m.KD}, {H, H, H}, {m.QD, m.KD, m.KD}, {H, H, H},
+                                   {EpiAccum{gr.wq, H, 1.f}, EpiAccum{gr.wk, H, 1.f},
+                                    EpiAccum{gr.wv, H, 1.f}}, {}};
+      gemm::gemm_launch_tn(g, cr, st);
+      SEG_LAUNCH_CHECK();
     }
     ProfScope prof("ly_norm", st);
     rms_bwd(x + r0 * H, w.g1, sv.rstd1 + r0, dbf, cr, H, pos + r0, dy1 + r0 * H, dx + r0 * H, part,
