@@ -343,7 +343,7 @@ def pmc_driver(cfg_name):
 
 
 LAYER_INTER = 18944   # MLP width of the 7B-class backbone (Qwen2-7B shape)
-LAYER_GROUPS = 4      # trajectory groups (micro-batches) per layer step
+LAYER_GROUPS = 2      # trajectory groups (micro-batches) per layer step
 LAYER_SCOPES = ["layout", "ly_norm", "ly_rope", "ly_proj", "ly_mlp", "ly_wgrad", "ly_misc",
                 "attn_prep", "attn_fwd", "attn_delta", "attn_bwd_dkdv", "attn_bwd_dq"]
 
@@ -390,10 +390,10 @@ class LayerRun:
         torch.cuda.empty_cache()
         # outputs, saved activations and workspaces sized for the largest group
         big = max(self.groups, key=lambda g: g["P"])
-        self.y, self.saved = S.seg_layer_fwd(big["lay"], self.lc, self.w, big["x"])
-        self.dx, self.grads = S.seg_layer_bwd(big["lay"], self.lc, self.w, big["x"], self.saved,
-                                              big["dy"])
         self.ws = S.layer_workspace(big["lay"], self.lc, True)
+        self.y, self.saved = S.seg_layer_fwd(big["lay"], self.lc, self.w, big["x"], ws=self.ws)
+        self.dx, self.grads = S.seg_layer_bwd(big["lay"], self.lc, self.w, big["x"], self.saved,
+                                              big["dy"], ws=self.ws)
         torch.cuda.synchronize()
         log(f"[layer {cfg.name}] groups={len(self.groups)} packed={self.P} "
             f"(largest {big['P']}) pairs/head={self.pairs} inter={inter}")

@@ -155,3 +155,21 @@ def backward(x, w, segments, masks, hq, hkv, d, eps, base, saved, dy):
     da = dq @ w.wq + dk @ w.wk + dv @ w.wv
     dx_n, grads["g1"] = rms_backward(x, w.g1, s["r1"], da)
     return dy1 + dx_n, grads
+
+
+def forward_rows(x_seg, w, mask, rows, hq, hkv, d, eps, base):
+    """Layer output y for some rows of ONE segment, from that segment's hidden
+    states x_seg [L, H] (row i at position i) and its visibility mask [L, L]:
+    keys and values come from every row of the segment, queries and the rest
+    of the layer only from `rows`.  Same definitions as :func:`forward`."""
+    L = x_seg.shape[0]
+    rows = np.asarray(rows)
+    a, _ = rms_forward(x_seg, w.g1, eps)
+    pos = np.arange(L)
+    k = rope((a @ w.wk.T).reshape(L, hkv, d), pos, base)
+    v = (a @ w.wv.T).reshape(L, hkv, d)
+    q = rope((a[rows] @ w.wq.T).reshape(len(rows), hq, d), pos[rows], base)
+    o, _ = OA.forward_rows(q, k, v, mask[rows], 1.0 / np.sqrt(d))
+    y1 = x_seg[rows] + o.reshape(len(rows), hq * d) @ w.wo.T
+    b, _ = rms_forward(y1, w.g2, eps)
+    return y1 + (silu(b @ w.wg.T) * (b @ w.wu.T)) @ w.wd.T

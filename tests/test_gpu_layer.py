@@ -7,7 +7,9 @@ several 128-row tiles with ragged tails, hidden and MLP widths that are not
 multiples of the GEMM tile, head_dim 64 and 128, buffer padding, row chunking
 smaller than the batch.  Plus: chunking leaves the row-wise results bitwise
 unchanged, padding rows get no gradient, and an empty batch gives zero
-weight gradients."""
+weight gradients.  At the 7B-class layer width (hidden 3584, MLP 18944,
+28q/4kv): sampled output rows against the oracle's row-sampled forward, and
+the chunking / padding properties with buffers."""
 import numpy as np
 import pytest
 
@@ -154,3 +156,55 @@ def test_layer_empty_batch_zero_grads():
     assert y.shape == (0, H) and dx.shape == (0, H)
     for n in grads:
         assert torch.count_nonzero(grads[n]).item() == 0, n
+
+
+# the 7B-class layer width (hidden 3584, MLP 18944, 28q/4kv, d = 128) on one
+# trajectory of the 7b workload's turn shapes
+FULL = WL.SEVEN_B.with_(num_traj=1, steps=(12, 12), seed=31)
+FULL_I = 18944
+
+
+def test_layer_full_width_sampled_rows():
+    """Outputs of sampled rows (first, last and random rows of every segment)
+    against the oracle's row-sampled forward, which takes keys and values
+    from the whole segment."""
+    c = FULL
+    lr = LayerRun(c, c.hidden, FULL_I, 0)
+    say(f"full width: P={lr.P}")
+    y, _, _, _ = lr.gpu()
+    yg = y.float().cpu().numpy()
+    ref = OL.build(lr.run.spans, c.window, c.seg_steps, 128, with_tiles=False, mode=c.mode)
+    w = OLY.Weights(**WL.layer_weights_np(lr.seed, c.hidden, FULL_I, c.hq, c.hkv, c.head_dim))
+    rng = np.random.default_rng(5)
+    for sg in ref.segments:
+        rows = np.unique(np.concatenate([[0, sg.length - 1],
+                                         rng.choice(sg.length, 6, replace=False)]))
+        x_seg = WL.layer_rows_np(lr.seed, "x", lr.src[sg.start:sg.start + sg.length], c.hidden)
+        mask = OL.visibility(sg, vis_window(c))
+        yr = OLY.forward_rows(x_seg, w, mask, rows, c.hq, c.hkv, c.head_dim, EPS, BASE)
+        e = rel(yg[sg.start + rows], yr)
+        say(f"  segment at {sg.start} ({sg.length} rows): rel err {e:.2e}")
+        assert e < TOL, (sg.start, e)
+
+
+def test_layer_full_width_chunking_and_padding():
+    """At the full width with buffer padding: row chunking leaves y and dx
+    bitwise unchanged and the weight gradients equal up to summation order;
+    padding rows get dx = 0."""
+    import torch
+    c = FULL.with_(buffer_tokens=40000, seed=32)
+    lr = LayerRun(c, c.hidden, FULL_I, 0)
+    pad = lr.run.host["tok_src"] < 0
+    say(f"full width with buffers: P={lr.P}, padding rows {int(pad.sum())}")
+    assert pad.any()
+    y0, _, dx0, g0 = lr.gpu()
+    y0, dx0 = y0.clone(), dx0.clone()
+    g0 = {n: t.clone() for n, t in g0.items()}
+    lr.lc.chunk_rows = 10000
+    y1, _, dx1, g1 = lr.gpu()
+    assert torch.equal(y0, y1)
+    assert torch.equal(dx0, dx1)
+    for n in g0:
+        e = rel(_np(g1[n]), _np(g0[n]))
+        assert e < 1e-4, (n, e)
+    assert np.all(_np(dx0)[pad] == 0)

@@ -170,3 +170,14 @@ def test_layer_attention_part_uses_segment_positions():
     masks = [OL.visibility(sg, 2) for sg in lay.segments]
     y, _ = OLY.forward(x, w, lay.segments, masks, hq, hkv, d, 1e-6, 1e4)
     np.testing.assert_allclose(y[:n], y[n:], rtol=1e-13, atol=1e-13)
+
+
+def test_forward_rows_matches_forward():
+    """The row-sampled forward (keys of the whole segment, queries of some
+    rows) equals the full forward on those rows."""
+    lay, x, w, masks, a = _tiny(seed=7, buffers=32)
+    y, _ = OLY.forward(x, w, lay.segments, masks, **a)
+    for sg, m in zip(lay.segments, masks):
+        rows = np.array([0, sg.length // 2, sg.length - 1])
+        ys = OLY.forward_rows(x[sg.start:sg.start + sg.length], w, m, rows, **a)
+        np.testing.assert_allclose(ys, y[sg.start + rows], rtol=1e-12, atol=1e-12)
