@@ -5,9 +5,12 @@
 //  - k_gemm_nt: 128x128 blocks, 4 waves of 64x64, K in steps of 32, the next
 //    step staged in registers; two blocks per CU.  For grids too small to
 //    fill the chip with 256-wide tiles.
-//  - k_gemm_big: 256x256 blocks, 4 waves of 128x128 (one per SIMD, 256
-//    accumulator registers each), K in steps of 64 fetched by direct
-//    buffer->LDS loads into two 64 KB stages; XCD-aware grouped tile order.
+//  - k_gemm_big: 256x256 blocks, 8 waves of 128x64 (two per SIMD), K in
+//    steps of 64 fetched by direct buffer->LDS loads into two 64 KB stages;
+//    XCD-aware grouped tile order.
+//  - k_gemm_big_tn: the same block with transposed operands (both row-major
+//    over K), 4 waves of 128x128, fragments by transpose reads; up to three
+//    problems per launch.
 #pragma once
 
 #include "common.h"
@@ -17,15 +20,15 @@ namespace gemm {
 
 constexpr int BM = 128, BN = 128, BK = 32;
 
-// Where a wave's accumulators sit: rows m0 + wm*wt + bm*32 + 8*(r/4) + 4*hh + r%4,
-// columns n0 + wn*wt + bn*32 + col for register r of acc[bm][bn]; wt is the
-// wave tile (64 or 128), the block is 2x2 waves.
+// Where a wave's accumulators sit: rows m0 + wr + bm*32 + 8*(r/4) + 4*hh + r%4,
+// columns n0 + wc + bn*32 + col for register r of acc[bm][bn]; (wr, wc) is the
+// wave tile's corner inside the block, brows the block's row count.
 struct Tile {
-  int m0, n0, M, N, wm, wn, col, hh, wt;
+  int m0, n0, M, N, wr, wc, col, hh, brows;
   __device__ __forceinline__ int row(int bm, int r) const {
-    return m0 + wm * wt + bm * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+    return m0 + wr + bm * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
   }
-  __device__ __forceinline__ int column(int bn) const { return n0 + wn * wt + bn * 32 + col; }
+  __device__ __forceinline__ int column(int bn) const { return n0 + wc + bn * 32 + col; }
 };
 
 // Raw buffer resource over [base, base + bytes): loads at or past the end
@@ -35,31 +38,23 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t gemm_rsrc(const void *base, lo
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)lim, 0x00020000);
 }
 
-// Epilogue stores go through a buffer resource that starts at the block's
-// corner (m0, n0) of C and spans its rows (at most 2*wt): a row past M has a
-// byte offset past the resource and its store is dropped by the hardware;
-// columns past N are masked per 32-column group.  A lane's offset is one register plus, per accumulator
-// row, a wave-uniform row offset; the 32-column group is an immediate.
-// ldc * (2*wt) * sizeof(element) must stay below 2^31.
-struct EpiRows {
-  __amdgpu_buffer_rsrc_t rs;
-  int lane;  // byte offset of the lane's first row and column
-  int rowb;  // bytes per row
-  __device__ __forceinline__ EpiRows(const void *base, long ld, int esz, const Tile &t) {
-    const int rows = t.M - t.m0 < 2 * t.wt ? t.M - t.m0 : 2 * t.wt;
-    rs = gemm_rsrc(static_cast<const char *>(base) + ((long)t.m0 * ld + t.n0) * esz,
-                   (long)rows * ld * esz);
-    rowb = (int)(ld * esz);
-    lane = (t.wm * t.wt + 4 * t.hh) * rowb + (t.wn * t.wt + t.col) * esz;
-  }
-  // byte offset of accumulator register r of row block bm, column group bn
-  __device__ __forceinline__ int at(int bm, int bn, int r, int esz) const {
-    return lane + (bm * 32 + 8 * (r >> 2) + (r & 3)) * rowb + bn * 32 * esz;
-  }
-};
-
-__device__ __forceinline__ void buf_store_bf16(__amdgpu_buffer_rsrc_t rs, int off, float v) {
-  __builtin_amdgcn_raw_buffer_store_b16(f2bf_bits(v), rs, off, 0, 0);
+// Calls f(m, n, v) for every accumulator of the wave inside [0, M) x [0, N)
+// (plain global stores: with two waves per SIMD they measured faster than
+// stores through a buffer resource).
+template <int TM, int TN, class F>
+__device__ __forceinline__ void tile_apply(const f32x16 (&acc)[TM][TN], const Tile &t, F &&f) {
+#pragma unroll
+  for (int bm = 0; bm < TM; ++bm)
+#pragma unroll
+    for (int bn = 0; bn < TN; ++bn) {
+      const int n = t.column(bn);
+      if (n >= t.N) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = t.row(bm, r);
+        if (m < t.M) f(m, n, acc[bm][bn][r]);
+      }
+    }
 }
 
 // C = scale * A B^T stored as TO (leading dimension ldc)
@@ -68,22 +63,12 @@ struct EpiStore {
   TO *c;
   long ldc;
   float scale;
-  template <int T>
-  __device__ __forceinline__ void operator()(const f32x16 (&acc)[T][T], const Tile &t) const {
-    const EpiRows o(c, ldc, (int)sizeof(TO), t);
-#pragma unroll
-    for (int bn = 0; bn < T; ++bn) {
-      if (t.column(bn) >= t.N) continue;
-#pragma unroll
-      for (int bm = 0; bm < T; ++bm)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float v = acc[bm][bn][r] * scale;
-          const int off = o.at(bm, bn, r, (int)sizeof(TO));
-          if constexpr (sizeof(TO) == 2) buf_store_bf16(o.rs, off, v);
-          else __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v), o.rs, off, 0, 0);
-        }
-    }
+  template <int TM, int TN>
+  __device__ __forceinline__ void operator()(const f32x16 (&acc)[TM][TN], const Tile &t) const {
+    TO *cc = c;
+    const long ld = ldc;
+    const float s = scale;
+    tile_apply(acc, t, [&](int m, int n, float v) { store_val(cc, (long)m * ld + n, v * s); });
   }
 };
 
@@ -94,20 +79,15 @@ struct EpiResid {
   const unsigned short *r;
   long ldr;
   float scale;
-  template <int T>
-  __device__ __forceinline__ void operator()(const f32x16 (&acc)[T][T], const Tile &t) const {
-    const EpiRows o(c, ldc, 2, t), i(r, ldr, 2, t);
-#pragma unroll
-    for (int bn = 0; bn < T; ++bn) {
-      if (t.column(bn) >= t.N) continue;
-#pragma unroll
-      for (int bm = 0; bm < T; ++bm)
-#pragma unroll
-        for (int rr = 0; rr < 16; ++rr) {
-          const unsigned short x = __builtin_amdgcn_raw_buffer_load_b16(i.rs, i.at(bm, bn, rr, 2), 0, 0);
-          buf_store_bf16(o.rs, o.at(bm, bn, rr, 2), bf_bits2f(x) + acc[bm][bn][rr] * scale);
-        }
-    }
+  template <int TM, int TN>
+  __device__ __forceinline__ void operator()(const f32x16 (&acc)[TM][TN], const Tile &t) const {
+    unsigned short *cc = c;
+    const unsigned short *rr = r;
+    const long ld = ldc, lr = ldr;
+    const float s = scale;
+    tile_apply(acc, t, [&](int m, int n, float v) {
+      cc[(long)m * ld + n] = f2bf_bits(bf_bits2f(rr[(long)m * lr + n]) + v * s);
+    });
   }
 };
 
@@ -116,22 +96,12 @@ struct EpiAccum {
   float *c;
   long ldc;
   float scale;
-  template <int T>
-  __device__ __forceinline__ void operator()(const f32x16 (&acc)[T][T], const Tile &t) const {
-    const EpiRows o(c, ldc, 4, t);
-#pragma unroll
-    for (int bn = 0; bn < T; ++bn) {
-      if (t.column(bn) >= t.N) continue;
-#pragma unroll
-      for (int bm = 0; bm < T; ++bm)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int off = o.at(bm, bn, r, 4);
-          const float x = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(o.rs, off, 0, 0));
-          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, x + acc[bm][bn][r] * scale),
-                                                o.rs, off, 0, 0);
-        }
-    }
+  template <int TM, int TN>
+  __device__ __forceinline__ void operator()(const f32x16 (&acc)[TM][TN], const Tile &t) const {
+    float *cc = c;
+    const long ld = ldc;
+    const float s = scale;
+    tile_apply(acc, t, [&](int m, int n, float v) { cc[(long)m * ld + n] += v * s; });
   }
 };
 
@@ -205,7 +175,7 @@ __global__ void __launch_bounds__(256, 2) k_gemm_nt(const unsigned short *__rest
     if (more) stash(buf ^ 1);
     __syncthreads();
   }
-  ep(acc, Tile{m0, n0, M, N, wm, wn, col, hh, 64});
+  ep(acc, Tile{m0, n0, M, N, wm * 64, wn * 64, col, hh, BM});
 }
 
 inline dim3 grid(int M, int N) { return dim3((unsigned)((N + BN - 1) / BN), (unsigned)((M + BM - 1) / BM)); }
@@ -222,16 +192,18 @@ constexpr int BIG_STAGE = 2 * BIG * BKB;  // bf16 elements of one stage (A then 
 // picks the half of the 256-byte bank line), so a fragment read of 32 rows x
 // 16 bytes is conflict-free.  A direct load writes 64 lanes x 16 bytes
 // = 8 rows in slot order; each lane fetches the chunk that belongs there.
+// The 8 waves of a block issue 4 such loads per operand and K step.
 struct BigFill {
-  int voff[8];   // byte offset of the lane's chunk in each of its 8 row groups
+  int voff[4];   // byte offset of the lane's chunk in each of its 4 row groups
   int kchunk;    // the lane's logical k chunk (0..7)
   __device__ __forceinline__ void init(int wave, int lane, long ld) {
     const int rr = lane >> 3, slot = lane & 7;
-    // (row >> 1) & 7 is the same for all 8 row groups (they start at multiples of 8)
-    kchunk = slot ^ (((wave * 8 + rr) >> 1) & 7);
+    // row group j*8 + wave starts at a multiple of 8 rows; (row >> 1) & 7
+    // depends only on the wave's parity and rr
+    kchunk = slot ^ ((((wave & 1) * 8 + rr) >> 1) & 7);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int row = (j * 4 + wave) * 8 + rr;
+    for (int j = 0; j < 4; ++j) {
+      const int row = (j * 8 + wave) * 8 + rr;
       voff[j] = (int)(row * ld * 2) + kchunk * 16;
     }
   }
@@ -242,9 +214,9 @@ struct BigFill {
 #if defined(__HIP_DEVICE_COMPILE__)
     const int add = k0 + kchunk * 8 < K ? k0 * 2 : 0x40000000;
 #pragma unroll
-    for (int j = 0; j < 8; ++j)
+    for (int j = 0; j < 4; ++j)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          rs, (__attribute__((address_space(3))) void *)(tile + (j * 4 + wave) * 8 * BKB), 16,
+          rs, (__attribute__((address_space(3))) void *)(tile + (j * 8 + wave) * 8 * BKB), 16,
           voff[j] + add, 0, 0, 0);
 #endif
   }
@@ -282,18 +254,10 @@ inline unsigned big_blocks(int M, int N) {
 }
 
 // Operand fragments of one 16-wide k slice: rows (w*128 + i*32 + col) of A and
-// B, 16 bytes each.
+// B, 16 bytes each (the transposed-operand kernel: 128 x 128 wave tiles).
 struct BigFrags {
   bf16x8 a[4], b[4];
 };
-
-__device__ __forceinline__ void big_load(BigFrags &f, const char *pa, const char *pb, int sw) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    f.a[i] = *reinterpret_cast<const bf16x8 *>(pa + i * 32 * 128 + sw);
-    f.b[i] = *reinterpret_cast<const bf16x8 *>(pb + i * 32 * 128 + sw);
-  }
-}
 
 __device__ __forceinline__ void big_mma(f32x16 (&acc)[4][4], const BigFrags &f) {
 #pragma unroll
@@ -302,15 +266,34 @@ __device__ __forceinline__ void big_mma(f32x16 (&acc)[4][4], const BigFrags &f) 
     for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(f.a[i], f.b[j], acc[i][j]);
 }
 
-// Scheduling of one slice: the eight fragment reads of the next slice are
-// spread over the sixteen products of this one (one per two), so their LDS latency
-// hides under the MFMA pipe (one wave per SIMD has no other wave to cover it).
-// The first slice of a step also carries the sixteen direct loads of the
-// next step.
-__device__ __forceinline__ void big_interleave(bool with_loads) {
+// NT kernel: a wave tile of 128 rows x 64 columns (8 waves, 2 x 4, two per
+// SIMD): per slice 4 A and 2 B fragments feed 8 products.
+struct NtFrags {
+  bf16x8 a[4], b[2];
+};
+
+__device__ __forceinline__ void nt_load(NtFrags &f, const char *pa, const char *pb, int sw) {
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    if (i % 2 == 0) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+  for (int i = 0; i < 4; ++i) f.a[i] = *reinterpret_cast<const bf16x8 *>(pa + i * 32 * 128 + sw);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) f.b[i] = *reinterpret_cast<const bf16x8 *>(pb + i * 32 * 128 + sw);
+}
+
+__device__ __forceinline__ void nt_mma(f32x16 (&acc)[4][2], const NtFrags &f) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = mfma32(f.a[i], f.b[j], acc[i][j]);
+}
+
+// Scheduling of one slice: the six fragment reads of the next slice ride
+// with the first six of its eight products, so their LDS latency hides under
+// the MFMA pipe; the first slice of a step also carries the eight direct
+// loads of the next step.
+__device__ __forceinline__ void nt_interleave(bool with_loads) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    if (i < 6) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
     if (with_loads) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // one global load
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
   }
@@ -320,35 +303,38 @@ __device__ __forceinline__ void big_interleave(bool with_loads) {
 // the end of K they read zeros into the idle buffer), then multiply slices
 // 0-2 of the current stage while reading slices 1-3.  f0 holds slice 0 on
 // entry; f1 holds slice 3 on exit.
-__device__ __forceinline__ void big_step(const unsigned short *__restrict__ rA,
-                                         const unsigned short *__restrict__ rB,
-                                         unsigned short *__restrict__ wA,
-                                         unsigned short *__restrict__ wB, const BigFill &fa,
-                                         const BigFill &fb, __amdgpu_buffer_rsrc_t ra,
-                                         __amdgpu_buffer_rsrc_t rb, int k_next, int K, int wave,
-                                         int offA, int offB, const int (&sw)[4], BigFrags &f0,
-                                         BigFrags &f1, f32x16 (&acc)[4][4]) {
+__device__ __forceinline__ void nt_step(const unsigned short *__restrict__ rA,
+                                        const unsigned short *__restrict__ rB,
+                                        unsigned short *__restrict__ wA,
+                                        unsigned short *__restrict__ wB, const BigFill &fa,
+                                        const BigFill &fb, __amdgpu_buffer_rsrc_t ra,
+                                        __amdgpu_buffer_rsrc_t rb, int k_next, int K, int wave,
+                                        int offA, int offB, const int (&sw)[4], NtFrags &f0,
+                                        NtFrags &f1, f32x16 (&acc)[4][2]) {
   fa.issue(wA, ra, k_next, K, wave);
   fb.issue(wB, rb, k_next, K, wave);
   const char *pa = reinterpret_cast<const char *>(rA) + offA;
   const char *pb = reinterpret_cast<const char *>(rB) + offB;
-  big_load(f1, pa, pb, sw[1]);
-  big_mma(acc, f0);
-  big_interleave(true);
-  big_load(f0, pa, pb, sw[2]);
-  big_mma(acc, f1);
-  big_interleave(false);
-  big_load(f1, pa, pb, sw[3]);
-  big_mma(acc, f0);
-  big_interleave(false);
+  nt_load(f1, pa, pb, sw[1]);
+  nt_mma(acc, f0);
+  nt_interleave(true);
+  nt_load(f0, pa, pb, sw[2]);
+  nt_mma(acc, f1);
+  nt_interleave(false);
+  nt_load(f1, pa, pb, sw[3]);
+  nt_mma(acc, f0);
+  nt_interleave(false);
 }
 
 // lda, ldb and K must be multiples of 8 and 256 * ld * 2 < 2^30; rows beyond
-// M / N and chunks beyond K read as zero.  Grid: big_blocks(M, N) x 256.
+// M / N and chunks beyond K read as zero.  Grid: big_blocks(M, N) x BIG_THREADS.
+constexpr int BIG_THREADS = 512;
+
 template <class Epi>
-__global__ void __launch_bounds__(256, 1) k_gemm_big(const unsigned short *__restrict__ A, long lda,
-                                                     const unsigned short *__restrict__ B, long ldb,
-                                                     int M, int N, int K, Epi ep) {
+__global__ void __launch_bounds__(BIG_THREADS, 1) k_gemm_big(const unsigned short *__restrict__ A,
+                                                             long lda,
+                                                             const unsigned short *__restrict__ B,
+                                                             long ldb, int M, int N, int K, Epi ep) {
   __shared__ __attribute__((aligned(1024))) unsigned short lds[2 * BIG_STAGE];
   const int nM = (M + BIG - 1) / BIG, nN = (N + BIG - 1) / BIG;
   int mt, nt;
@@ -356,7 +342,7 @@ __global__ void __launch_bounds__(256, 1) k_gemm_big(const unsigned short *__res
   const int m0 = mt * BIG, n0 = nt * BIG;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1, col = lane & 31, hh = lane >> 5;
+  const int wm = wave >> 2, wn = wave & 3, col = lane & 31, hh = lane >> 5;
 
   // each resource covers only the block's own rows (< 2^30 bytes), so the
   // offset of a chunk past K (+2^30) is out of range and reads zero
@@ -368,18 +354,18 @@ __global__ void __launch_bounds__(256, 1) k_gemm_big(const unsigned short *__res
   fa.init(wave, lane, lda);
   fb.init(wave, lane, ldb);
 
-  // fragment reads: row (w*128 + i*32 + col), logical chunk 2*kk + hh
+  // fragment reads: row (wave corner + i*32 + col), logical chunk 2*kk + hh
   const int sx = (col >> 1) & 7;
   int sw[4];
 #pragma unroll
   for (int kk = 0; kk < 4; ++kk) sw[kk] = ((2 * kk + hh) ^ sx) * 16;
-  const int offA = (wm * 128 + col) * 128, offB = (wn * 128 + col) * 128;
+  const int offA = (wm * 128 + col) * 128, offB = (wn * 64 + col) * 128;
 
-  f32x16 acc[4][4];
+  f32x16 acc[4][2];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
 
   unsigned short *s0 = lds, *s1 = lds + BIG_STAGE;
   const int nk = (K + BKB - 1) / BKB;
@@ -387,25 +373,25 @@ __global__ void __launch_bounds__(256, 1) k_gemm_big(const unsigned short *__res
   fb.issue(s0 + BIG * BKB, rb, 0, K, wave);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  BigFrags f0, f1;
-  big_load(f0, reinterpret_cast<const char *>(s0) + offA,
-           reinterpret_cast<const char *>(s0 + BIG * BKB) + offB, sw[0]);
+  NtFrags f0, f1;
+  nt_load(f0, reinterpret_cast<const char *>(s0) + offA,
+          reinterpret_cast<const char *>(s0 + BIG * BKB) + offB, sw[0]);
   for (int kt = 0; kt < nk; ++kt) {
     unsigned short *cur = (kt & 1) ? s1 : s0;
     unsigned short *nxt = (kt & 1) ? s0 : s1;
-    big_step(cur, cur + BIG * BKB, nxt, nxt + BIG * BKB, fa, fb, ra, rb, (kt + 1) * BKB, K, wave,
-             offA, offB, sw, f0, f1, acc);
+    nt_step(cur, cur + BIG * BKB, nxt, nxt + BIG * BKB, fa, fb, ra, rb, (kt + 1) * BKB, K, wave,
+            offA, offB, sw, f0, f1, acc);
     // every wave is done reading this stage and the next one has landed; the
     // last slice's products then cover the reads of the next stage's first
     // slice (after the last step they read the zero-filled idle buffer)
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    big_load(f0, reinterpret_cast<const char *>(nxt) + offA,
-             reinterpret_cast<const char *>(nxt + BIG * BKB) + offB, sw[0]);
-    big_mma(acc, f1);
-    big_interleave(false);
+    nt_load(f0, reinterpret_cast<const char *>(nxt) + offA,
+            reinterpret_cast<const char *>(nxt + BIG * BKB) + offB, sw[0]);
+    nt_mma(acc, f1);
+    nt_interleave(false);
   }
-  ep(acc, Tile{m0, n0, M, N, wm, wn, col, hh, 128});
+  ep(acc, Tile{m0, n0, M, N, wm * 128, wn * 64, col, hh, BIG});
 }
 
 // ------------------------------------------------- 256x256, transposed operands
@@ -593,7 +579,7 @@ __global__ void __launch_bounds__(256, 1) k_gemm_big_tn(const TnGroup<Epi, NP> g
     big_mma(acc, f1);
     big_interleave_tn(false);
   }
-  ep(acc, Tile{m0, n0, M, N, wm, wn, col, hh, 128});
+  ep(acc, Tile{m0, n0, M, N, wm * 128, wn * 128, col, hh, BIG});
 }
 
 inline int big_tiles(int M, int N) {
@@ -633,7 +619,7 @@ inline void gemm_launch(const unsigned short *A, long lda, const unsigned short 
                         int N, int K, const Epi &ep, hipStream_t st) {
   if (M <= 0 || N <= 0) return;
   if (gemm_use_big(M, N))
-    k_gemm_big<Epi><<<big_blocks(M, N), 256, 0, st>>>(A, lda, B, ldb, M, N, K, ep);
+    k_gemm_big<Epi><<<big_blocks(M, N), BIG_THREADS, 0, st>>>(A, lda, B, ldb, M, N, K, ep);
   else
     k_gemm_nt<Epi><<<grid(M, N), 256, 0, st>>>(A, lda, B, ldb, M, N, K, ep);
 }

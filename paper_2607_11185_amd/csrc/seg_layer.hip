@@ -237,11 +237,11 @@ __global__ void __launch_bounds__(256) k_rope(unsigned short *__restrict__ x, lo
 
 __device__ __forceinline__ float sigmoidf_(float g) { return 1.f / (1.f + __expf(-g)); }
 
-// Gate and up projections side by side: block j of 128 rows of wgu holds
-// wg rows 64j..64j+63 then wu rows 64j..64j+63 (zero rows past I), so one
-// GEMM against wgu gives, in each 128-column wave tile, the gate and up
-// values of the same 64 features.  Grid-stride over 16-byte chunks.
-constexpr int GU_BLOCK = 64;
+// Gate and up projections side by side: block j of 64 rows of wgu holds
+// wg rows 32j..32j+31 then wu rows 32j..32j+31 (zero rows past I), so one
+// GEMM against wgu gives, in each 64-column wave tile, the gate and up
+// values of the same 32 features.  Grid-stride over 16-byte chunks.
+constexpr int GU_BLOCK = 32;
 
 __global__ void k_interleave_gu(const unsigned short *__restrict__ wg,
                                 const unsigned short *__restrict__ wu, int I, int H, long rows2,
@@ -257,46 +257,35 @@ __global__ void k_interleave_gu(const unsigned short *__restrict__ wg,
   }
 }
 
-// Epilogue of the GEMM against wgu (256-wide tiles): m = silu(g) * u for the
-// wave's 64 features, in fp32 from the accumulators (acc[.][0..1] hold the
-// gate, acc[.][2..3] the up values of the same rows and features); with g and
-// u set, also stores the gate and up values (the backward's recompute).
+// Epilogue of the GEMM against wgu (the 256-wide NT kernel): m = silu(g) * u
+// for the wave's 32 features, in fp32 from the accumulators (acc[.][0] holds
+// the gate, acc[.][1] the up values of the same rows and features); with g
+// and u set, also stores the gate and up values (the backward's recompute).
 // Outputs are [rows][ld] bf16 at feature columns.
 struct EpiSwiGLU {
   unsigned short *m, *g, *u;
   long ld;
   int I;
-  template <int T>
-  __device__ __forceinline__ void operator()(const f32x16 (&acc)[T][T], const gemm::Tile &t) const {
-    static_assert(T == 4, "SwiGLU epilogue expects 128-column wave tiles");
-    const int f0 = (t.n0 + t.wn * t.wt) / 2;  // first feature of the wave
-    const int rows = t.M - t.m0 < 2 * t.wt ? t.M - t.m0 : 2 * t.wt;
-    const long base = (long)t.m0 * ld + f0;
-    const long span = (long)rows * ld * 2 - (long)f0 * 2;
-    const __amdgpu_buffer_rsrc_t rm = gemm::gemm_rsrc(m + base, span);
-    __amdgpu_buffer_rsrc_t rg = rm, ru = rm;
-    if (g) {
-      rg = gemm::gemm_rsrc(g + base, span);
-      ru = gemm::gemm_rsrc(u + base, span);
-    }
-    const int rowb = (int)(ld * 2);
-    const int lane = (t.wm * t.wt + 4 * t.hh) * rowb + t.col * 2;
+  template <int TM, int TN>
+  __device__ __forceinline__ void operator()(const f32x16 (&acc)[TM][TN],
+                                             const gemm::Tile &t) const {
+    static_assert(TN == 2, "SwiGLU epilogue expects 64-column wave tiles");
+    const int f = (t.n0 + t.wc) / 2 + t.col;  // the lane's feature
+    if (f >= I) return;
 #pragma unroll
-    for (int bn = 0; bn < 2; ++bn) {
-      if (f0 + bn * 32 + t.col >= I) continue;
+    for (int bm = 0; bm < TM; ++bm)
 #pragma unroll
-      for (int bm = 0; bm < T; ++bm)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float gv = acc[bm][bn][r], uv = acc[bm][bn + 2][r];
-          const int off = lane + (bm * 32 + 8 * (r >> 2) + (r & 3)) * rowb + bn * 64;
-          __builtin_amdgcn_raw_buffer_store_b16(f2bf_bits(gv * sigmoidf_(gv) * uv), rm, off, 0, 0);
-          if (g) {
-            __builtin_amdgcn_raw_buffer_store_b16(f2bf_bits(gv), rg, off, 0, 0);
-            __builtin_amdgcn_raw_buffer_store_b16(f2bf_bits(uv), ru, off, 0, 0);
-          }
+      for (int r = 0; r < 16; ++r) {
+        const int row = t.row(bm, r);
+        if (row >= t.M) continue;
+        const float gv = acc[bm][0][r], uv = acc[bm][1][r];
+        const long off = (long)row * ld + f;
+        m[off] = f2bf_bits(gv * sigmoidf_(gv) * uv);
+        if (g) {
+          g[off] = f2bf_bits(gv);
+          u[off] = f2bf_bits(uv);
         }
-    }
+      }
   }
 };
 
@@ -448,13 +437,14 @@ void build_wgu(const seg_layer_weights &w, int I, int H, unsigned short *wgu, hi
 }
 
 // rows x [gate | up] of a chunk against the interleaved weights, consumed by
-// the SwiGLU epilogue (always the 256-wide tiles: it pairs the two 64-column
-// halves of a 128-column wave tile)
+// the SwiGLU epilogue (always the 256-wide tiles: it pairs the two 32-column
+// halves of a 64-column wave tile)
 void gate_up(const unsigned short *a, const unsigned short *wgu, int rows, int H, int I,
              const EpiSwiGLU &ep, hipStream_t st) {
   const int N = 2 * ((I + GU_BLOCK - 1) / GU_BLOCK * GU_BLOCK);
   if (rows <= 0) return;
-  gemm::k_gemm_big<EpiSwiGLU><<<gemm::big_blocks(rows, N), 256, 0, st>>>(a, H, wgu, H, rows, N, H, ep);
+  gemm::k_gemm_big<EpiSwiGLU><<<gemm::big_blocks(rows, N), gemm::BIG_THREADS, 0, st>>>(
+      a, H, wgu, H, rows, N, H, ep);
   SEG_LAUNCH_CHECK();
 }
 

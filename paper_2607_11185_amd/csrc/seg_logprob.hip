@@ -38,20 +38,21 @@ struct EpiLogits {
   const int32_t *target;  // [N]
   float *ztgt;      // [N]
   float scale;
-  // for the 256-wide tiles: a wave covers one 128-row slab of M; the two lane
-  // halves of a column are combined by a shuffle
-  template <int T>
-  __device__ __forceinline__ void operator()(const f32x16 (&acc)[T][T], const gemm::Tile &t) const {
-    static_assert(T == 4, "logits epilogue expects 128-row wave tiles");
-    const int slab_row = t.m0 + t.wm * t.wt;
+  // for the 256-wide NT kernel: a wave covers one 128-row slab of M; the two
+  // lane halves of a column are combined by a shuffle
+  template <int TM, int TN>
+  __device__ __forceinline__ void operator()(const f32x16 (&acc)[TM][TN],
+                                             const gemm::Tile &t) const {
+    static_assert(TM == 4, "logits epilogue expects 128-row wave tiles");
+    const int slab_row = t.m0 + t.wr;
 #pragma unroll
-    for (int bn = 0; bn < T; ++bn) {
+    for (int bn = 0; bn < TN; ++bn) {
       const int n = t.column(bn);
       const bool nok = n < t.N;
       const int tgt = nok ? target[n] : -1;
       float mx = -INFINITY;
 #pragma unroll
-      for (int bm = 0; bm < T; ++bm)
+      for (int bm = 0; bm < TM; ++bm)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int m = t.row(bm, r);
@@ -66,7 +67,7 @@ struct EpiLogits {
       float sm = 0.f;
       if (mx != -INFINITY) {
 #pragma unroll
-        for (int bm = 0; bm < T; ++bm)
+        for (int bm = 0; bm < TM; ++bm)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int m = t.row(bm, r);
@@ -292,8 +293,8 @@ void logprob_impl(int rows, int H, int V, const TI *h, const int32_t *row_index,
   {
     EpiLogits e{zt, Rp, stats, rows, target, ztgt, cfg.logit_scale};
     ProfScope prof("logits", st);
-    gemm::k_gemm_big<EpiLogits><<<gemm::big_blocks(V, rows), 256, 0, st>>>(wb, H, hb, H, V, rows,
-                                                                          H, e);
+    gemm::k_gemm_big<EpiLogits><<<gemm::big_blocks(V, rows), gemm::BIG_THREADS, 0, st>>>(
+        wb, H, hb, H, V, rows, H, e);
     SEG_LAUNCH_CHECK();
   }
   // 2. per-row loss
