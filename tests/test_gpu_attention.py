@@ -92,7 +92,8 @@ def _segment_of_rows(ref, rows):
     return out
 
 
-@pytest.mark.parametrize("cfg", [WL.SMALL, WL.SEVEN_B], ids=lambda c: c.name)
+@pytest.mark.parametrize("cfg", [WL.SMALL, WL.SEVEN_B, WL.SEVEN_B_ANCHORED, WL.LONG],
+                         ids=lambda c: c.name)
 def test_full_size_sampled_rows_and_identities(cfg):
     """Full-size launch: O, LSE and dQ of sampled rows against the oracle
     computed row by row; dK and dV through exact identities of every segment
