@@ -576,7 +576,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the segmented path runs on a single MI355X and this "
-              "build has no multi-GPU code (run with --gpus 1).", file=sys.stderr)
+              "library has no multi-GPU code (run with --gpus 1).", file=sys.stderr)
         sys.exit(2)
 
     import torch

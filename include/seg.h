@@ -247,11 +247,12 @@ seg_status seg_logprob_loss(int32_t rows, int32_t hidden, int32_t vocab, seg_dty
 
 /*
  * One decoder layer of the language model around the segmented attention
- * (row f4 of the build: the policy update trains the language model on VCS
- * segments while the vision encoder stays fixed, App. E RL stage, so the
- * screenshot tokens enter as given hidden states).  The paper does not spell
- * the layer out; it is the pre-norm layer of the Qwen-style backbones it
- * trains, all matrices row-major, y = x W^T for a weight W [out, in]:
+ * (the policy update trains the language model on VCS segments while the
+ * vision encoder stays fixed, App. E RL stage, so the screenshot tokens enter
+ * as given hidden states).  The paper does not spell the layer out; this is a
+ * generic pre-norm Qwen-family layer (no projection biases, no per-head q/k
+ * norm, one-dimensional positions), all matrices row-major, y = x W^T for a
+ * weight W [out, in]:
  *   a = rms(x) * g1,  rms(x) = x / sqrt(mean(x^2) + rms_eps)
  *   q, k, v = a wq^T, a wk^T, a wv^T       ([P, hq, d], [P, hkv, d])
  *   q, k = rope(q), rope(k)                (rotate-half pairs (i, i + d/2) by

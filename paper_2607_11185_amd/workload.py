@@ -70,7 +70,7 @@ class Config:
         return dataclasses.replace(self, **kw)
 
 
-# The five workloads of the build (shapes of the paper's OSWorld/ScienceBoard
+# The workloads (shapes of the paper's OSWorld/ScienceBoard
 # style rollouts; 1920x1080 screenshots with 28-px merged patches give
 # round(1920/28) * round(1080/28) = 69 * 39 = 2691 image tokens).
 TINY = Config("tiny", 1, (8, 8), 64, 64, (32, 32), 8, 2, 4, 4, 1, 64, 128, 1024,
