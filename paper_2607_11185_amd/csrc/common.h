@@ -141,4 +141,22 @@ __host__ __device__ __forceinline__ int kperm(int p) {
   return (p & ~12) | ((p & 4) << 1) | ((p & 8) >> 1);
 }
 
+// dst[i] = value for i < n 32-bit words.  Compute entry points clear their
+// outputs with this kernel rather than hipMemsetAsync, so a caller can
+// capture them in a HIP graph and replay it.
+namespace {
+__global__ void __launch_bounds__(256) k_fill32(uint32_t *__restrict__ dst, long n, uint32_t value) {
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x)
+    dst[i] = value;
+}
+}  // namespace
+
+inline void fill32(void *dst, long n, uint32_t value, hipStream_t st) {
+  if (n <= 0) return;
+  const long blocks = (n + 255) / 256;
+  k_fill32<<<(unsigned)(blocks < 16384 ? blocks : 16384), 256, 0, st>>>(static_cast<uint32_t *>(dst), n,
+                                                                        value);
+  SEG_LAUNCH_CHECK();
+}
+
 }  // namespace seg

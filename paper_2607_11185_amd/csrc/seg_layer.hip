@@ -494,6 +494,19 @@ void rope(unsigned short *x, long P, int heads, int d, const int32_t *pos, float
   SEG_LAUNCH_CHECK();
 }
 
+void zero_grads(const seg_layer_grads &g, const seg_layer_cfg &c, hipStream_t st) {
+  const long H = c.hidden, I = c.inter, QD = (long)c.hq * c.d, KD = (long)c.hkv * c.d;
+  fill32(g.g1, H, 0u, st);
+  fill32(g.g2, H, 0u, st);
+  fill32(g.wq, QD * H, 0u, st);
+  fill32(g.wk, KD * H, 0u, st);
+  fill32(g.wv, KD * H, 0u, st);
+  fill32(g.wo, H * QD, 0u, st);
+  fill32(g.wg, I * H, 0u, st);
+  fill32(g.wu, I * H, 0u, st);
+  fill32(g.wd, H * I, 0u, st);
+}
+
 void check_status(seg_status s) {
   if (s != SEG_OK) throw Fail{s};
 }
@@ -575,15 +588,7 @@ void layer_bwd_impl(const seg_layout *L, const seg_sizes *sz, const seg_layer_cf
                        *y1 = CUS(sv.y1);
   {
     ProfScope prof("ly_misc", st);
-    SEG_HIP(hipMemsetAsync(gr.g1, 0, sizeof(float) * H, st));
-    SEG_HIP(hipMemsetAsync(gr.g2, 0, sizeof(float) * H, st));
-    SEG_HIP(hipMemsetAsync(gr.wq, 0, sizeof(float) * (size_t)m.QD * H, st));
-    SEG_HIP(hipMemsetAsync(gr.wk, 0, sizeof(float) * (size_t)m.KD * H, st));
-    SEG_HIP(hipMemsetAsync(gr.wv, 0, sizeof(float) * (size_t)m.KD * H, st));
-    SEG_HIP(hipMemsetAsync(gr.wo, 0, sizeof(float) * (size_t)H * m.QD, st));
-    SEG_HIP(hipMemsetAsync(gr.wg, 0, sizeof(float) * (size_t)I * H, st));
-    SEG_HIP(hipMemsetAsync(gr.wu, 0, sizeof(float) * (size_t)I * H, st));
-    SEG_HIP(hipMemsetAsync(gr.wd, 0, sizeof(float) * (size_t)H * I, st));
+    zero_grads(gr, c, st);
     positions(L, sz, P, pos, st);
     build_wgu(w, I, H, wgu, st);
     // transposed weights (k-contiguous operands of the data-gradient GEMMs)
@@ -721,17 +726,7 @@ extern "C" seg_status seg_layer_bwd(const seg_layout *L, const seg_sizes *sz,
     SEG_CHECK(g && g->g1 && g->wq && g->wk && g->wv && g->wo && g->g2 && g->wg && g->wu && g->wd,
               SEG_ERR_ARG, "a gradient pointer is NULL");
     if (sz->packed_tokens == 0) {
-      const seg_layer_cfg &c = *cfg;
-      const size_t H = c.hidden, I = c.inter, QD = (size_t)c.hq * c.d, KD = (size_t)c.hkv * c.d;
-      SEG_HIP(hipMemsetAsync(g->g1, 0, 4 * H, stream));
-      SEG_HIP(hipMemsetAsync(g->g2, 0, 4 * H, stream));
-      SEG_HIP(hipMemsetAsync(g->wq, 0, 4 * QD * H, stream));
-      SEG_HIP(hipMemsetAsync(g->wk, 0, 4 * KD * H, stream));
-      SEG_HIP(hipMemsetAsync(g->wv, 0, 4 * KD * H, stream));
-      SEG_HIP(hipMemsetAsync(g->wo, 0, 4 * H * QD, stream));
-      SEG_HIP(hipMemsetAsync(g->wg, 0, 4 * I * H, stream));
-      SEG_HIP(hipMemsetAsync(g->wu, 0, 4 * I * H, stream));
-      SEG_HIP(hipMemsetAsync(g->wd, 0, 4 * H * I, stream));
+      zero_grads(*g, *cfg, stream);
       return;
     }
     SEG_CHECK(x && saved && dy && dx && ws, SEG_ERR_ARG, "x, saved, dy, dx or ws is NULL");

@@ -289,7 +289,7 @@ void logprob_impl(int rows, int H, int V, const TI *h, const int32_t *row_index,
   }
   // 1. logits zT = s * W h^T with partial softmax stats; the target logit
   //    stays NaN for a target outside [0, vocab)
-  SEG_HIP(hipMemsetAsync(ztgt, 0xff, sizeof(float) * Rp, st));
+  fill32(ztgt, Rp, 0xffffffffu, st);
   {
     EpiLogits e{zt, Rp, stats, rows, target, ztgt, cfg.logit_scale};
     ProfScope prof("logits", st);
