@@ -17,7 +17,10 @@ device time of the two attention calls (the FlashAttention convention, 14*d
 with a 10*d backward that counts the recompute of S, is reported alongside as
 attn_tflops_fa_convention); `ms_per_step` and the trajectory token rates cover
 the whole step.  roofline.traffic is the counter-measured HBM bytes of one
-launch of the dominant kernel (see MEASURED_TRAFFIC).
+launch of the dominant kernel (see MEASURED_TRAFFIC).  For the 7B-class
+workloads the line also carries `layer`: the training step of one full
+decoder layer around the attention (2 timed steps), segmented and step-wise
+(`--no-layer` skips it; `--layer` runs it alone with its own options).
 """
 from __future__ import annotations
 
@@ -483,6 +486,10 @@ def layer_bench(cfg, steps, warmup, inter, groups, stepwise=True):
     """Training step of one full decoder layer around the segmented attention
     (forward + backward, all weight gradients) over the batch, segmented and
     step-wise.  One JSON line (not the bench line)."""
+    print(json.dumps(layer_result(cfg, steps, warmup, inter, groups, stepwise)), flush=True)
+
+
+def layer_result(cfg, steps, warmup, inter, groups, stepwise=True):
     import torch
     dev = torch.device("cuda:0")
     res = {}
@@ -517,7 +524,7 @@ def layer_bench(cfg, steps, warmup, inter, groups, stepwise=True):
     if stepwise:
         out["speedup_vs_stepwise"] = round(res["stepwise"]["ms_per_step"] /
                                            res["segmented"]["ms_per_step"], 3)
-    print(json.dumps(out), flush=True)
+    return out
 
 
 SWEEP_K = (1, 3, 5, 8, 10, 15)
@@ -571,6 +578,8 @@ def main():
                     help="training step of one full decoder layer (projections, RoPE, segmented "
                          "attention, SwiGLU MLP) segmented vs step-wise (one JSON line; not the "
                          "bench line)")
+    ap.add_argument("--no-layer", action="store_true",
+                    help="skip the decoder-layer measurement reported beside the bench line")
     ap.add_argument("--layer-inter", type=int, default=LAYER_INTER)
     ap.add_argument("--layer-groups", type=int, default=LAYER_GROUPS)
     args = ap.parse_args()
@@ -664,6 +673,22 @@ def main():
         out["reference_forward_speedup_vs_stepwise"] = round(ref_sw["total"] / ref_seg["total"], 3)
         sw.free()
         del sw
+        torch.cuda.empty_cache()
+
+    if not args.no_layer and cfg.hidden == 3584:
+        # one decoder layer around the attention (the next row past the hot
+        # path), segmented vs step-wise, reported beside the bench numbers
+        try:
+            lr = layer_result(cfg, 2, 1, LAYER_INTER, LAYER_GROUPS, not args.no_stepwise)
+            out["layer"] = {k: lr[k] for k in ("layer", "steps", "warmup", "speedup_vs_stepwise")
+                            if k in lr}
+            for k in ("segmented", "stepwise"):
+                if k in lr:
+                    out["layer"][k] = {n: lr[k][n] for n in ("packed_tokens", "ms_per_step",
+                                                             "traj_tokens_per_s", "layer_tflops",
+                                                             "gemm_tflops")}
+        except Exception as e:  # the bench line is reported either way
+            out["layer"] = {"error": f"{type(e).__name__}: {e}"}
         torch.cuda.empty_cache()
 
     if not args.no_cpu_baseline:
