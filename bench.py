@@ -356,7 +356,7 @@ class LayerRun:
     over the batch, forward and backward, in trajectory groups: each group is
     packed and run on its own (a micro-batch), all groups' inputs resident."""
 
-    def __init__(self, cfg, dev, inter, groups):
+    def __init__(self, cfg, dev, inter, groups, chunk=0):
         import numpy as np
         import torch
 
@@ -364,7 +364,7 @@ class LayerRun:
         from paper_2607_11185_amd import workload as WL
         self.S, self.cfg, self.dev = S, cfg, dev
         H, d = cfg.hidden, cfg.head_dim
-        self.lc = S.LayerCfg(H, inter, cfg.hq, cfg.hkv, d, 1e-6, 1e6, 16384)
+        self.lc = S.LayerCfg(H, inter, cfg.hq, cfg.hkv, d, 1e-6, 1e6, chunk)
         spans = WL.make_spans(cfg)
         bounds = np.linspace(0, spans.num_traj, groups + 1).round().astype(int)
         self.w = WL.layer_weights_torch(cfg.seed, H, inter, cfg.hq, cfg.hkv, d, dev)
@@ -482,14 +482,14 @@ def time_layer(run, steps, warmup):
     return ph, scopes
 
 
-def layer_bench(cfg, steps, warmup, inter, groups, stepwise=True):
+def layer_bench(cfg, steps, warmup, inter, groups, stepwise=True, chunk=0):
     """Training step of one full decoder layer around the segmented attention
     (forward + backward, all weight gradients) over the batch, segmented and
     step-wise.  One JSON line (not the bench line)."""
-    print(json.dumps(layer_result(cfg, steps, warmup, inter, groups, stepwise)), flush=True)
+    print(json.dumps(layer_result(cfg, steps, warmup, inter, groups, stepwise, chunk)), flush=True)
 
 
-def layer_result(cfg, steps, warmup, inter, groups, stepwise=True):
+def layer_result(cfg, steps, warmup, inter, groups, stepwise=True, chunk=0):
     import torch
     dev = torch.device("cuda:0")
     res = {}
@@ -498,7 +498,7 @@ def layer_result(cfg, steps, warmup, inter, groups, stepwise=True):
         cfgs.append(("stepwise", cfg.with_(name=cfg.name + "_stepwise", seg_steps=1,
                                            mode="sliding")))
     for label, c in cfgs:
-        run = LayerRun(c, dev, inter, groups)
+        run = LayerRun(c, dev, inter, groups, chunk)
         ph, scopes = time_layer(run, steps, warmup)
         gemm_ms = sum(scopes.get(n, 0.0) for n in ("ly_proj", "ly_mlp", "ly_wgrad"))
         attn_ms = sum(scopes.get(n, 0.0) for n in ("attn_prep", "attn_fwd", "attn_delta",
@@ -582,6 +582,8 @@ def main():
                     help="skip the decoder-layer measurement reported beside the bench line")
     ap.add_argument("--layer-inter", type=int, default=LAYER_INTER)
     ap.add_argument("--layer-groups", type=int, default=LAYER_GROUPS)
+    ap.add_argument("--layer-chunk", type=int, default=0,
+                    help="rows per projection / MLP chunk (0: the library default, 65536)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the segmented path runs on a single MI355X and this "
@@ -599,7 +601,7 @@ def main():
         return
     if args.layer:
         layer_bench(WL.CONFIGS[args.config], args.steps, args.warmup, args.layer_inter,
-                    args.layer_groups, not args.no_stepwise)
+                    args.layer_groups, not args.no_stepwise, args.layer_chunk)
         return
     if args.sweep:
         sweep(WL.CONFIGS[args.config], args.steps, args.warmup)

@@ -265,7 +265,7 @@ seg_status seg_logprob_loss(int32_t rows, int32_t hidden, int32_t vocab, seg_dty
  * bf16 storage, fp32 accumulation.  Padding rows: their outputs are
  * undefined and they contribute nothing to any gradient (dy there counts as
  * zero; dx there is 0).  Projections and the MLP run over chunks of
- * chunk_rows rows (0 = 32768; at most 2^20); weight gradients are summed over
+ * chunk_rows rows (0 = 65536; at most 2^20); weight gradients are summed over
  * the chunks in order, so results are bitwise reproducible.
  */
 typedef struct {

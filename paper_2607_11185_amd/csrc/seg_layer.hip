@@ -35,7 +35,7 @@ using gemm::k_transpose2d;
 
 constexpr int MAX_CH = 16;   // hidden <= 8 * 64 * MAX_CH
 constexpr int RMS_ROWS = 32; // rows per block of the norm backward
-constexpr int DEFAULT_CHUNK = 32768;     // rows per chunk when chunk_rows = 0
+constexpr int DEFAULT_CHUNK = 65536;     // rows per chunk when chunk_rows = 0
 constexpr int MAX_CHUNK = 1 << 20;       // GEMM rows are addressed with 32-bit offsets
 
 // ------------------------------------------------------------------ kernels
