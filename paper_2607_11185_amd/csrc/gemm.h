@@ -9,8 +9,7 @@
 //    steps of 64 fetched by direct buffer->LDS loads into two 64 KB stages;
 //    XCD-aware grouped tile order.
 //  - k_gemm_big_tn: the same block with transposed operands (both row-major
-//    over K), 4 waves of 128x128, fragments by transpose reads; up to three
-//    problems per launch.
+//    over K), fragments by transpose reads; up to three problems per launch.
 #pragma once
 
 #include "common.h"
@@ -253,21 +252,8 @@ inline unsigned big_blocks(int M, int N) {
   return (unsigned)((t + 7) / 8 * 8);
 }
 
-// Operand fragments of one 16-wide k slice: rows (w*128 + i*32 + col) of A and
-// B, 16 bytes each (the transposed-operand kernel: 128 x 128 wave tiles).
-struct BigFrags {
-  bf16x8 a[4], b[4];
-};
-
-__device__ __forceinline__ void big_mma(f32x16 (&acc)[4][4], const BigFrags &f) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = mfma32(f.a[i], f.b[j], acc[i][j]);
-}
-
-// NT kernel: a wave tile of 128 rows x 64 columns (8 waves, 2 x 4, two per
-// SIMD): per slice 4 A and 2 B fragments feed 8 products.
+// Both 256x256 kernels: a wave tile of 128 rows x 64 columns (8 waves, 2 x 4,
+// two per SIMD): per slice 4 A and 2 B fragments feed 8 products.
 struct NtFrags {
   bf16x8 a[4], b[2];
 };
@@ -408,22 +394,22 @@ typedef short gemm_v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) gemm_v4i16 gemm_lds_v4i16;
 
 struct BigFillT {
-  int voff[8];  // byte offset of the lane's chunk in each of its 8 row pairs
+  int voff[4];  // byte offset of the lane's chunk in each of its 4 row pairs
   __device__ __forceinline__ void init(int wave, int lane, long ld) {
     const int rr = lane >> 5, p = lane & 31;
-    // op j of a wave covers rows 2*(4j + wave) + {0, 1}; row & 3 = (2*wave + rr) & 3
+    // op j of a wave covers rows 2*(8j + wave) + {0, 1}; row & 3 = (2*wave + rr) & 3
     const int c = p ^ (4 * ((2 * wave + rr) & 3));
 #pragma unroll
-    for (int j = 0; j < 8; ++j) voff[j] = (int)((2 * (j * 4 + wave) + rr) * ld * 2) + c * 16;
+    for (int j = 0; j < 4; ++j) voff[j] = (int)((2 * (j * 8 + wave) + rr) * ld * 2) + c * 16;
   }
   // rs covers the step's rows (from k0) of the block's columns
   __device__ __forceinline__ void issue(unsigned short *__restrict__ tile,
                                         __amdgpu_buffer_rsrc_t rs, int wave) const {
 #if defined(__HIP_DEVICE_COMPILE__)
 #pragma unroll
-    for (int j = 0; j < 8; ++j)
+    for (int j = 0; j < 4; ++j)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          rs, (__attribute__((address_space(3))) void *)(tile + (j * 4 + wave) * 2 * BIG), 16,
+          rs, (__attribute__((address_space(3))) void *)(tile + (j * 8 + wave) * 2 * BIG), 16,
           voff[j], 0, 0, 0);
 #endif
   }
@@ -450,21 +436,22 @@ __device__ __forceinline__ bf16x8 tr_frag(const char *p) {
 
 // slice kk of the stage: rows 16*kk.. ; oa/ob: per-lane byte offsets of the
 // four 32-column blocks (row part included)
-__device__ __forceinline__ void big_load_tn(BigFrags &f, const char *pa, const char *pb,
-                                            const int (&oa)[4], const int (&ob)[4], int kk) {
+__device__ __forceinline__ void big_load_tn(NtFrags &f, const char *pa, const char *pb,
+                                            const int (&oa)[4], const int (&ob)[2], int kk) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    f.a[i] = tr_frag(pa + kk * 16 * 512 + oa[i]);
-    f.b[i] = tr_frag(pb + kk * 16 * 512 + ob[i]);
-  }
+  for (int i = 0; i < 4; ++i) f.a[i] = tr_frag(pa + kk * 16 * 512 + oa[i]);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) f.b[i] = tr_frag(pb + kk * 16 * 512 + ob[i]);
 }
 
+// the twelve transpose reads of the next slice ride with its eight products
 __device__ __forceinline__ void big_interleave_tn(bool with_loads) {
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS transpose read
+  for (int i = 0; i < 8; ++i) {
+    if (i < 4) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // two LDS reads
+    else __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);       // one LDS read
     if (with_loads) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // one global load
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                 // one MFMA
   }
 }
 
@@ -474,20 +461,20 @@ __device__ __forceinline__ void big_step_tn(const unsigned short *__restrict__ r
                                             unsigned short *__restrict__ wB, const BigFillT &fa,
                                             const BigFillT &fb, __amdgpu_buffer_rsrc_t ra,
                                             __amdgpu_buffer_rsrc_t rb, int wave, const int (&oa)[4],
-                                            const int (&ob)[4], BigFrags &f0, BigFrags &f1,
-                                            f32x16 (&acc)[4][4]) {
+                                            const int (&ob)[2], NtFrags &f0, NtFrags &f1,
+                                            f32x16 (&acc)[4][2]) {
   fa.issue(wA, ra, wave);
   fb.issue(wB, rb, wave);
   const char *pa = reinterpret_cast<const char *>(rA);
   const char *pb = reinterpret_cast<const char *>(rB);
   big_load_tn(f1, pa, pb, oa, ob, 1);
-  big_mma(acc, f0);
+  nt_mma(acc, f0);
   big_interleave_tn(true);
   big_load_tn(f0, pa, pb, oa, ob, 2);
-  big_mma(acc, f1);
+  nt_mma(acc, f1);
   big_interleave_tn(false);
   big_load_tn(f1, pa, pb, oa, ob, 3);
-  big_mma(acc, f0);
+  nt_mma(acc, f0);
   big_interleave_tn(false);
 }
 
@@ -507,7 +494,7 @@ struct TnGroup {
 // as zero); columns past M / N are computed from whatever the rows hold there
 // and dropped by the epilogue.  Grid: 8 * ceil(tiles / 8) x 256.
 template <class Epi, int NP>
-__global__ void __launch_bounds__(256, 1) k_gemm_big_tn(const TnGroup<Epi, NP> g, int K) {
+__global__ void __launch_bounds__(512, 1) k_gemm_big_tn(const TnGroup<Epi, NP> g, int K) {
   __shared__ __attribute__((aligned(1024))) unsigned short lds[2 * BIG_STAGE];
   const int idx = big_index(g.start[NP]);
   if (idx >= g.start[NP]) return;
@@ -534,28 +521,31 @@ __global__ void __launch_bounds__(256, 1) k_gemm_big_tn(const TnGroup<Epi, NP> g
   const int m0 = mt * BIG, n0 = nt * BIG;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 1, wn = wave & 1, col = lane & 31, hh = lane >> 5;
+  const int wm = wave >> 2, wn = wave & 3, col = lane & 31, hh = lane >> 5;
 
   BigFillT fa, fb;
   fa.init(wave, lane, lda);
   fb.init(wave, lane, ldb);
-  // transpose-read offsets: row 4*hh + (lane%16)/4, column
-  // w*128 + 32*i + 16*((lane/16)%2) + 4*(lane%4)
+  // transpose-read offsets: row 4*hh + (lane%16)/4 of the slice, column
+  // (wave corner) + 32*i + 16*((lane/16)%2) + 4*(lane%4)
   const int l16 = lane & 15, r = 4 * hh + (l16 >> 2), sx = 4 * (r & 3);
-  int oa[4], ob[4];
+  int oa[4], ob[2];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int ca = wm * 128 + 32 * i + 16 * ((lane >> 4) & 1) + 4 * (l16 & 3);
-    const int cb = wn * 128 + 32 * i + 16 * ((lane >> 4) & 1) + 4 * (l16 & 3);
     oa[i] = r * 512 + (((ca >> 3) ^ sx) << 4) + (ca & 7) * 2;
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int cb = wn * 64 + 32 * i + 16 * ((lane >> 4) & 1) + 4 * (l16 & 3);
     ob[i] = r * 512 + (((cb >> 3) ^ sx) << 4) + (cb & 7) * 2;
   }
 
-  f32x16 acc[4][4];
+  f32x16 acc[4][2];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
 
   unsigned short *s0 = lds, *s1 = lds + BIG_STAGE;
   const int nk = (K + BKB - 1) / BKB;
@@ -563,7 +553,7 @@ __global__ void __launch_bounds__(256, 1) k_gemm_big_tn(const TnGroup<Epi, NP> g
   fb.issue(s0 + BIG * BKB, tn_rsrc(Bt, ldb, 0, K, n0, N), wave);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  BigFrags f0, f1;
+  NtFrags f0, f1;
   big_load_tn(f0, reinterpret_cast<const char *>(s0), reinterpret_cast<const char *>(s0 + BIG * BKB),
               oa, ob, 0);
   for (int kt = 0; kt < nk; ++kt) {
@@ -576,10 +566,10 @@ __global__ void __launch_bounds__(256, 1) k_gemm_big_tn(const TnGroup<Epi, NP> g
     __syncthreads();
     big_load_tn(f0, reinterpret_cast<const char *>(nxt),
                 reinterpret_cast<const char *>(nxt + BIG * BKB), oa, ob, 0);
-    big_mma(acc, f1);
+    nt_mma(acc, f1);
     big_interleave_tn(false);
   }
-  ep(acc, Tile{m0, n0, M, N, wm * 128, wn * 128, col, hh, BIG});
+  ep(acc, Tile{m0, n0, M, N, wm * 128, wn * 64, col, hh, BIG});
 }
 
 inline int big_tiles(int M, int N) {
@@ -591,7 +581,7 @@ inline void gemm_launch_tn(TnGroup<Epi, NP> g, int K, hipStream_t st) {
   g.start[0] = 0;
   for (int q = 0; q < NP; ++q) g.start[q + 1] = g.start[q] + big_tiles(g.M[q], g.N[q]);
   if (g.start[NP] == 0) return;
-  k_gemm_big_tn<Epi, NP><<<(unsigned)((g.start[NP] + 7) / 8 * 8), 256, 0, st>>>(g, K);
+  k_gemm_big_tn<Epi, NP><<<(unsigned)((g.start[NP] + 7) / 8 * 8), 512, 0, st>>>(g, K);
 }
 
 template <class Epi>
