@@ -383,7 +383,7 @@ __global__ void __launch_bounds__(BIG_THREADS, 1) k_gemm_big(const unsigned shor
 // ------------------------------------------------- 256x256, transposed operands
 // C[m][n] = sum_k At[k][m] * Bt[k][n] with At [K][lda], Bt [K][ldb] row-major
 // (the weight gradients W^T-style: both operands run along the rows of a
-// chunk).  Tiles hold 64 k-rows x 256 columns (512 B per row); 16-byte chunk
+// chunk); lda and ldb are multiples of 8 with lda >= M and ldb >= N.  Tiles hold 64 k-rows x 256 columns (512 B per row); 16-byte chunk
 // c of row r sits in slot c ^ 4*(r & 3), so a 32-lane transpose read (4 rows x
 // 64 bytes) hits 16 distinct slots of the 64 banks.  Fragments come from
 // ds_read_b64_tr_b16 pairs: lane l gets column (l % 32) of rows
@@ -416,11 +416,14 @@ struct BigFillT {
 };
 
 // resource over rows [k0, min(K, k0 + 64)) of columns [c0, C) of a [K][ld]
-// matrix (zero rows past K; the last row stops at column C)
+// matrix (zero rows past K).  The last row stops at column C rounded up to
+// a 16-byte chunk, so the range never ends inside a chunk or a dword whose
+// first element is in range; ld is a multiple of 8 and every row holds ld
+// elements, so the rounded end stays inside the matrix.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t tn_rsrc(const unsigned short *X, long ld, int k0,
                                                          int K, int c0, int C) {
   const int rows = K - k0 < BKB ? K - k0 : BKB;
-  const long bytes = rows > 0 ? ((long)(rows - 1) * ld + (C - c0)) * 2 : 0;
+  const long bytes = rows > 0 ? ((long)(rows - 1) * ld + ((C - c0 + 7) & ~7)) * 2 : 0;
   return gemm_rsrc(X + (long)k0 * ld + c0, bytes);
 }
 

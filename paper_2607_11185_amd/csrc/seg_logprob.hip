@@ -213,7 +213,7 @@ __global__ void k_gather_rows(const TI *__restrict__ x, long ldx, const int32_t 
 }
 
 struct LpWs {
-  size_t hb, ht, wt, wb, zt, stats, ztgt, lse, g, dz, dzt, total;
+  size_t hb, wb, zt, stats, ztgt, lse, g, dz, dzt, total;
   int Rp, Vp, ntiles;
 };
 
@@ -230,8 +230,6 @@ LpWs lp_ws(int rows, int hidden, int vocab, seg_dtype dt) {
   };
   const size_t Rp = w.Rp, Vp = w.Vp, H = hidden;
   w.hb = take(Rp * H * 2);
-  w.ht = take(H * Rp * 2);
-  w.wt = take(H * Vp * 2);
   w.wb = dt == SEG_F32 ? take((size_t)vocab * H * 2) : 0;
   w.zt = take((size_t)vocab * Rp * 4);
   w.stats = take((size_t)w.ntiles * std::max(rows, 1) * sizeof(float2));
@@ -257,8 +255,6 @@ void logprob_impl(int rows, int H, int V, const TI *h, const int32_t *row_index,
                   const LpWs &L, hipStream_t st) {
   const int Rp = L.Rp, Vp = L.Vp;
   unsigned short *hb = reinterpret_cast<unsigned short *>(base + L.hb);
-  unsigned short *ht = reinterpret_cast<unsigned short *>(base + L.ht);
-  unsigned short *wt = reinterpret_cast<unsigned short *>(base + L.wt);
   float *zt = reinterpret_cast<float *>(base + L.zt);
   float2 *stats = reinterpret_cast<float2 *>(base + L.stats);
   float *ztgt = reinterpret_cast<float *>(base + L.ztgt);
@@ -313,26 +309,20 @@ void logprob_impl(int rows, int H, int V, const TI *h, const int32_t *row_index,
   k_dz<<<grid2(Rp, Vp), 256, 0, st>>>(zt, Rp, V, rows, Vp, Rp, lse, g, target, dz, dzt);
   SEG_LAUNCH_CHECK();
   }
-  // transposed operands: hT [H][Rp], Wt [H][Vp]
-  {
-  ProfScope prof("lp_prep", st);
-  k_transpose2d<unsigned short><<<grid2(H, Rp), 256, 0, st>>>(hb, H, nullptr, Rp, H, Rp, ht, Rp);
-  SEG_LAUNCH_CHECK();
-  k_transpose2d<unsigned short><<<grid2(H, Vp), 256, 0, st>>>(wb, H, nullptr, V, H, Vp, wt, Vp);
-  SEG_LAUNCH_CHECK();
-  }
-  // 4. dH = s * dz W  (M = rows, N = H, K = Vp)
+  // 4. dH = s * dz W = s (dz^T)^T W: the transposed-operand GEMM over the
+  //    vocabulary (At = dz^T [V][Rp], Bt = W [V][H]; M = rows, N = H, K = V)
   {
     EpiStore<TO> e{static_cast<TO *>(dh), H, cfg.logit_scale};
     ProfScope prof("dh", st);
-    gemm::gemm_launch(dz, Vp, wt, Vp, rows, H, Vp, e, st);
+    gemm::gemm_launch_tn(dzt, Rp, wb, H, rows, H, V, e, st);
     SEG_LAUNCH_CHECK();
   }
-  //    dW = s * dz^T h  (M = V, N = H, K = Rp)
+  //    dW = s * dz^T h over the rows (At = dz [Rp][Vp], Bt = h [Rp][H];
+  //    M = V, N = H, K = rows)
   {
     EpiStore<float> e{dw, H, cfg.logit_scale};
     ProfScope prof("dw", st);
-    gemm::gemm_launch(dzt, Rp, ht, Rp, V, H, Rp, e, st);
+    gemm::gemm_launch_tn(dz, Vp, hb, H, V, H, rows, e, st);
     SEG_LAUNCH_CHECK();
   }
 }

@@ -66,8 +66,10 @@ def _full_case(cfg, dual=0.0, want_grad=True, kl=None):
     return run, ref, out, old
 
 
-@pytest.mark.parametrize("cfg,dual", [(WL.TINY, 0.0), (WL.SMALL, 0.0), (WL.SMALL, 1.15)],
-                         ids=["tiny", "small", "small_dualclip"])
+@pytest.mark.parametrize("cfg,dual", [(WL.TINY, 0.0), (WL.SMALL, 0.0), (WL.SMALL, 1.15),
+                                     (WL.TINY.with_(vocab=1001, action_len=5, steps=(7, 7), old_noise_std=0.3,
+                                                  seed=5), 0.0)],
+                         ids=["tiny", "small", "small_dualclip", "tiny_odd_vocab_rows"])
 def test_full_parity(cfg, dual):
     say(f"logprob {cfg.name} dual={dual}")
     run, ref, out, old = _full_case(cfg, dual)
@@ -90,6 +92,14 @@ def test_full_parity(cfg, dual):
     e_dw = rel(out["dw"].cpu().numpy(), ref["dw"])
     say(f"  dh {e_dh:.2e} dw {e_dw:.2e}")
     assert e_dh < TOL and e_dw < TOL
+    # the last row of dh and the last vocabulary row of dW sit in the ragged
+    # tails of the gradient GEMMs (output edge and reduction edge)
+    dh = out["dh"][:R].float().cpu().numpy()
+    dw = out["dw"].cpu().numpy()
+    for i in (0, R - 1):
+        assert rel(dh[i], ref["dh"][i]) < TOL, ("dh row", i)
+    for v in (0, dw.shape[0] - 1):
+        assert rel(dw[v], ref["dw"][v]) < TOL, ("dw row", v)
 
 
 @pytest.mark.parametrize("cfg,kl", [(WL.TINY, 0.5), (WL.SMALL, 0.5), (WL.SMALL, 1e-4)],
