@@ -23,8 +23,6 @@ namespace seg {
 namespace {
 
 using gemm::EpiStore;
-using gemm::k_gemm_nt;
-using gemm::k_transpose2d;
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
 
