@@ -368,8 +368,8 @@ extern "C" seg_status seg_logprob_loss(int32_t rows, int32_t hidden, int32_t voc
               ws_bytes, L.total);
     SEG_CHECK(loss_sum != nullptr, SEG_ERR_ARG, "loss_sum is NULL");
     if (rows == 0) {
-      SEG_HIP(hipMemsetAsync(loss_sum, 0, sizeof(float), stream));
-      if (cfg->want_grad && dw) SEG_HIP(hipMemsetAsync(dw, 0, sizeof(float) * (size_t)vocab * hidden, stream));
+      fill32(loss_sum, 1, 0u, stream);
+      if (cfg->want_grad && dw) fill32(dw, (long)vocab * hidden, 0u, stream);
       return;
     }
     SEG_CHECK(h && w && target && old_logp && adv && row_traj && logp && loss_tok && clipped && ws,

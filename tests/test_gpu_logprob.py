@@ -175,3 +175,25 @@ def test_seven_b_full_rows_sampled():
     assert rel(out["dh"][torch.from_numpy(sel).cuda()].float().cpu().numpy(), ref["dh"]) < TOL
     dw = out["dw"].double()
     assert float(dw.sum(0).norm()) < TOL * float(dw.norm())
+
+
+def test_no_loss_rows():
+    """A batch without action rows: zero loss and a zero weight gradient
+    (the outputs are cleared by a kernel, so this also holds under graph
+    capture)."""
+    import torch
+    dev = "cuda"
+    H, V = 64, 300
+    h = torch.randn(5, H, device=dev).to(torch.bfloat16)
+    w = torch.randn(V, H, device=dev).to(torch.bfloat16)
+    e32 = torch.empty(0, dtype=torch.int32, device=dev)
+    ef = torch.empty(0, dtype=torch.float32, device=dev)
+    out = {"logp": torch.empty(1, device=dev), "loss_tok": torch.empty(1, device=dev),
+           "clipped": torch.empty(1, dtype=torch.uint8, device=dev),
+           "kl_tok": torch.empty(1, device=dev), "loss_sum": torch.full((1,), 7.0, device=dev),
+           "dh": torch.empty((1, H), dtype=torch.bfloat16, device=dev),
+           "dw": torch.full((V, H), 7.0, device=dev)}
+    S.seg_logprob_loss(h, e32, w, e32, ef, torch.zeros(1, device=dev), e32, S.LossCfg(), out=out)
+    torch.cuda.synchronize()
+    assert float(out["loss_sum"][0]) == 0.0
+    assert torch.count_nonzero(out["dw"]).item() == 0
