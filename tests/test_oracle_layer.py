@@ -181,3 +181,41 @@ def test_forward_rows_matches_forward():
         rows = np.array([0, sg.length // 2, sg.length - 1])
         ys = OLY.forward_rows(x[sg.start:sg.start + sg.length], w, m, rows, **a)
         np.testing.assert_allclose(ys, y[sg.start + rows], rtol=1e-12, atol=1e-12)
+
+
+def test_layer_forward_matches_torch_composition():
+    """The whole forward against the same layer composed from library
+    primitives on the CPU in float64: torch's RMS normalisation formula,
+    rotary embedding as a complex multiplication of (x_i + i x_{i+d/2}) by
+    e^{i theta}, scaled_dot_product_attention with the boolean visibility
+    mask and kv heads repeated per group, and F.silu for the MLP."""
+    import torch
+    import torch.nn.functional as F
+    lay, x, w, masks, a = _tiny(seed=7, hq=6, hkv=2, d=8)
+    y_o, _ = OLY.forward(x, w, lay.segments, masks, **a)
+    hq, hkv, d, eps, base = a["hq"], a["hkv"], a["d"], a["eps"], a["base"]
+    T = {n: torch.from_numpy(np.asarray(v)) for n, v in w.__dict__.items()}
+    for sg, m in zip(lay.segments, masks):
+        xs = torch.from_numpy(x[sg.start:sg.start + sg.length])
+        n = xs.shape[0]
+        an = xs * torch.rsqrt(xs.pow(2).mean(-1, keepdim=True) + eps) * T["g1"]
+        q = (an @ T["wq"].T).view(n, hq, d)
+        k = (an @ T["wk"].T).view(n, hkv, d)
+        v = (an @ T["wv"].T).view(n, hkv, d)
+        inv = base ** (-torch.arange(0, d, 2, dtype=torch.float64) / d)
+        rot = torch.polar(torch.ones(n, d // 2, dtype=torch.float64),
+                          torch.arange(n, dtype=torch.float64)[:, None] * inv[None, :])
+
+        def rope(t):
+            z = torch.complex(t[..., : d // 2], t[..., d // 2:]) * rot[:, None, :]
+            return torch.cat([z.real, z.imag], dim=-1)
+
+        qh = rope(q).transpose(0, 1)
+        kh = rope(k).transpose(0, 1).repeat_interleave(hq // hkv, dim=0)
+        vh = v.transpose(0, 1).repeat_interleave(hq // hkv, dim=0)
+        o = F.scaled_dot_product_attention(qh, kh, vh, attn_mask=torch.from_numpy(m))
+        y1 = xs + o.transpose(0, 1).reshape(n, hq * d) @ T["wo"].T
+        b = y1 * torch.rsqrt(y1.pow(2).mean(-1, keepdim=True) + eps) * T["g2"]
+        y = y1 + (F.silu(b @ T["wg"].T) * (b @ T["wu"].T)) @ T["wd"].T
+        np.testing.assert_allclose(y_o[sg.start:sg.start + sg.length], y.numpy(),
+                                   rtol=1e-10, atol=1e-10)
