@@ -687,14 +687,19 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
   auto ds_side = [&](const int b, const int pb) __attribute__((always_inline)) {
     const char *cQ = reinterpret_cast<const char *>(sQ[b]);
     const char *cD = reinterpret_cast<const char *>(sD[b]);
+    f32x16 dpb[2];
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
       bf16x8 ad[KK];
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) ad[kk] = frag_row<D>(cD, qb * 32, lo.row[kk]);
-      f32x16 dp = f32x16{};
+      dpb[qb] = f32x16{};
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) dp = mfma32(ad[kk], xf[kk], dp);
+      for (int kk = 0; kk < KK; ++kk) dpb[qb] = mfma32(ad[kk], xf[kk], dpb[qb]);
+    }
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      f32x16 dp = dpb[qb];
       const bf16x8 *psrc = reinterpret_cast<const bf16x8 *>(sP[pb]) + ((qb * 4 + kg) * 2) * 64 + lane;
       const bf16x8 p0 = psrc[0], p1 = psrc[64];
 #pragma unroll
