@@ -31,6 +31,10 @@ CASES = {
     "med_anchored_k2_d3": MED.with_(mode="anchored", window=2, seg_steps=3, seed=13, steps=(8, 11)),
     "med_anchored_k1_d1_d64": MED.with_(mode="anchored", window=1, seg_steps=1, hq=8, hkv=2,
                                         head_dim=64, seed=14),
+    # segments of exactly 5 and 5.5 tiles (640 and 704 rows): no ragged rows,
+    # and a last tile that is exactly one 64-row half
+    "exact_tiles": MED.with_(steps=(4, 8), prompt_len=128, img_len=64, text_len=(64, 64),
+                             action_len=8, window=4, seg_steps=4, seed=15),
     "tiny": WL.TINY,
 }
 
