@@ -86,3 +86,31 @@ def forward_generic(q, k, v, mask, scale):
         o[:, h, :] = (p / tot) @ v[:, g, :]
         lse[h] = (m + np.log(tot))[:, 0]
     return o, lse
+
+
+def key_grads(q, k, v, mask, scale, dout, keys):
+    """dK and dV of the keys ``keys`` only, from query rows ``q`` [r, hq, d]
+    with their mask rows [r, n] over all n keys k, v [n, hkv, d] and their
+    dout [r, hq, d].  Each row's softmax (its max, sum and so its LSE) and
+    Delta = dout . O are taken over every key the row sees; a key's gradient
+    is the sum over the given rows, so rows that do not see the keys may be
+    left out, and disjoint row sets add up (the backward definitions above,
+    restricted to a few columns of P and dS)."""
+    r, hq, d = q.shape
+    hkv = k.shape[1]
+    keys = np.asarray(keys)
+    dk = np.zeros((len(keys), hkv, d), np.float64)
+    dv = np.zeros((len(keys), hkv, d), np.float64)
+    for h in range(hq):
+        g = _kv_head(h, hq, hkv)
+        s = scale * (q[:, h, :] @ k[:, g, :].T)
+        s = np.where(mask, s, -np.inf)
+        p = np.exp(s - s.max(axis=1, keepdims=True))
+        p = p / p.sum(axis=1, keepdims=True)
+        delta = (dout[:, h, :] * (p @ v[:, g, :])).sum(axis=1)
+        pk = p[:, keys]
+        dpk = dout[:, h, :] @ v[keys, g, :].T
+        dsk = pk * (dpk - delta[:, None])
+        dv[:, g, :] += pk.T @ dout[:, h, :]
+        dk[:, g, :] += scale * (dsk.T @ q[:, h, :])
+    return dk, dv

@@ -271,6 +271,8 @@ def build(spans, W, L, tile, cap=0, buffer_tokens=0, with_tiles=True,
                 c, k, s = segment_tokens(p, img, text, W, a, b, canon_off[t])
             else:
                 c, k, s = segment_tokens_with(p, img, text, images, b, canon_off[t])
+            if len(c) == 0:
+                raise ValueError(f"segment of trajectory {t}, turns {a}..{b - 1} holds no token")
             if buffer_tokens and len(c) > buffer_tokens:
                 raise CapacityError(f"segment of {len(c)} tokens exceeds the buffer")
             segs.append(Segment(t, a, b, -1, c, k, s))
@@ -310,6 +312,9 @@ def build(spans, W, L, tile, cap=0, buffer_tokens=0, with_tiles=True,
             xj = np.nonzero((sg.kind == KIND_TEXT) & (sg.step == j))[0]
             nact = int(act[j - 1])
             for i in (xj[len(xj) - nact:] if nact else []):
+                if i == 0:
+                    # pi(a_t | x_<t) needs a row before the token (Eq. loss)
+                    raise ValueError(f"turn {j}: a trained token opens its segment")
                 pred.append(sg.start + int(i) - 1)
                 tgt.append(int(sg.canon[i]))
                 trj.append(sg.traj)

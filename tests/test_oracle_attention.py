@@ -106,6 +106,37 @@ def test_backward_matches_autograd():
     assert np.allclose(dv, tv.grad.numpy(), atol=1e-10)
 
 
+def test_key_grads_match_autograd_on_row_subsets():
+    """dK/dV of a few keys from only the rows that see them, split into two
+    disjoint row sets and summed, equal torch autograd's full gradients at
+    those keys (and the screenshot keys' rows exclude expired turns)."""
+    sg, mask = _segment(W=1, L=4, seed=11)
+    rng = np.random.default_rng(4)
+    hq, hkv, d = 6, 2, 8
+    q, k, v = _seg_inputs(rng, sg.length, hq, hkv, d)
+    dout = rng.standard_normal((sg.length, hq, d))
+    scale = 1 / math.sqrt(d)
+    tq = torch.tensor(q, requires_grad=True)
+    tk = torch.tensor(k, requires_grad=True)
+    tv = torch.tensor(v, requires_grad=True)
+    rep = hq // hkv
+    o = torch.nn.functional.scaled_dot_product_attention(
+        tq.permute(1, 0, 2), tk.repeat_interleave(rep, 1).permute(1, 0, 2),
+        tv.repeat_interleave(rep, 1).permute(1, 0, 2), attn_mask=torch.tensor(mask),
+        scale=scale).permute(1, 0, 2)
+    (o * torch.tensor(dout)).sum().backward()
+    keys = np.nonzero(sg.kind == OL.KIND_IMAGE)[0][:3]
+    rows = np.nonzero(mask[:, keys].any(1))[0]
+    assert 0 < len(rows) < sg.length - keys.min()    # the window hides them from later turns
+    half = len(rows) // 2
+    parts = [OA.key_grads(q[r], k, v, mask[r], scale, dout[r], keys)
+             for r in (rows[:half], rows[half:])]
+    dk = parts[0][0] + parts[1][0]
+    dv = parts[0][1] + parts[1][1]
+    assert np.allclose(dk, tk.grad.numpy()[keys], atol=1e-10)
+    assert np.allclose(dv, tv.grad.numpy()[keys], atol=1e-10)
+
+
 def test_backward_finite_differences():
     sg, mask = _segment(W=1, L=3, seed=9)
     rng = np.random.default_rng(4)

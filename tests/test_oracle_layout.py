@@ -313,3 +313,23 @@ def test_anchored_visibility_is_causal_and_trains_every_action_once():
     assert len(set(lay.loss_tgt_src.tolist())) == T
     with pytest.raises(ValueError):
         OL.build(sp, 3, 2, 4, cap=100, mode="anchored")
+
+
+def test_empty_prompt():
+    """A trajectory without a prompt opens its first segment with turn 1's
+    screenshot; later turns stop seeing it once it leaves the window.  A
+    segment without tokens, and a trained token opening its segment (no row
+    before it predicts it, Eq. loss), are argument errors."""
+    sp = WL.explicit_spans([3], [0], [2, 2, 2], [2, 2, 2], [1, 1, 1])
+    lay = OL.build(sp, 1, 3, 4)
+    sg = lay.segments[0]
+    assert sg.length == 12 and sg.kind[0] == OL.KIND_IMAGE and sg.canon[0] == 0
+    m = OL.visibility(sg, 1)
+    later = np.nonzero(sg.step >= 2)[0]
+    assert not m[later][:, :2].any()          # turn 1's screenshot has expired
+    assert m[later][:, 2:4].all()             # turn 1's text has not
+    assert lay.loss_pred_row.tolist() == [2, 6, 10]
+    with pytest.raises(ValueError):           # turn 1 is all trained text
+        OL.build(WL.explicit_spans([2], [0], [0, 1], [2, 2], [2, 1]), 1, 1, 4)
+    with pytest.raises(ValueError):           # turn 1 has no token at all
+        OL.build(WL.explicit_spans([2], [0], [0, 1], [0, 2], [0, 1]), 1, 1, 4)
