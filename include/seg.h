@@ -147,7 +147,6 @@ typedef struct {
   uint8_t *kt_cls;        /* [Z] */
   int64_t *seg_pairs;     /* [S] exact visible (query, key) pairs of each segment */
   int64_t *tile_nnz;      /* [1] non-skipped tiles */
-  int32_t *work_order;    /* [G] tiles by decreasing CSR row length (ties: ascending index) */
   int32_t window;         /* set by seg_build_layout: the visibility window the
                              attention kernels apply (W; SEG_WINDOW_ANCHORED,
                              larger than any turn index, in the anchored mode) */
@@ -319,7 +318,10 @@ seg_status seg_layer_bwd(const seg_layout *L, const seg_sizes *sz, const seg_lay
  * "logits", "row_loss", "dz", "lp_prep", "dh", "dw", and for the layer
  * "ly_norm", "ly_rope", "ly_proj", "ly_mlp", "ly_wgrad", "ly_misc"), waiting for them to
  * finish; seg_profile_reset forgets the records.  Timing adds two event
- * records per launch and is off by default.
+ * records per launch and is off by default.  These three calls are the one
+ * place with process-wide state (an atomic enable flag and a mutex-guarded
+ * record list shared by all threads and devices); with timing off a launch
+ * only reads the flag.
  */
 void seg_profile_enable(int32_t on);
 void seg_profile_reset(void);

@@ -56,7 +56,7 @@ class SegLayout(ctypes.Structure):
     _fields_ = [("seg_info", VP), ("tok_src", VP), ("tok_meta", VP), ("loss_pred_row", VP),
                 ("loss_tgt_src", VP), ("loss_traj", VP), ("tile_seg", VP), ("qt_ptr", VP),
                 ("qt_col", VP), ("qt_cls", VP), ("kt_ptr", VP), ("kt_row", VP), ("kt_cls", VP),
-                ("seg_pairs", VP), ("tile_nnz", VP), ("work_order", VP),
+                ("seg_pairs", VP), ("tile_nnz", VP),
                 ("window", ctypes.c_int32), ("tile", ctypes.c_int32)]
 
 

@@ -358,8 +358,8 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd(
     const unsigned short *__restrict__ v, const int32_t *__restrict__ seg_info,
     const int32_t *__restrict__ tile_seg, const int32_t *__restrict__ tok_meta,
     const int32_t *__restrict__ qt_ptr, const int32_t *__restrict__ qt_col,
-    const uint8_t *__restrict__ qt_cls, const int32_t *__restrict__ work_order, int ntiles, int hq,
-    int hkv, int W, float scale_log2, long P, TO *__restrict__ o, float *__restrict__ lse) {
+    const uint8_t *__restrict__ qt_cls, int ntiles, int hq, int hkv, int W, float scale_log2,
+    long P, TO *__restrict__ o, float *__restrict__ lse) {
   constexpr int KK = D / 16, DB = D / 32, T64 = 64 * D;
   __shared__ __attribute__((aligned(16))) unsigned short sK0[T64], sK1[T64], sV0[T64], sV1[T64];
   __shared__ __attribute__((aligned(16))) int sM0[64], sM1[64];
@@ -445,8 +445,10 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd(
     // tile max exceeds it by more than 8, so unnormalised P stays below 2^8.
     const bool grow = mloc > m_run + 8.f;
     if (__any(grow)) {
+      // lanes that keep their max keep alpha = 1: with an unset (-inf) max,
+      // exp2(m_run - m_new) would be exp2(NaN)
       const float m_new = grow ? mloc : m_run;
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      const float alpha = grow ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.f;
       l_run *= alpha;
 #pragma unroll
       for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
@@ -611,7 +613,7 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
                                                           : (const void *)(tok_meta + tr.start),
                                               wave < 2 ? pbytes : (unsigned)tr.len * 4);
   u16x8 stq[PW], sto[PW];
-  int stv = 0;
+  int stv = 0, st_vrows = 0;
   auto load = [&](int r0, int vrows, int hi) __attribute__((always_inline)) {
     const int so = r0 * qrow_bytes + hi * D * 2;
 #pragma unroll
@@ -619,16 +621,23 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
       stq[i] = __builtin_bit_cast(u16x8, __builtin_amdgcn_raw_buffer_load_b128(rQ, voff[i], so, 0));
       sto[i] = __builtin_bit_cast(u16x8, __builtin_amdgcn_raw_buffer_load_b128(rO, voff[i], so, 0));
     }
+    // The per-row resource of a head spans the following rows of the packed
+    // batch (other segments, or buffer padding whose log-sum-exp and Delta
+    // were never computed): rows past the unit's valid rows are replaced by
+    // zeros when stored, so no non-finite value can reach dS = P (dP - Delta)
+    // through a masked P = 0.
     if (wave < 3)
       stv = __builtin_amdgcn_raw_buffer_load_b32(rS, lane * 4,
                                                  (wave < 2 ? hi * (int)P * 4 : 0) + r0 * 4, 0);
+    st_vrows = vrows;
   };
   auto store = [&](int b) __attribute__((always_inline)) {
     sp.store(sQ[b], stq, wave, lane);
     sp.store(sD[b], sto, wave, lane);
-    if (wave == 0) sL[b][lane] = __builtin_bit_cast(float, stv);
-    else if (wave == 1) sE[b][lane] = __builtin_bit_cast(float, stv);
-    else if (wave == 2) sM[b][lane] = stv;
+    const int val = lane < st_vrows ? stv : 0;
+    if (wave == 0) sL[b][lane] = __builtin_bit_cast(float, val);
+    else if (wave == 1) sE[b][lane] = __builtin_bit_cast(float, val);
+    else if (wave == 2) sM[b][lane] = val;
   };
 
   // P side: one unit (rows r0 .. r0 + vrows - 1, PARTIAL or ragged if masked)
@@ -834,9 +843,8 @@ __global__ void __launch_bounds__(256, 2) k_attn_bwd_dq(
     const float *__restrict__ lse2, const float *__restrict__ delta,
     const int32_t *__restrict__ seg_info, const int32_t *__restrict__ tile_seg,
     const int32_t *__restrict__ tok_meta, const int32_t *__restrict__ qt_ptr,
-    const int32_t *__restrict__ qt_col, const uint8_t *__restrict__ qt_cls,
-    const int32_t *__restrict__ work_order, int ntiles, int hq, int hkv, int W,
-    float scale_log2, float scale, long P, TO *__restrict__ dq) {
+    const int32_t *__restrict__ qt_col, const uint8_t *__restrict__ qt_cls, int ntiles, int hq,
+    int hkv, int W, float scale_log2, float scale, long P, TO *__restrict__ dq) {
   constexpr int KK = D / 16, DB = D / 32, T64 = 64 * D;
   __shared__ __attribute__((aligned(16))) unsigned short sK0[T64], sK1[T64], sV0[T64], sV1[T64];
   __shared__ __attribute__((aligned(16))) int sM0[64], sM1[64];
@@ -1044,8 +1052,7 @@ void fwd_impl(const seg_layout *L, const seg_sizes *sz, int hq, int hkv, float s
   ProfScope prof("attn_fwd", st);
   k_attn_fwd<D, TO><<<xcd_grid(G, hq), 256, 0, st>>>(
       q, k, v, L->seg_info, L->tile_seg, L->tok_meta, L->qt_ptr, L->qt_col, L->qt_cls,
-      L->work_order, G, hq, hkv, L->window, scale * LOG2E, sz->packed_tokens, static_cast<TO *>(o),
-      lse);
+      G, hq, hkv, L->window, scale * LOG2E, sz->packed_tokens, static_cast<TO *>(o), lse);
   SEG_LAUNCH_CHECK();
 }
 
@@ -1075,8 +1082,7 @@ void bwd_impl(const seg_layout *L, const seg_sizes *sz, int hq, int hkv, float s
   ProfScope prof("attn_bwd_dq", st);
   k_attn_bwd_dq<D, TO><<<xcd_grid(G, hq), 256, 0, st>>>(
       q, k, v, dout, lse2, delta, L->seg_info, L->tile_seg, L->tok_meta, L->qt_ptr, L->qt_col,
-      L->qt_cls, L->work_order, G, hq, hkv, L->window, scale * LOG2E, scale, P,
-      static_cast<TO *>(dq));
+      L->qt_cls, G, hq, hkv, L->window, scale * LOG2E, scale, P, static_cast<TO *>(dq));
   SEG_LAUNCH_CHECK();
 }
 

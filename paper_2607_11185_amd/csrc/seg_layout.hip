@@ -110,7 +110,7 @@ void validate(const seg_problem *p) {
   for (int t = 0; t < p->num_traj; ++t) {
     SEG_CHECK(p->step_offsets[t + 1] >= p->step_offsets[t], SEG_ERR_ARG,
               "step_offsets must be non-decreasing (trajectory %d)", t);
-    SEG_CHECK(p->prompt_len[t] >= 1, SEG_ERR_ARG, "prompt_len[%d] must be >= 1", t);
+    SEG_CHECK(p->prompt_len[t] >= 0, SEG_ERR_ARG, "prompt_len[%d] < 0", t);
   }
   int32_t ns = p->step_offsets[p->num_traj];
   if (ns > 0)
@@ -160,6 +160,8 @@ Plan make_plan(const seg_problem *p) {
       const int La = a == 1 ? L0 : L;
       while (b - a < La && b <= T && (!cap || seg_len(img, text, pr, W, a, b + 1) <= cap)) ++b;
       int64_t n = seg_len(img, text, pr, W, a, b);
+      SEG_CHECK(n >= 1, SEG_ERR_ARG, "segment of trajectory %d, turns %d..%d holds no token", t, a,
+                b - 1);
       SEG_CHECK(!B || n <= B, SEG_ERR_CAPACITY,
                 "segment of %lld tokens (trajectory %d, turns %d..%d) exceeds buffer_tokens %lld",
                 (long long)n, t, a, b - 1, (long long)B);
@@ -227,6 +229,11 @@ Plan make_plan(const seg_problem *p) {
       if (x > 0) {
         if (j >= sg.a && act[j - 1] > 0) {
           int32_t na = act[j - 1];
+          // the ratio of a token uses the row before it (Eq. loss): a trained
+          // token cannot open its segment
+          SEG_CHECK(off + x - na > 0, SEG_ERR_ARG,
+                    "trajectory %d turn %d: a trained token is the first token of its segment "
+                    "(no row predicts it)", sg.traj, j);
           pl.lpieces.push_back({(int32_t)rows, d.start + off + x - na, c + x - na, sg.traj});
           rows += na;
         }
@@ -388,7 +395,8 @@ __global__ void __launch_bounds__(256) k_classify(
 
 // Exclusive scan of n counts into ptr[0..n] (one block of 1024 threads).
 __global__ void __launch_bounds__(1024) k_scan(const int32_t *__restrict__ cnt, int n,
-                                               int32_t *__restrict__ ptr) {
+                                               int32_t *__restrict__ ptr,
+                                               int64_t *__restrict__ total) {
   __shared__ int part[1024];
   const int t = threadIdx.x;
   const int per = (n + 1023) / 1024;
@@ -408,7 +416,10 @@ __global__ void __launch_bounds__(1024) k_scan(const int32_t *__restrict__ cnt, 
     ptr[i] = run;
     run += cnt[i];
   }
-  if (t == 1023) ptr[n] = part[1023];
+  if (t == 1023) {
+    ptr[n] = part[1023];
+    if (total) *total = part[1023];
+  }
 }
 
 // CSR rows: one wave per q-tile, k-tiles ascending.
@@ -460,50 +471,6 @@ __global__ void __launch_bounds__(64) k_fill_cols(const DevSeg *__restrict__ seg
   }
 }
 
-constexpr int kOrderBuckets = 8192;
-
-// work_order: tiles by decreasing CSR row length, ties by ascending index
-// (stable counting sort; one block of 64 threads, ordered pass by one wave).
-__global__ void __launch_bounds__(64) k_work_order(const int32_t *__restrict__ qcnt, int n,
-                                                   int32_t *__restrict__ order,
-                                                   const int32_t *__restrict__ qt_ptr,
-                                                   int64_t *__restrict__ nnz_out) {
-  __shared__ int cnt[kOrderBuckets];
-  const int lane = threadIdx.x;
-  for (int b = lane; b < kOrderBuckets; b += 64) cnt[b] = 0;
-  __syncthreads();
-  auto bucket = [](int len) { return kOrderBuckets - 1 - min(len, kOrderBuckets - 1); };
-  for (int g = lane; g < n; g += 64) atomicAdd(&cnt[bucket(qcnt[g])], 1);
-  __syncthreads();
-  if (lane == 0) {
-    int run = 0;
-    for (int b = 0; b < kOrderBuckets; ++b) {
-      int c = cnt[b];
-      cnt[b] = run;
-      run += c;
-    }
-    *nnz_out = qt_ptr[n];
-  }
-  __syncthreads();
-  for (int g0 = 0; g0 < n; g0 += 64) {
-    const int g = g0 + lane;
-    const bool valid = g < n;
-    const int key = valid ? bucket(qcnt[g]) : -1;
-    unsigned long long pending = __ballot(valid);
-    while (pending) {
-      const int leader = __ffsll((long long)pending) - 1;
-      const int lk = __shfl(key, leader, 64);
-      const unsigned long long m = __ballot(valid && key == lk);
-      if (valid && key == lk) order[cnt[lk] + __popcll(m & ((1ull << lane) - 1))] = g;
-      __syncthreads();
-      if (lane == leader) cnt[lk] += __popcll(m);
-      __syncthreads();
-      pending &= ~m;
-    }
-  }
-  if (n == 0 && lane == 0) *nnz_out = 0;
-}
-
 int grid_for(int64_t n, int block = 256) {
   int64_t g = (n + block - 1) / block;
   return (int)std::max<int64_t>(1, std::min<int64_t>(g, 65536));
@@ -542,7 +509,7 @@ extern "C" seg_status seg_build_layout(const seg_problem *p, const seg_sizes *sz
     if (S > 0) {
       SEG_CHECK(ws && out->seg_info && out->tok_src && out->tok_meta && out->tile_seg &&
                     out->qt_ptr && out->qt_col && out->qt_cls && out->kt_ptr && out->kt_row &&
-                    out->kt_cls && out->seg_pairs && out->tile_nnz && out->work_order,
+                    out->kt_cls && out->seg_pairs && out->tile_nnz,
                 SEG_ERR_ARG, "a layout array is NULL");
       SEG_CHECK(R == 0 || (out->loss_pred_row && out->loss_tgt_src && out->loss_traj),
                 SEG_ERR_ARG, "a loss-row array is NULL");
@@ -598,17 +565,15 @@ extern "C" seg_status seg_build_layout(const seg_problem *p, const seg_sizes *sz
     k_classify<<<G, 256, 0, stream>>>(d_segs, out->tile_seg, out->tok_meta, Wv, p->tile,
                                       d_cls, d_qcnt, d_kcnt, out->seg_pairs);
     SEG_LAUNCH_CHECK();
-    k_scan<<<1, 1024, 0, stream>>>(d_qcnt, G, out->qt_ptr);
+    k_scan<<<1, 1024, 0, stream>>>(d_qcnt, G, out->qt_ptr, out->tile_nnz);
     SEG_LAUNCH_CHECK();
-    k_scan<<<1, 1024, 0, stream>>>(d_kcnt, G, out->kt_ptr);
+    k_scan<<<1, 1024, 0, stream>>>(d_kcnt, G, out->kt_ptr, nullptr);
     SEG_LAUNCH_CHECK();
     k_fill_rows<<<G, 64, 0, stream>>>(d_segs, out->tile_seg, d_cls, out->qt_ptr, out->qt_col,
                                       out->qt_cls);
     SEG_LAUNCH_CHECK();
     k_fill_cols<<<G, 64, 0, stream>>>(d_segs, out->tile_seg, d_cls, out->kt_ptr, out->kt_row,
                                       out->kt_cls);
-    SEG_LAUNCH_CHECK();
-    k_work_order<<<1, 64, 0, stream>>>(d_qcnt, G, out->work_order, out->qt_ptr, out->tile_nnz);
     SEG_LAUNCH_CHECK();
   });
 }

@@ -1,6 +1,7 @@
 // Optional per-kernel timing: when enabled, every kernel launch of the library
 // is bracketed by HIP events recorded on the launch stream, so a caller can read
 // the device time of each kernel without an external profiler.
+#include <atomic>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -15,23 +16,35 @@ struct Rec {
 };
 std::mutex g_mu;
 std::vector<Rec> g_recs;
-bool g_on = false;
+// read by every launch of any thread, written by seg_profile_enable
+std::atomic<bool> g_on{false};
+
+void destroy_pair(hipEvent_t a, hipEvent_t b) {
+  (void)hipEventDestroy(a);
+  (void)hipEventDestroy(b);
+}
 }  // namespace
 
 ProfScope::ProfScope(const char *name, hipStream_t s) : name_(name), stream_(s) {
-  if (!g_on) return;
+  if (!g_on.load(std::memory_order_relaxed)) return;
   if (hipEventCreate(&start_) != hipSuccess) return;
   if (hipEventCreate(&stop_) != hipSuccess) {
     (void)hipEventDestroy(start_);
     return;
   }
-  if (hipEventRecord(start_, stream_) != hipSuccess) return;
+  if (hipEventRecord(start_, stream_) != hipSuccess) {
+    destroy_pair(start_, stop_);
+    return;
+  }
   active_ = true;
 }
 
 ProfScope::~ProfScope() {
   if (!active_) return;
-  if (hipEventRecord(stop_, stream_) != hipSuccess) return;
+  if (hipEventRecord(stop_, stream_) != hipSuccess) {
+    destroy_pair(start_, stop_);
+    return;
+  }
   std::lock_guard<std::mutex> lk(g_mu);
   g_recs.push_back({name_, start_, stop_});
 }
@@ -40,7 +53,7 @@ ProfScope::~ProfScope() {
 
 using namespace seg;
 
-extern "C" void seg_profile_enable(int32_t on) { g_on = on != 0; }
+extern "C" void seg_profile_enable(int32_t on) { g_on.store(on != 0, std::memory_order_relaxed); }
 
 extern "C" void seg_profile_reset(void) {
   std::lock_guard<std::mutex> lk(g_mu);

@@ -76,7 +76,7 @@ class Layout:
 
     FIELDS = ["seg_info", "tok_src", "tok_meta", "loss_pred_row", "loss_tgt_src", "loss_traj",
               "tile_seg", "qt_ptr", "qt_col", "qt_cls", "kt_ptr", "kt_row", "kt_cls",
-              "seg_pairs", "tile_nnz", "work_order"]
+              "seg_pairs", "tile_nnz"]
 
     def __init__(self, sizes: SegSizes, device):
         import torch
@@ -104,7 +104,6 @@ class Layout:
         self.kt_cls = e(Z, u8)
         self.seg_pairs = e(S, i64)
         self.tile_nnz = e(1, i64)
-        self.work_order = e(G, i32)
         self.ws = e(sizes.workspace_bytes, u8)
         self.c = SegLayout(*[getattr(self, f).data_ptr() for f in self.FIELDS], 0, 0)
 
@@ -117,7 +116,7 @@ class Layout:
                 "loss_tgt_src": s.loss_rows, "loss_traj": s.loss_rows,
                 "tile_seg": s.num_qtiles, "qt_ptr": s.num_qtiles + 1, "qt_col": nnz,
                 "qt_cls": nnz, "kt_ptr": s.num_qtiles + 1, "kt_row": nnz, "kt_cls": nnz,
-                "seg_pairs": s.num_segments, "tile_nnz": 1, "work_order": s.num_qtiles}
+                "seg_pairs": s.num_segments, "tile_nnz": 1}
         out = {f: getattr(self, f)[:lens[f]].cpu().numpy() for f in self.FIELDS}
         out["seg_info"] = out["seg_info"].reshape(-1, 8)
         return out

@@ -64,12 +64,20 @@ def test_query_random_and_edge():
         T = rng.integers(0, 7, size=n)
         ns = int(T.sum())
         text = rng.integers(0, 9, size=ns)
-        sp = WL.explicit_spans(T, rng.integers(1, 9, size=n), rng.integers(0, 9, size=ns), text,
+        # prompts may be empty: a segment without tokens, or one opened by a
+        # trained token, is an argument error on both sides
+        sp = WL.explicit_spans(T, rng.integers(0, 9, size=n), rng.integers(0, 9, size=ns), text,
                                [int(rng.integers(0, t + 1)) for t in text])
         W, L, tile = int(rng.integers(1, 4)), int(rng.integers(1, 4)), int(rng.choice([1, 4, 128]))
         pr = S.Problem.from_spans(sp, W, L, 0, 0, tile)
+        try:
+            want = _sizes_oracle(sp, W, L, tile)
+        except ValueError:
+            with pytest.raises(_lib.SegError) as ei:
+                S.seg_layout_query(pr)
+            assert ei.value.status == _lib.SEG_ERR_ARG
+            continue
         got = S.seg_layout_query(pr).as_dict()
-        want = _sizes_oracle(sp, W, L, tile)
         for k, v in want.items():
             assert got[k] == v, (it, k, got[k], v)
 
@@ -100,7 +108,9 @@ def test_query_errors(kw, status, text):
 def test_bad_spans():
     _lib_or_skip()
     bad = [
-        WL.explicit_spans([2], [0], [1, 1], [2, 2], [1, 1]),        # empty prompt
+        WL.explicit_spans([2], [-1], [1, 1], [2, 2], [1, 1]),       # negative prompt
+        WL.explicit_spans([2], [0], [0, 1], [2, 2], [2, 1]),        # trained token opens a segment
+        WL.explicit_spans([2], [0], [0, 1], [0, 2], [0, 1]),        # segment without tokens
         WL.explicit_spans([2], [3], [1, -1], [2, 2], [1, 1]),       # negative screenshot
         WL.explicit_spans([2], [3], [1, 1], [2, 2], [3, 1]),        # action longer than text
     ]
