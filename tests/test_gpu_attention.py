@@ -268,6 +268,66 @@ def test_full_size_sampled_rows_and_identities(cfg):
         assert np.linalg.norm(dk_sum) < TOL * float(dk_seg.pow(2).sum().sqrt())
 
 
+def _tail_keys(sg, turn, n, span, rng):
+    """n screenshot keys of `turn` among the last `span` rows of its screenshot
+    (always its last row)."""
+    img = np.nonzero((sg.kind == OL.KIND_IMAGE) & (sg.step == turn))[0][-span:]
+    return np.unique(np.concatenate([img[-1:], rng.choice(img, n - 1, replace=False)]))
+
+
+# (workload, also sample keys of the second-to-last turn)
+KEY_CASES = [(WL.SEVEN_B, True), (WL.SEVEN_B_ANCHORED, False), (WL.LONG, False)]
+
+
+@pytest.mark.parametrize("cfg,prev_turn", KEY_CASES, ids=[c.name for c, _ in KEY_CASES])
+def test_full_size_key_gradients(cfg, prev_turn):
+    """Full-size launch (28q/4kv, d = 128: seven query heads per kv head):
+    dK and dV of sampled screenshot keys, key by key, against the oracle, on
+    the last kv head.  Keys lie in the tail of the last turn's screenshot of
+    the shortest segment with two or more turns (two 128-row tiles), and for
+    the 7B-class batch also in the tail of the turn before, which the last
+    turn's rows still see; only rows at or after a key can see it, and each
+    such row's softmax (its LSE and Delta) is the oracle's over every key it
+    sees."""
+    import torch
+    say(f"full-size key gradients {cfg.name}")
+    run = GpuRun(cfg).packed_inputs()
+    run.fwd()
+    run.bwd()
+    torch.cuda.synchronize()
+    ref = _ref_layout(run)
+    multi = [sg for sg in ref.segments if len(np.unique(sg.step[sg.step > 0])) >= 2]
+    sg = min(multi, key=lambda s: s.length)
+    turns = np.unique(sg.step[sg.step > 0])
+    rng = np.random.default_rng(1)
+    keys = [_tail_keys(sg, turns[-1], 10, 192, rng)]
+    if prev_turn:
+        keys.append(_tail_keys(sg, turns[-2], 4, 64, rng))
+    keys = np.unique(np.concatenate(keys))
+    rows = np.arange(keys.min(), sg.length)
+    mask = OL.visibility_rows(sg, vis_window(cfg), rows)
+    sees = mask[:, keys].any(1)
+    rows, mask = rows[sees], mask[sees]
+    say(f"  segment at {sg.start}: {sg.length} tokens, {len(keys)} keys, {len(rows)} rows")
+    grp = cfg.hq // cfg.hkv
+    g = cfg.hkv - 1
+    hs = slice(g * grp, (g + 1) * grp)
+    k_all = run.inp.k_np(sg.canon)[:, g:g + 1]
+    v_all = run.inp.v_np(sg.canon)[:, g:g + 1]
+    q = run.inp.q_np(sg.canon[rows])[:, hs]
+    dout = run.inp.dout_np(sg.start + rows)[:, hs]
+    idx = torch.from_numpy(sg.start + keys).cuda()
+    dk_g = run.dk[idx, g].float().cpu().numpy()
+    dv_g = run.dv[idx, g].float().cpu().numpy()
+    dk_r, dv_r = OA.key_grads(q, k_all, v_all, mask, run.scale, dout, keys)
+    e_k, e_v = rel(dk_g, dk_r[:, 0]), rel(dv_g, dv_r[:, 0])
+    say(f"  kv head {g}: dK rel err {e_k:.2e}, dV rel err {e_v:.2e}")
+    assert e_k < TOL and e_v < TOL, (e_k, e_v)
+    for i in range(len(keys)):   # and no single key off
+        assert rel(dk_g[i], dk_r[i, 0]) < TOL, ("dk", int(keys[i]))
+        assert rel(dv_g[i], dv_r[i, 0]) < TOL, ("dv", int(keys[i]))
+
+
 def test_action_rows_segment_equals_stepwise():
     """Attention outputs of the action-predicting rows agree between the
     segmented layout and the step-wise decomposition of the same canonical

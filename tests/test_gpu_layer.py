@@ -79,9 +79,36 @@ def _np(t):
     return t.float().cpu().numpy().astype(np.float64)
 
 
+def _big_tiles(M, N):
+    """256x256 tiles of an M x N product: the data-gradient and projection
+    GEMMs take the 256-wide kernel from 192 tiles on."""
+    return -(-M // 256) * -(-N // 256)
+
+
+# GEMMs on the 256-wide kernel: ~4.9k packed rows at the 7B-class widths
+# (hidden 3584, 28q/4kv, d = 128) with an MLP width of 3072, so dm, db, dO and
+# the dq/dk/dv data gradients (and the forward projections) pass 192 tiles
+WIDE = (MED.with_(hq=28, hkv=4, head_dim=128, steps=(4, 5), img_len=300, text_len=(60, 120),
+                  seed=33), 3584, 3072)
+
+
 @pytest.mark.parametrize("name", list(CASES))
 def test_layer_full_parity(name):
     cfg, H, I, chunk = CASES[name]
+    _full_parity(name, cfg, H, I, chunk)
+
+
+def test_layer_wide_gemm_parity():
+    """Full parity where the layer's GEMMs run the 256x256 kernels with the
+    accumulate / fp32-store epilogues of the backward (dx and all nine weight
+    gradients against the oracle)."""
+    cfg, H, I = WIDE
+    lr = _full_parity("wide", cfg, H, I, 0)
+    assert _big_tiles(lr.P, H) >= 192 and _big_tiles(lr.P, I) >= 192
+    assert _big_tiles(lr.P, cfg.hq * cfg.head_dim) >= 192
+
+
+def _full_parity(name, cfg, H, I, chunk):
     say(f"case {name}: H={H} I={I} chunk_rows={chunk}")
     lr = LayerRun(cfg, H, I, chunk)
     y, saved, dx, grads = lr.gpu()
@@ -105,6 +132,7 @@ def test_layer_full_parity(name):
     assert not bad, (name, bad)
     # padding rows carry no gradient
     assert np.all(_np(dx)[~seg] == 0)
+    return lr
 
 
 def test_layer_chunking_keeps_rowwise_results_bitwise():
