@@ -197,6 +197,33 @@ seg_status seg_attn_bwd(const seg_layout *L, const seg_sizes *sz, seg_dtype dt, 
                         const void *d_o, void *dq, void *dk, void *dv, void *ws,
                         size_t ws_bytes, hipStream_t stream);
 
+/* Size of the fixed device scratch behind seg_attn_bwd_noalloc: 64 MiB. */
+#define SEG_ATTN_BWD_SCRATCH_BYTES ((size_t)64 << 20)
+
+/*
+ * seg_attn_bwd without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments, results and kernels as
+ * seg_attn_bwd; its workspace is a library-owned device array of
+ * SEG_ATTN_BWD_SCRATCH_BYTES, one per GPU, held until the process ends
+ * (its address on the current device is looked up once per device on the
+ * first call there).  The call allocates nothing and needs
+ * seg_attn_workspace_bytes(sz, dt, hq, hkv, d, 1) <= SEG_ATTN_BWD_SCRATCH_BYTES
+ * (bf16: 8 * hq * packed_tokens bytes rounded up to 256, e.g. 28 heads x
+ * 299,000 packed rows); a larger problem returns SEG_ERR_WORKSPACE before any
+ * launch.  `stream` must belong to the current device.  Every call on a GPU
+ * shares that GPU's scratch (nothing in it needs to start at zero: each call
+ * writes what it reads), so calls that overlap on one GPU, on different
+ * streams or from different threads, race and give wrong results: serialise
+ * them.  Errors as seg_attn_bwd, plus SEG_ERR_HIP when the scratch address
+ * cannot be obtained.
+ */
+seg_status seg_attn_bwd_noalloc(const seg_layout *L, const seg_sizes *sz, seg_dtype dt,
+                                int32_t hq, int32_t hkv, int32_t d, float softmax_scale,
+                                const void *q, const void *k, const void *v, const void *o,
+                                const float *lse, const void *d_o, void *dq, void *dk, void *dv,
+                                hipStream_t stream);
+
 /*
  * Settings of the clipped policy-ratio objective with its KL penalty
  * (Eq. (loss), App. E): per row, rho = exp(logp - old_logp), A = adv[row_traj];

@@ -18,10 +18,11 @@ SEG_OK, SEG_ERR_ARG, SEG_ERR_CAPACITY, SEG_ERR_WORKSPACE, SEG_ERR_UNSUPPORTED, S
 STATUS_NAMES = {0: "SEG_OK", 1: "SEG_ERR_ARG", 2: "SEG_ERR_CAPACITY", 3: "SEG_ERR_WORKSPACE",
                 4: "SEG_ERR_UNSUPPORTED", 5: "SEG_ERR_HIP"}
 SEG_BF16, SEG_F32 = 0, 1
+SEG_ATTN_BWD_SCRATCH_BYTES = 64 << 20
 
 # every symbol include/seg.h declares
 EXPORTS = ["seg_layout_query", "seg_build_layout", "seg_attn_workspace_bytes", "seg_attn_fwd",
-           "seg_attn_bwd", "seg_logprob_workspace_bytes", "seg_logprob_loss",
+           "seg_attn_bwd", "seg_attn_bwd_noalloc", "seg_logprob_workspace_bytes", "seg_logprob_loss",
            "seg_layer_workspace_bytes", "seg_layer_fwd", "seg_layer_bwd", "seg_profile_enable",
            "seg_profile_reset", "seg_profile_read", "seg_last_error"]
 
@@ -125,6 +126,11 @@ def lib() -> ctypes.CDLL:
         L.seg_attn_bwd.argtypes = [ctypes.POINTER(SegLayout), ctypes.POINTER(SegSizes), ctypes.c_int,
                                    ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_float,
                                    VP, VP, VP, VP, VP, VP, VP, VP, VP, VP, ctypes.c_size_t, VP]
+        L.seg_attn_bwd_noalloc.restype = ctypes.c_int
+        L.seg_attn_bwd_noalloc.argtypes = [ctypes.POINTER(SegLayout), ctypes.POINTER(SegSizes),
+                                           ctypes.c_int, ctypes.c_int32, ctypes.c_int32,
+                                           ctypes.c_int32, ctypes.c_float,
+                                           VP, VP, VP, VP, VP, VP, VP, VP, VP, VP]
         L.seg_logprob_workspace_bytes.restype = ctypes.c_size_t
         L.seg_logprob_workspace_bytes.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                                   ctypes.c_int]

@@ -14,8 +14,9 @@
 // their other operand from LDS through transpose reads in the same row order
 // (kperm() in common.h).
 #include <climits>
-#include <type_traits>
 #include <cmath>
+#include <mutex>
+#include <type_traits>
 
 #include "common.h"
 
@@ -1187,4 +1188,58 @@ extern "C" seg_status seg_attn_bwd(const seg_layout *L, const seg_sizes *sz, seg
                                                      dv, stream);
     }
   });
+}
+
+// Workspace of seg_attn_bwd_noalloc: one copy of this array per GPU, held
+// until the process ends.  Host code never uses the name itself (on the host
+// it is a stand-in, not a device address): the device address comes from
+// hipGetSymbolAddress, once per device.
+static __device__ __align__(256) unsigned char scratch[SEG_ATTN_BWD_SCRATCH_BYTES];
+
+namespace seg {
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on the current device.
+void *scratch_on_current_device() {
+  int dev = -1;
+  SEG_HIP(hipGetDevice(&dev));
+  SEG_CHECK(dev >= 0 && dev < kMaxDevices, SEG_ERR_UNSUPPORTED, "device %d above %d", dev,
+            kMaxDevices - 1);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *ptr = nullptr;
+    SEG_HIP(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)));
+    SEG_CHECK(ptr != nullptr, SEG_ERR_HIP, "no device address for the scratch array");
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace
+}  // namespace seg
+
+extern "C" seg_status seg_attn_bwd_noalloc(const seg_layout *L, const seg_sizes *sz, seg_dtype dt,
+                                           int32_t hq, int32_t hkv, int32_t d,
+                                           float softmax_scale, const void *q, const void *k,
+                                           const void *v, const void *o, const float *lse,
+                                           const void *d_o, void *dq, void *dk, void *dv,
+                                           hipStream_t stream) {
+  void *ptr = nullptr;
+  const seg_status st = guarded([&] {
+    check_common(L, sz, dt, hq, hkv, d);
+    const size_t need = attn_ws(*sz, dt, hq, hkv, d, 1).total;
+    SEG_CHECK(need <= SEG_ATTN_BWD_SCRATCH_BYTES, SEG_ERR_WORKSPACE,
+              "the backward needs %zu bytes of workspace, above the %zu-byte fixed scratch of "
+              "seg_attn_bwd_noalloc (use seg_attn_bwd with a workspace)",
+              need, (size_t)SEG_ATTN_BWD_SCRATCH_BYTES);
+    if (sz->num_qtiles == 0) return;
+    ptr = scratch_on_current_device();
+  });
+  if (st != SEG_OK) return st;
+  return seg_attn_bwd(L, sz, dt, hq, hkv, d, softmax_scale, q, k, v, o, lse, d_o, dq, dk, dv, ptr,
+                      SEG_ATTN_BWD_SCRATCH_BYTES, stream);
 }

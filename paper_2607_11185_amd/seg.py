@@ -203,6 +203,24 @@ def seg_attn_bwd(lay: Layout, q, k, v, o, lse, dout, softmax_scale: float, dq=No
     return dq, dk, dv
 
 
+def seg_attn_bwd_noalloc(lay: Layout, q, k, v, o, lse, dout, softmax_scale: float, dq, dk, dv):
+    """seg_attn_bwd on the library's fixed device scratch: the caller passes
+    every output, nothing is allocated (calls on one GPU must not overlap)."""
+    dt = _dtype_code(q)
+    P, hq, d = q.shape
+    hkv = k.shape[1]
+    for t in (q, k, v, o, dout, dq):
+        assert t.is_contiguous() and t.dtype == q.dtype
+    for t in (dk, dv):
+        assert t.is_contiguous() and t.dtype == q.dtype
+    check(_lib.lib().seg_attn_bwd_noalloc(ctypes.byref(lay.c), ctypes.byref(lay.sizes), dt, hq,
+                                          hkv, d, float(softmax_scale), q.data_ptr(),
+                                          k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                          lse.data_ptr(), dout.data_ptr(), dq.data_ptr(),
+                                          dk.data_ptr(), dv.data_ptr(), _stream(q.device)))
+    return dq, dk, dv
+
+
 @dataclasses.dataclass
 class LossCfg:
     eps_low: float = 0.2

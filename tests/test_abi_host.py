@@ -181,6 +181,26 @@ def test_build_and_compute_reject_bad_args_before_any_launch():
         assert b"kl" in L.seg_last_error()
 
 
+def test_noalloc_backward_rejects_before_any_launch():
+    """The fixed-scratch backward checks its size limit and the shapes on the
+    host: no device is touched for a rejected call."""
+    L = _lib_or_skip()
+    sz = S.seg_layout_query(_prob())
+    lay = _lib.SegLayout()
+    lay.tile, lay.window = 128, 2
+    big = _lib.SegSizes.from_buffer_copy(sz)
+    hq, hkv, d = 28, 4, 128
+    big.packed_tokens = _lib.SEG_ATTN_BWD_SCRATCH_BYTES // (8 * hq) + 256
+    assert L.seg_attn_workspace_bytes(ctypes.byref(big), 0, hq, hkv, d, 1) > \
+        _lib.SEG_ATTN_BWD_SCRATCH_BYTES
+    nul = [None] * 10
+    st = L.seg_attn_bwd_noalloc(ctypes.byref(lay), ctypes.byref(big), 0, hq, hkv, d, 0.1, *nul, None)
+    assert st == _lib.SEG_ERR_WORKSPACE
+    assert b"seg_attn_bwd_noalloc" in L.seg_last_error()
+    st = L.seg_attn_bwd_noalloc(ctypes.byref(lay), ctypes.byref(sz), 0, 4, 1, 96, 0.1, *nul, None)
+    assert st == _lib.SEG_ERR_UNSUPPORTED
+
+
 def test_query_anchored_matches_oracle():
     """Sizes of the anchored mode (the App. D algorithm) against the oracle,
     on the workloads and on random span lists."""
