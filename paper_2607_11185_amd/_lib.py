@@ -12,7 +12,9 @@ import os
 from typing import Optional
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libseg.so")
+# SEG_LIB_PATH selects another build of the same library (the host-sanitizer
+# build of build.py); by default the in-tree libseg.so
+LIB_PATH = os.environ.get("SEG_LIB_PATH") or os.path.join(HERE, "libseg.so")
 
 SEG_OK, SEG_ERR_ARG, SEG_ERR_CAPACITY, SEG_ERR_WORKSPACE, SEG_ERR_UNSUPPORTED, SEG_ERR_HIP = range(6)
 STATUS_NAMES = {0: "SEG_OK", 1: "SEG_ERR_ARG", 2: "SEG_ERR_CAPACITY", 3: "SEG_ERR_WORKSPACE",

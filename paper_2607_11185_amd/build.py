@@ -23,16 +23,36 @@ FLAGS = [
 ]
 
 
-def build(verbose: bool = False, jobs: int = 3) -> str:
-    """Compile every HIP source and link libseg.so next to this file."""
-    objdir = os.path.join(HERE, "_build")
+# Host-code sanitizers (AddressSanitizer + UndefinedBehaviorSanitizer) for a
+# CPU-side check build: every flag applies to the host compilation only, the
+# device code is built as usual.
+SANITIZE_FLAGS = [
+    "-Xarch_host", "-fsanitize=address",
+    "-Xarch_host", "-fsanitize=undefined",
+    "-Xarch_host", "-fno-sanitize-recover=undefined",
+    "-Xarch_host", "-fno-omit-frame-pointer", "-g",
+]
+SANITIZE_LINK = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                 "-Xarch_host", "-shared-libasan"]
+SANITIZED_LIB = os.path.join(HERE, "_build", "sanitize", "libseg.so")
+
+
+def build(verbose: bool = False, jobs: int = 3, sanitize: bool = False) -> str:
+    """Compile every HIP source and link libseg.so next to this file; with
+    `sanitize`, the host-sanitizer build at SANITIZED_LIB instead (load it
+    with the ASan runtime preloaded, e.g. through SEG_LIB_PATH)."""
+    objdir = os.path.join(HERE, "_build", "sanitize") if sanitize else os.path.join(HERE, "_build")
+    out = SANITIZED_LIB if sanitize else LIB
+    flags = FLAGS + SANITIZE_FLAGS if sanitize else FLAGS
+    if sanitize:
+        flags = [f if f != "-O3" else "-O1" for f in flags]
     os.makedirs(objdir, exist_ok=True)
     procs = []
     objs = []
     for src in SOURCES:
         obj = os.path.join(objdir, src.replace(".hip", ".o"))
         objs.append(obj)
-        cmd = [HIPCC, *FLAGS, "-I", INCLUDE, "-I", CSRC, "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [HIPCC, *flags, "-I", INCLUDE, "-I", CSRC, "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)))
@@ -40,11 +60,21 @@ def build(verbose: bool = False, jobs: int = 3) -> str:
             _wait(procs.pop(0))
     for p in procs:
         _wait(p)
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs]
+    tmp = out + ".tmp"
+    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *(SANITIZE_LINK if sanitize else []),
+           "-o", tmp, *objs]
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
+
+
+def asan_runtime() -> str:
+    """Path of the compiler's shared AddressSanitizer runtime."""
+    clang = os.path.join(os.path.dirname(os.path.realpath(HIPCC)), "..", "llvm", "bin", "clang")
+    if not os.path.exists(clang):
+        clang = "/opt/rocm/llvm/bin/clang"
+    return subprocess.run([clang, "-print-file-name=libclang_rt.asan-x86_64.so"], check=True,
+                          capture_output=True, text=True).stdout.strip()
 
 
 def _wait(item):
@@ -60,4 +90,4 @@ def _wait(item):
 
 
 if __name__ == "__main__":
-    print(build(verbose=True))
+    print(build(verbose=True, sanitize="--sanitize" in sys.argv))

@@ -151,6 +151,21 @@ def test_fwd_bwd_full_parity(name):
         e = rel(np.concatenate(g), np.concatenate(r))
         say(f"  {n}: rel err {e:.2e}")
         assert e < TOL, (name, n, e)
+    if cfg.dtype == "f32":
+        # fp32 inputs are rounded to bf16 at load: the error against the
+        # oracle on the unrounded values, reported next to the one above
+        for sg in ref.segments:
+            q, k, v = (run.inp.q_np(sg.canon), run.inp.k_np(sg.canon), run.inp.v_np(sg.canon))
+            dout = run.inp.dout_np(np.arange(sg.start, sg.start + sg.length))
+            mask = OL.visibility(sg, vis_window(cfg))
+            o_r, lse_r = OA.forward(q, k, v, mask, run.scale)
+            dq_r, dk_r, dv_r = OA.backward(q, k, v, mask, run.scale, dout)
+            rows = slice(sg.start, sg.start + sg.length)
+            for n, g, r in (("o", o[rows], o_r), ("lse", lse[:, rows], lse_r),
+                            ("dq", dq[rows], dq_r), ("dk", dk[rows], dk_r), ("dv", dv[rows], dv_r)):
+                e = rel(g, r)
+                say(f"  {n} vs unrounded fp32 inputs (segment at {sg.start}): rel err {e:.2e}")
+                assert e < TOL, (name, "unrounded", n, e)
     if fac is not None:
         say(f"  running-max moves of > 9 log2 units after a finite max: {events}")
         assert events > 0

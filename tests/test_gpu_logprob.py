@@ -78,14 +78,27 @@ def test_full_parity(cfg, dual):
     assert np.abs(logp - ref["logp"]).max() < 2e-2 * max(1.0, np.abs(ref["logp"]).max())
     assert rel(logp, ref["logp"]) < TOL
     assert rel(out["loss_tok"][:R].cpu().numpy(), ref["loss_tok"]) < TOL
-    # clip decisions agree except where the ratio sits next to a clip bound
-    rho = np.exp(ref["logp"] - old)
-    near = (np.abs(np.log(rho) - np.log(1 - cfg.eps_low)) < 1e-2) | \
-           (np.abs(np.log(rho) - np.log(1 + cfg.eps_high)) < 1e-2)
-    if dual:
-        near |= np.abs(np.log(rho) - np.log(dual)) < 1e-2
+    # Clip decisions.  (1) The kernel decides from its own log-prob: its flag
+    # equals the decision recomputed from that log-prob, except within 1e-5
+    # of a bound in ln(rho) (the float32 ratio's rounding).  (2) A flag that
+    # differs from the oracle's needs the row's ratio to lie nearer a bound
+    # than the row's own log-prob error (plus that 1e-5).
     cl = out["clipped"][:R].cpu().numpy().astype(bool)
-    assert (cl == ref["clipped"])[~near].all()
+    adv_rows = _inputs(run)[3]
+    bounds = [np.log(1 - cfg.eps_low), np.log(1 + cfg.eps_high)] + ([np.log(dual)] if dual else [])
+
+    def near(log_rho, width):
+        return np.any([np.abs(log_rho - b) <= width for b in bounds], axis=0)
+
+    _, _, _, own = OLS.clipped_objective(logp.astype(np.float64), old.astype(np.float64), adv_rows,
+                                         cfg.eps_low, cfg.eps_high, dual)
+    lr_gpu = logp.astype(np.float64) - old
+    assert (cl == own)[~near(lr_gpu, 1e-5)].all()
+    err = np.abs(logp.astype(np.float64) - ref["logp"])
+    lr_ref = ref["logp"] - old
+    flips = cl != ref["clipped"]
+    say(f"  clip flags differing from the oracle: {int(flips.sum())} of {R}")
+    assert near(lr_ref, err + 1e-5)[flips].all()
     assert ref["clipped"].any() and (~ref["clipped"]).any()
     assert abs(float(out["loss_sum"][0]) - ref["loss_sum"]) < TOL * max(1e-3, abs(ref["loss_sum"]))
     e_dh = rel(out["dh"][:R].float().cpu().numpy(), ref["dh"])
@@ -100,6 +113,27 @@ def test_full_parity(cfg, dual):
         assert rel(dh[i], ref["dh"][i]) < TOL, ("dh row", i)
     for v in (0, dw.shape[0] - 1):
         assert rel(dw[v], ref["dw"][v]) < TOL, ("dw row", v)
+
+
+def test_tiny_against_unrounded_fp32_inputs():
+    """The tiny workload's fp32 h and W are rounded to bf16 at load; report
+    (and bound) the error against the oracle on the unrounded values, next to
+    the error against the oracle on the rounded ones."""
+    cfg = WL.TINY
+    run, ref, out, old = _full_case(cfg)
+    R = run.lay.sizes.loss_rows
+    hst = run.host
+    h = run.inp.h_np(hst["tok_src"][hst["loss_pred_row"]])
+    w = run.inp.w_np()
+    _, _, tgt, adv = _inputs(run)
+    raw = OLS.loss_and_grads(h, w, tgt, old.astype(np.float64), adv, cfg.eps_low, cfg.eps_high,
+                             loss_scale=1.0 / R)
+    for n, g in (("logp", out["logp"][:R].cpu().numpy()),
+                 ("loss_tok", out["loss_tok"][:R].cpu().numpy()),
+                 ("dh", out["dh"][:R].float().cpu().numpy()), ("dw", out["dw"].cpu().numpy())):
+        e_round, e_raw = rel(g, ref[n]), rel(g, raw[n])
+        say(f"  {n}: rel err {e_round:.2e} vs bf16-rounded inputs, {e_raw:.2e} vs unrounded fp32")
+        assert e_round < TOL and e_raw < TOL, (n, e_round, e_raw)
 
 
 @pytest.mark.parametrize("cfg,kl", [(WL.TINY, 0.5), (WL.SMALL, 0.5), (WL.SMALL, 1e-4)],
