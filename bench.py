@@ -78,14 +78,17 @@ def log(*a):
 class PathRun:
     """All device buffers of one path (segmented or step-wise) and its step."""
 
-    def __init__(self, cfg, dev):
+    def __init__(self, cfg, dev, spans=None, quick_inputs=False):
+        """quick_inputs: draw q, k, v, dO, hidden states and the projection
+        with torch.randn (a handful of large launches; for counter passes,
+        which serialise every launch) instead of the workload generator."""
         import numpy as np
         import torch
 
         from paper_2607_11185_amd import seg as S
         from paper_2607_11185_amd import workload as WL
         self.S, self.cfg, self.dev = S, cfg, dev
-        inp = WL.Inputs(cfg)
+        inp = WL.Inputs(cfg, spans)
         self.problem = S.Problem.from_spans(inp.spans, cfg.window, cfg.seg_steps,
                                             cfg.max_seg_tokens, cfg.buffer_tokens, 128, cfg.mode)
         self.sizes = S.seg_layout_query(self.problem)
@@ -97,14 +100,28 @@ class PathRun:
         log(f"[{cfg.name}] segments={sz.num_segments} packed={P} traj_tokens={sz.traj_tokens} "
             f"loss_rows={R} tiles={sz.num_qtiles} nnz={int(host['tile_nnz'][0])} pairs/head={self.pairs}")
         src = torch.from_numpy(host["tok_src"].astype(np.int64)).to(dev)
-        self.q = inp.q_torch(dev)[src].contiguous()
-        self.k = inp.k_torch(dev)[src].contiguous()
-        self.v = inp.v_torch(dev)[src].contiguous()
-        torch.cuda.empty_cache()
-        self.dout = inp.dout_torch(P, dev)
-        self.h = inp.h_torch(dev)[src].contiguous()
-        torch.cuda.empty_cache()
-        self.w = inp.w_torch(dev)
+        if quick_inputs:
+            g = torch.Generator(device=dev)
+            g.manual_seed(cfg.seed)
+
+            def rn(*shape, std=1.0):
+                return (torch.randn(*shape, generator=g, device=dev, dtype=torch.float32)
+                        * std).to(torch.bfloat16)
+            hd = cfg.head_dim
+            self.q, self.k, self.v = rn(P, cfg.hq, hd), rn(P, cfg.hkv, hd), rn(P, cfg.hkv, hd)
+            self.dout, self.h = rn(P, cfg.hq, hd), rn(P, cfg.hidden)
+            self.w = rn(cfg.vocab, cfg.hidden, std=cfg.w_std)
+        else:
+            self.q = inp.q_torch(dev)[src].contiguous()
+            self.k = inp.k_torch(dev)[src].contiguous()
+            self.v = inp.v_torch(dev)[src].contiguous()
+            torch.cuda.empty_cache()
+            log(f"  [{cfg.name}] q, k, v ready")
+            self.dout = inp.dout_torch(P, dev)
+            self.h = inp.h_torch(dev)[src].contiguous()
+            torch.cuda.empty_cache()
+            self.w = inp.w_torch(dev)
+        log(f"  [{cfg.name}] inputs ready")
         self.tgt = torch.from_numpy(inp.tgt_np(host["loss_tgt_src"])).to(dev)
         self.adv = torch.from_numpy(inp.adv_np().astype(np.float32)).to(dev)
         self.scale = 1.0 / math.sqrt(cfg.head_dim)
@@ -225,6 +242,67 @@ def time_path(run, steps, warmup, profile=True):
     return ph, kern, wall / steps * 1e3
 
 
+# packed rows per trajectory group: about 40 KB of device memory per packed
+# row (q, o, dq, dO, hidden states, k, v and their gradients, per-row fp32)
+GROUP_ROWS = 4_500_000
+
+
+def traj_groups(cfg, max_rows=GROUP_ROWS):
+    """Consecutive trajectory ranges of the workload whose packed rows stay
+    within max_rows each (a range holds at least one trajectory)."""
+    from paper_2607_11185_amd import seg as S
+    from paper_2607_11185_amd import workload as WL
+    spans = WL.make_spans(cfg)
+    groups, t0 = [], 0
+    while t0 < spans.num_traj:
+        t1 = t0 + 1
+        while t1 < spans.num_traj:
+            sub = spans.subset(t0, t1 + 1)
+            pr = S.Problem.from_spans(sub, cfg.window, cfg.seg_steps, cfg.max_seg_tokens,
+                                      cfg.buffer_tokens, 128, cfg.mode)
+            if S.seg_layout_query(pr).packed_tokens > max_rows:
+                break
+            t1 += 1
+        groups.append(spans.subset(t0, t1))
+        t0 = t1
+    return groups
+
+
+def time_groups(cfg, dev, steps, warmup):
+    """time_path and time_ref over the workload's trajectory groups, one
+    group resident at a time; per-step times add up over the groups."""
+    import torch
+    groups = traj_groups(cfg)
+    ph, kern, wall, ref, tot = {}, {}, 0.0, {}, {"pairs": 0, "packed": 0, "segments": 0,
+                                                  "traj_tokens": 0, "flop": 0.0, "loss_rows": 0}
+    for gi, sub in enumerate(groups):
+        run = PathRun(cfg, dev, sub if len(groups) > 1 else None)
+        if len(groups) > 1:
+            log(f"  group {gi + 1}/{len(groups)}: {sub.num_traj} trajectories")
+        p, k, w = time_path(run, steps, warmup)
+        r = time_ref(run, steps, warmup)
+        for n, v in p.items():
+            ph[n] = ph.get(n, 0.0) + v
+        for n, v in k.items():
+            a = kern.setdefault(n, {"ms_per_step": 0.0, "launches_per_step": 0.0})
+            a["ms_per_step"] += v["ms_per_step"]
+            a["launches_per_step"] += v["launches_per_step"]
+        for n, v in r.items():
+            ref[n] = round(ref.get(n, 0.0) + v, 3)
+        wall += w
+        tot["pairs"] += run.pairs
+        tot["packed"] += run.sizes.packed_tokens
+        tot["segments"] += run.sizes.num_segments
+        tot["traj_tokens"] += run.sizes.traj_tokens
+        tot["loss_rows"] += run.sizes.loss_rows
+        tot["flop"] += run.attn_flop()
+        run.free()
+        del run
+        torch.cuda.empty_cache()
+    tot["groups"] = len(groups)
+    return ph, kern, wall, ref, tot
+
+
 def time_ref(run, steps, warmup):
     """Mean device ms of the reference forward pass (attention, log-prob)."""
     import torch
@@ -241,90 +319,92 @@ def time_ref(run, steps, warmup):
     return {"attn_fwd": round(att, 3), "logprob": round(lp, 3), "total": round(att + lp, 3)}
 
 
-def cpu_baseline(cfg, budget_note):
-    """The float64 oracle on a bounded sample (about 10 s): attention forward
-    and backward of the first segment for four query heads of one kv head."""
+def cpu_baseline(cfg):
+    """The float64 oracle on a bounded sample (about 10-15 s on 16 threads):
+    attention forward and backward of the first segment for up to four query
+    heads of one kv head (every segment and head for the tiny workload), and
+    the log-prob loss with its gradients for 16 action rows at the full
+    vocabulary.  The oracle's rates, extrapolated by the FLOP counts of the
+    whole step, give its trajectory tokens/s (labelled as extrapolated)."""
     import numpy as np
     from threadpoolctl import threadpool_info
 
     from oracle import attention as OA
     from oracle import layout as OL
+    from oracle import loss as OLS
     from paper_2607_11185_amd import workload as WL
     inp = WL.Inputs(cfg)
     ref = OL.build(inp.spans, cfg.window, cfg.seg_steps, 128, cfg.max_seg_tokens,
                    cfg.buffer_tokens, with_tiles=False, mode=cfg.mode)
-    sg = ref.segments[0]
-    nh = min(4, cfg.hq // cfg.hkv)  # query heads of kv head 0
-    q = inp.q_np(sg.canon)[:, :nh]
-    k = inp.k_np(sg.canon)[:, :1]
-    v = inp.v_np(sg.canon)[:, :1]
-    dout = inp.dout_np(np.arange(sg.start, sg.start + sg.length))[:, :nh]
+    full = cfg.name == "tiny"
+    segs = ref.segments if full else ref.segments[:1]
+    if not full and segs[0].length > 16384:
+        # a prefix of the segment is an attention problem of its own (rows see
+        # no key after them): the first 16,384 tokens
+        import dataclasses
+        sg0 = segs[0]
+        segs = [dataclasses.replace(sg0, canon=sg0.canon[:16384], kind=sg0.kind[:16384],
+                                    step=sg0.step[:16384])]
+    nh = cfg.hq if full else min(4, cfg.hq // cfg.hkv)  # query heads of kv head 0
+    nkv = cfg.hkv if full else 1
+    win = None if cfg.mode == "anchored" else cfg.window
     scale = 1.0 / math.sqrt(cfg.head_dim)
+    t_attn, pairs_done, toks = 0.0, 0, 0
+    for sg in segs:
+        q = inp.q_np(sg.canon)[:, :nh]
+        k = inp.k_np(sg.canon)[:, :nkv]
+        v = inp.v_np(sg.canon)[:, :nkv]
+        dout = inp.dout_np(np.arange(sg.start, sg.start + sg.length))[:, :nh]
+        t0 = time.perf_counter()
+        mask = OL.visibility(sg, win)
+        OA.forward(q, k, v, mask, scale)
+        OA.backward(q, k, v, mask, scale, dout)
+        t_attn += time.perf_counter() - t0
+        pairs_done += int(mask.sum())
+        toks += sg.length
+    attn_rate = 12.0 * cfg.head_dim * pairs_done * nh / t_attn
+    # log-prob sample: the first rows of the batch's loss rows
+    n_rows = min(16, len(ref.loss_pred_row))
+    sel = np.arange(n_rows)
+    h = inp.h_np(ref.tok_src[ref.loss_pred_row[sel]])
+    w = inp.w_np()
+    tgt = inp.tgt_np(ref.loss_tgt_src[sel])
+    adv = inp.adv_np()[ref.loss_traj[sel]]
     t0 = time.perf_counter()
-    mask = OL.visibility(sg, None if cfg.mode == "anchored" else cfg.window)
-    OA.forward(q, k, v, mask, scale)
-    OA.backward(q, k, v, mask, scale, dout)
-    dt = time.perf_counter() - t0
-    pairs = int(mask.sum())
-    flop = 12.0 * cfg.head_dim * pairs * nh
+    lp, _, _ = OLS.logprob(h, w, tgt)
+    OLS.loss_and_grads(h, w, tgt, lp + 0.1, adv, cfg.eps_low, cfg.eps_high,
+                       loss_scale=1.0 / max(n_rows, 1))
+    t_lp = time.perf_counter() - t0
+    lp_rate = 8.0 * cfg.vocab * cfg.hidden * n_rows / t_lp  # logits twice (logp + loss), dH, dW
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
-    return {"value": flop / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": (f"attention fwd+bwd of segment 0 ({sg.length} tokens, {pairs} visible "
-                       f"pairs), {nh} query heads / 1 kv head, d={cfg.head_dim}, float64 NumPy; "
-                       f"{dt:.1f} s"),
-            "seconds": dt}
-
-
-def _host_bf16_rows(gen, rows, dev, what, chunk=1 << 16):
-    """bf16 device tensor of generator rows, produced on the host in chunks
-    (no GPU kernel runs: the counter passes profile only the path's kernels)."""
-    import numpy as np
-    import torch
-
-    from paper_2607_11185_amd import workload as WL
-    first = gen(rows[:1])
-    out = np.empty((len(rows),) + first.shape[1:], np.uint16)
-    for c0 in range(0, len(rows), chunk):
-        x = gen(rows[c0:c0 + chunk])
-        out[c0:c0 + len(x)] = WL.bf16_round_np(x.astype(np.float32))
-        if (c0 // chunk) % 4 == 0:
-            log(f"  {what}: rows {c0 + len(x)}/{len(rows)}")
-    return torch.from_numpy(out).view(torch.bfloat16).to(dev)
+    out = {"value": attn_rate / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+           "sample": (f"attention fwd+bwd of {'every segment' if full else 'segment 0'} "
+                      f"({toks} tokens{', a prefix' if segs[0].length < ref.segments[0].length else ''}, "
+                      f"{pairs_done} visible pairs per head), {nh} query heads / "
+                      f"{nkv} kv head, d={cfg.head_dim}, {t_attn:.1f} s; log-prob loss with "
+                      f"gradients of {n_rows} action rows at vocab {cfg.vocab}, hidden "
+                      f"{cfg.hidden}, {t_lp:.1f} s; float64 NumPy"),
+           "seconds": round(t_attn + t_lp, 2)}
+    return out, attn_rate, lp_rate
 
 
 def pmc_driver(cfg_name):
-    """One launch of each attention kernel on the workload, then one launch
-    of the f32->bf16 conversion kernel over a known number of bytes (the
-    plain streaming kernel that calibrates the HBM byte counters).  Inputs
-    are generated on the host; prints one JSON line with the sizes."""
+    """One launch of the f32->bf16 conversion kernel over a known number of
+    bytes (the plain streaming kernel that calibrates the HBM byte counters),
+    then one step on the workload: every kernel of the path (the layout
+    build, attention forward, Delta, dK/dV, dQ, and the fused log-prob loss
+    with its gradients) runs last, so the last dispatch of each kernel name
+    (the last two of the transposed-operand GEMM: dH, then dW) is the step's.
+    The layout and the loss targets come from the workload; q, k, v, dO,
+    hidden states and the projection are drawn with torch.randn (a few large
+    launches, left out of the counter tables by name).  Prints one JSON line
+    with the sizes."""
     import numpy as np
     import torch
 
     from paper_2607_11185_amd import seg as S
     from paper_2607_11185_amd import workload as WL
     dev = torch.device("cuda:0")
-    cfg = WL.CONFIGS[cfg_name]
-    inp = WL.Inputs(cfg)
-    pr = S.Problem.from_spans(inp.spans, cfg.window, cfg.seg_steps, cfg.max_seg_tokens,
-                              cfg.buffer_tokens, 128, cfg.mode)
-    lay = S.seg_build_layout(pr, device=dev)
-    host = lay.host()
-    src = host["tok_src"].astype(np.int64)
-    src[src < 0] = 0
-    P = lay.sizes.packed_tokens
-    q = _host_bf16_rows(inp.q_np, src, dev, "q")
-    k = _host_bf16_rows(inp.k_np, src, dev, "k")
-    v = _host_bf16_rows(inp.v_np, src, dev, "v")
-    dout = _host_bf16_rows(inp.dout_np, np.arange(P), dev, "dout")
-    torch.cuda.synchronize()
-    log("inputs ready")
-    sc = 1.0 / math.sqrt(cfg.head_dim)
-    o, lse = S.seg_attn_fwd(lay, q, k, v, sc)
-    S.seg_attn_bwd(lay, q, k, v, o, lse, dout, sc)
-    torch.cuda.synchronize()
-    pairs = int(host["seg_pairs"].sum())
-    del q, k, v, dout, o, lse
-    torch.cuda.empty_cache()
     # calibration: 4096 one-turn samples of 256 tokens, 8 heads, d = 128, f32
     # inputs; the forward converts q, k and v with one streaming kernel each
     n_s, hc, d = 4096, 8, 128
@@ -336,10 +416,20 @@ def pmc_driver(cfg_name):
     kc = torch.from_numpy(zeros).to(dev)
     vc = torch.from_numpy(zeros).to(dev)
     torch.cuda.synchronize()
-    S.seg_attn_fwd(cal, qc, kc, vc, sc)
+    S.seg_attn_fwd(cal, qc, kc, vc, 1.0 / math.sqrt(d))
     torch.cuda.synchronize()
     n = Pc * hc * d
-    print(json.dumps({"config": cfg.name, "packed_tokens": P, "visible_pairs_per_head": pairs,
+    del qc, kc, vc, cal
+    torch.cuda.empty_cache()
+    cfg = WL.CONFIGS[cfg_name]
+    run = PathRun(cfg, dev, quick_inputs=True)
+    torch.cuda.synchronize()
+    log("inputs ready")
+    run.step()
+    torch.cuda.synchronize()
+    log("step done")
+    print(json.dumps({"config": cfg.name, "packed_tokens": run.sizes.packed_tokens,
+                      "loss_rows": run.sizes.loss_rows, "visible_pairs_per_head": run.pairs,
                       "calibration": {"kernel": "k_f32_to_bf16", "elements": n,
                                       "read_bytes": 4 * n, "write_bytes": 2 * n,
                                       "launches": 3}}), flush=True)
@@ -572,7 +662,7 @@ def main():
                     help="W = L = K sweep over K in (1, 3, 5, 8, 10, 15) on the workload "
                          "(one JSON line; not the bench line)")
     ap.add_argument("--pmc-driver", action="store_true",
-                    help="one launch of each attention kernel plus a calibration copy, for "
+                    help="one launch of each kernel of the step plus a calibration copy, for "
                          "rocprofv3 --pmc counter passes (no timing, no JSON bench line)")
     ap.add_argument("--layer", action="store_true",
                     help="training step of one full decoder layer (projections, RoPE, segmented "
@@ -609,16 +699,15 @@ def main():
     dev = torch.device("cuda:0")
     cfg = WL.CONFIGS[args.config]
 
-    seg = PathRun(cfg, dev)
-    ph, kern, wall_ms = time_path(seg, args.steps, args.warmup)
-    ref_seg = time_ref(seg, args.steps, args.warmup)
+    ph, kern, wall_ms, ref_seg, tot = time_groups(cfg, dev, args.steps, args.warmup)
     attn_ms = ph["attn_fwd"] + ph["attn_bwd"]
-    value = seg.attn_flop() / (attn_ms * 1e-3) / 1e12
-    traj_tokens = seg.sizes.traj_tokens
+    value = tot["flop"] / (attn_ms * 1e-3) / 1e12
+    traj_tokens = tot["traj_tokens"]
     # dominant attention kernel and its roofline from the live event timing
     dom = max(KERNEL_FLOP_PER_PAIR_D, key=lambda n: kern.get(n, {}).get("ms_per_step", 0.0))
-    dom_ms = kern[dom]["ms_per_step"] / kern[dom]["launches_per_step"]
-    dom_flop = KERNEL_FLOP_PER_PAIR_D[dom] * cfg.head_dim * seg.pairs * cfg.hq
+    launches = kern[dom]["launches_per_step"]
+    dom_ms = kern[dom]["ms_per_step"] / launches
+    dom_flop = KERNEL_FLOP_PER_PAIR_D[dom] * cfg.head_dim * tot["pairs"] * cfg.hq / launches
     achieved = dom_flop / (dom_ms * 1e-3) / 1e12
     cut = (f"anchored K={cfg.window} delta={cfg.seg_steps}" if cfg.mode == "anchored"
            else f"W={cfg.window}, L={cfg.seg_steps}")
@@ -633,12 +722,14 @@ def main():
                                f"{cfg.text_len[1]} (last {cfg.action_len} trained), {cut}, "
                                f"{cfg.hq}q/{cfg.hkv}kv heads, d={cfg.head_dim}, "
                                f"hidden {cfg.hidden}, vocab {cfg.vocab}, clip {cfg.eps_low}/"
-                               f"{cfg.eps_high}" + (f" cap {cfg.dual_clip}" if cfg.dual_clip else ""),
-                   "packed_tokens": seg.sizes.packed_tokens, "traj_tokens": traj_tokens,
-                   "segments": seg.sizes.num_segments, "visible_pairs_per_head": seg.pairs},
+                               f"{cfg.eps_high}" + (f" cap {cfg.dual_clip}" if cfg.dual_clip else "")
+                               + (f", {cfg.buffer_tokens}-token buffers" if cfg.buffer_tokens else ""),
+                   "packed_tokens": tot["packed"], "traj_tokens": traj_tokens,
+                   "segments": tot["segments"], "visible_pairs_per_head": tot["pairs"],
+                   "loss_rows": tot["loss_rows"]},
         "traj_tokens_per_s": round(traj_tokens / (ph["step"] * 1e-3), 1),
         "attn_ms": round(attn_ms, 3),
-        "attn_tflops_fa_convention": round(seg.attn_flop() * 14.0 / 12.0 / (attn_ms * 1e-3) / 1e12, 2),
+        "attn_tflops_fa_convention": round(tot["flop"] * 14.0 / 12.0 / (attn_ms * 1e-3) / 1e12, 2),
         "phases_ms": {k: round(v, 3) for k, v in ph.items()},
         "kernels_ms": {k: round(v["ms_per_step"], 3) for k, v in kern.items()},
         "wall_ms_per_step": round(wall_ms, 3),
@@ -650,34 +741,30 @@ def main():
         "kl_coef": KL_COEF,
         "reference_forward_ms": ref_seg,
     }
-    seg.free()
-    del seg
-    torch.cuda.empty_cache()
+    if tot["groups"] > 1:
+        out["config"]["trajectory_groups"] = tot["groups"]
 
     if not args.no_stepwise:
         # step-wise decomposition: one item per turn holding its K (or W)
-        # most recent screenshots
+        # most recent screenshots; trajectory groups when it does not fit
         sw_cfg = cfg.with_(name=cfg.name + "_stepwise", seg_steps=1, mode="sliding")
-        sw = PathRun(sw_cfg, dev)
-        ph2, kern2, _ = time_path(sw, args.steps, args.warmup)
-        ref_sw = time_ref(sw, args.steps, args.warmup)
+        ph2, kern2, _, ref_sw, tot2 = time_groups(sw_cfg, dev, args.steps, args.warmup)
         attn2 = ph2["attn_fwd"] + ph2["attn_bwd"]
         out["stepwise"] = {
             "ms_per_step": round(ph2["step"], 3),
             "traj_tokens_per_s": round(traj_tokens / (ph2["step"] * 1e-3), 1),
-            "attn_tflops": round(sw.attn_flop() / (attn2 * 1e-3) / 1e12, 2),
-            "attn_ms": round(attn2, 3), "packed_tokens": sw.sizes.packed_tokens,
-            "segments": sw.sizes.num_segments, "visible_pairs_per_head": sw.pairs,
+            "attn_tflops": round(tot2["flop"] / (attn2 * 1e-3) / 1e12, 2),
+            "attn_ms": round(attn2, 3), "packed_tokens": tot2["packed"],
+            "segments": tot2["segments"], "visible_pairs_per_head": tot2["pairs"],
             "phases_ms": {k: round(v, 3) for k, v in ph2.items()},
         }
+        if tot2["groups"] > 1:
+            out["stepwise"]["trajectory_groups"] = tot2["groups"]
         out["speedup_vs_stepwise"] = round(ph2["step"] / ph["step"], 3)
         out["stepwise"]["reference_forward_ms"] = ref_sw
         out["reference_forward_speedup_vs_stepwise"] = round(ref_sw["total"] / ref_seg["total"], 3)
-        sw.free()
-        del sw
-        torch.cuda.empty_cache()
 
-    if not args.no_layer and cfg.hidden == 3584:
+    if not args.no_layer and cfg.name in ("7b", "7b_anchored"):
         # one decoder layer around the attention (the next row past the hot
         # path), segmented vs step-wise, reported beside the bench numbers
         try:
@@ -694,7 +781,15 @@ def main():
         torch.cuda.empty_cache()
 
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, "")
+        cb, attn_rate, lp_rate = cpu_baseline(cfg)
+        # the oracle's step time for the whole batch at the sampled rates
+        # (extrapolated by FLOP counts; not a measurement of the whole batch)
+        R = out["config"]["loss_rows"]
+        t_or = tot["flop"] / attn_rate + 6.0 * cfg.vocab * cfg.hidden * R / lp_rate
+        cb["gpu_over_oracle_attn"] = round(value * 1e12 / attn_rate, 1)
+        cb["traj_tokens_per_s_extrapolated"] = round(traj_tokens / t_or, 3)
+        cb["step_seconds_extrapolated"] = round(t_or, 1)
+        out["cpu_baseline"] = cb
     print(json.dumps(out), flush=True)
 
 
