@@ -68,8 +68,10 @@ enum {
 /*
  * A batch of trajectories (all arrays host memory, read during the call).
  * Turns of trajectory i are steps [step_offsets[i], step_offsets[i+1]), numbered
- * 1..T inside the trajectory.  prompt_len >= 1; img_len, text_len >= 0;
+ * 1..T inside the trajectory.  prompt_len, img_len, text_len >= 0;
  * 0 <= action_len <= text_len.  A trajectory with no turns yields no segment.
+ * A segment without tokens, or one whose first token is a trained token (no
+ * row before it predicts it, Eq. (loss)), is an argument error.
  *
  * Segmentation (Sec. 3.3, App. D; the segment length L plays the removal
  * threshold Delta and W the kept-screenshot count K):
@@ -129,7 +131,8 @@ typedef struct {
 /*
  * Device arrays of a layout, sized from seg_sizes (S segments, P packed rows,
  * R loss rows, G q-tiles, Z = tile_nnz_max).  Filled by seg_build_layout, which
- * also sets the scalars `window` and `tile`.
+ * also sets the scalars `window` and `tile` and the launch schedule
+ * (`xcd_rows`, `xcd_cols`) of the attention kernels.
  */
 typedef struct {
   int32_t *seg_info;      /* [S*8] see SEG_INFO_*; turns are 1-based, segments in packed order */
@@ -151,6 +154,13 @@ typedef struct {
                              attention kernels apply (W; SEG_WINDOW_ANCHORED,
                              larger than any turn index, in the anchored mode) */
   int32_t tile;           /* set by seg_build_layout */
+  /* Set by seg_build_layout (host values): tile boundaries of the eight
+   * ranges the attention kernels give to the chip's eight dies (XCDs, each
+   * with its own L2), xcd_rows for the forward and dQ passes balanced by the
+   * tiles' listed k-tiles, xcd_cols for the dK/dV pass balanced by their
+   * listed q-tiles; [0] = 0, [8] = number of tiles, non-decreasing. */
+  int32_t xcd_rows[9];
+  int32_t xcd_cols[9];
 } seg_layout;
 
 /* Sizes of the layout of `p` (host only, no HIP call).  Errors: SEG_ERR_ARG for

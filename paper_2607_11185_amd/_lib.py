@@ -60,7 +60,8 @@ class SegLayout(ctypes.Structure):
                 ("loss_tgt_src", VP), ("loss_traj", VP), ("tile_seg", VP), ("qt_ptr", VP),
                 ("qt_col", VP), ("qt_cls", VP), ("kt_ptr", VP), ("kt_row", VP), ("kt_cls", VP),
                 ("seg_pairs", VP), ("tile_nnz", VP),
-                ("window", ctypes.c_int32), ("tile", ctypes.c_int32)]
+                ("window", ctypes.c_int32), ("tile", ctypes.c_int32),
+                ("xcd_rows", ctypes.c_int32 * 9), ("xcd_cols", ctypes.c_int32 * 9)]
 
 
 class SegLossCfg(ctypes.Structure):

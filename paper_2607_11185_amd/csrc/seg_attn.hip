@@ -292,23 +292,39 @@ __device__ __forceinline__ float sum8(const bf16x8 &v, float acc) {
 
 // XCD-aware block mapping.  Blocks are dispatched round-robin over the 8
 // XCDs (block b runs on XCD b % 8), each with its own L2.  XCD x takes the
-// contiguous tile range [x*C, (x+1)*C), C = ceil(ntiles / 8), and runs the nh
-// heads of one tile back to back: heads of a tile read the same key/value
-// tiles, and neighbouring tiles of a segment read mostly the same ones, so
-// they meet in one L2.  Each range holds several whole segments, which keeps
-// the XCDs balanced.  `reverse` walks the range from its end (the longest
-// rows of each segment first).  The grid is 8*C*nh blocks; blocks past the
-// last tile exit at once.
-__device__ __forceinline__ bool xcd_block(int nh, int ntiles, bool reverse, int &tile, int &head) {
-  const int b = blockIdx.x, x = b & 7, i = b >> 3;
-  const int C = (ntiles + 7) >> 3;
+// contiguous tile range [r.b[x], r.b[x+1]) chosen by the layout so that the
+// ranges hold about equal work (the kernel ends with the slowest XCD), and
+// runs the nh heads of one tile back to back: heads of a tile read the same
+// key/value tiles, and neighbouring tiles of a segment read mostly the same
+// ones, so they meet in one L2.  `reverse` walks the range from its end (the
+// longest rows of each segment first).  The grid is 8 * max range * nh
+// blocks; blocks past their XCD's range exit at once.
+struct XcdRanges {
+  int32_t b[9];
+};
+
+__device__ __forceinline__ bool xcd_block(const XcdRanges &r, int nh, bool reverse, int &tile,
+                                          int &head) {
+  const int bx = blockIdx.x, x = bx & 7, i = bx >> 3;
+  const int lo = r.b[x], C = r.b[x + 1] - lo;
   const int t = i / nh;
+  if (t >= C) return false;
   head = i - t * nh;
-  tile = x * C + (reverse ? C - 1 - t : t);
-  return tile < ntiles;
+  tile = lo + (reverse ? C - 1 - t : t);
+  return true;
 }
 
-__host__ __device__ inline int xcd_grid(int ntiles, int nh) { return (ntiles + 7) / 8 * 8 * nh; }
+inline XcdRanges xcd_ranges(const int32_t (&b)[9]) {
+  XcdRanges r;
+  for (int i = 0; i < 9; ++i) r.b[i] = b[i];
+  return r;
+}
+
+inline int xcd_grid(const XcdRanges &r, int nh) {
+  int c = 0;
+  for (int x = 0; x < 8; ++x) c = std::max(c, r.b[x + 1] - r.b[x]);
+  return std::max(1, 8 * c * nh);
+}
 
 // A unit of work: 64 rows (half of a 128-row tile) of the tile listed at CSR
 // entry e.
@@ -359,14 +375,14 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd(
     const unsigned short *__restrict__ v, const int32_t *__restrict__ seg_info,
     const int32_t *__restrict__ tile_seg, const int32_t *__restrict__ tok_meta,
     const int32_t *__restrict__ qt_ptr, const int32_t *__restrict__ qt_col,
-    const uint8_t *__restrict__ qt_cls, int ntiles, int hq, int hkv, int W, float scale_log2,
-    long P, TO *__restrict__ o, float *__restrict__ lse) {
+    const uint8_t *__restrict__ qt_cls, const XcdRanges xr, int hq, int hkv, int W,
+    float scale_log2, long P, TO *__restrict__ o, float *__restrict__ lse) {
   constexpr int KK = D / 16, DB = D / 32, T64 = 64 * D;
   __shared__ __attribute__((aligned(16))) unsigned short sK0[T64], sK1[T64], sV0[T64], sV1[T64];
   __shared__ __attribute__((aligned(16))) int sM0[64], sM1[64];
 
   int g, h;
-  if (!xcd_block(hq, ntiles, true, g, h)) return;
+  if (!xcd_block(xr, hq, true, g, h)) return;
   const int hk = h / (hq / hkv);
   const TileRows tr = tile_rows(seg_info, tile_seg, g);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -546,9 +562,9 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
     const float *__restrict__ lse2, const float *__restrict__ delta,
     const int32_t *__restrict__ seg_info, const int32_t *__restrict__ tile_seg,
     const int32_t *__restrict__ tok_meta, const int32_t *__restrict__ kt_ptr,
-    const int32_t *__restrict__ kt_row, const uint8_t *__restrict__ kt_cls, int ntiles, int hq,
-    int hkv, int W, float scale_log2, float scale, long P, TO *__restrict__ dk,
-    TO *__restrict__ dv) {
+    const int32_t *__restrict__ kt_row, const uint8_t *__restrict__ kt_cls, const XcdRanges xr,
+    int hq, int hkv, int W,
+    float scale_log2, float scale, long P, TO *__restrict__ dk, TO *__restrict__ dv) {
   constexpr int KK = D / 16, T64 = 64 * D, DB = D / 32, NB = 3;
   __shared__ __attribute__((aligned(16))) unsigned short sQ[NB][T64], sD[NB][T64];
   __shared__ __attribute__((aligned(16))) unsigned short sP[2][64 * TQ];
@@ -557,13 +573,17 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
 
   int g, hk;
   {
-    // XCD x takes tiles [x*C, (x+1)*C) and runs them kv head by kv head, so
-    // the blocks resident on one XCD read the same query heads
+    // XCD x takes the tiles of its range in order and runs them kv head by
+    // kv head, so the blocks resident on one XCD are neighbouring k-tiles of
+    // one kv head: they walk the same q-tiles of a segment and share their
+    // Q/dO tiles in L2 (ordering the range longest column first instead mixes
+    // segments and was 7% slower)
     const int bx = blockIdx.x, x = bx & 7, i = bx >> 3;
-    const int C = (ntiles + 7) >> 3;
+    const int lo = xr.b[x], C = xr.b[x + 1] - lo;
+    if (C == 0) return;
     hk = i / C;
-    g = x * C + (i - hk * C);
-    if (g >= ntiles || hk >= hkv) return;
+    if (hk >= hkv) return;
+    g = lo + (i - hk * C);
   }
   const int grp = hq / hkv;
   const TileRows tr = tile_rows(seg_info, tile_seg, g);
@@ -844,14 +864,14 @@ __global__ void __launch_bounds__(256, 2) k_attn_bwd_dq(
     const float *__restrict__ lse2, const float *__restrict__ delta,
     const int32_t *__restrict__ seg_info, const int32_t *__restrict__ tile_seg,
     const int32_t *__restrict__ tok_meta, const int32_t *__restrict__ qt_ptr,
-    const int32_t *__restrict__ qt_col, const uint8_t *__restrict__ qt_cls, int ntiles, int hq,
-    int hkv, int W, float scale_log2, float scale, long P, TO *__restrict__ dq) {
+    const int32_t *__restrict__ qt_col, const uint8_t *__restrict__ qt_cls, const XcdRanges xr,
+    int hq, int hkv, int W, float scale_log2, float scale, long P, TO *__restrict__ dq) {
   constexpr int KK = D / 16, DB = D / 32, T64 = 64 * D;
   __shared__ __attribute__((aligned(16))) unsigned short sK0[T64], sK1[T64], sV0[T64], sV1[T64];
   __shared__ __attribute__((aligned(16))) int sM0[64], sM1[64];
 
   int g, h;
-  if (!xcd_block(hq, ntiles, true, g, h)) return;
+  if (!xcd_block(xr, hq, true, g, h)) return;
   const int hk = h / (hq / hkv);
   const TileRows tr = tile_rows(seg_info, tile_seg, g);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -1028,6 +1048,12 @@ void check_common(const seg_layout *L, const seg_sizes *sz, seg_dtype dt, int hq
   SEG_CHECK(L->tile == TQ, SEG_ERR_UNSUPPORTED, "attention needs a layout with tile 128 (got %d)",
             L->tile);
   SEG_CHECK(L->window >= 1, SEG_ERR_ARG, "layout window not set (build the layout first)");
+  // the launch schedule: eight ranges covering every tile once
+  for (const int32_t *b : {L->xcd_rows, L->xcd_cols}) {
+    bool ok = b[0] == 0 && b[8] == sz->num_qtiles;
+    for (int x = 0; x < 8; ++x) ok = ok && b[x] <= b[x + 1];
+    SEG_CHECK(ok, SEG_ERR_ARG, "layout schedule ranges not set (build the layout first)");
+  }
   SEG_CHECK((long)sz->packed_tokens * hq * d < (1L << 40), SEG_ERR_CAPACITY, "tensor too large");
   // tile loads address a segment's rows, and the per-row values of a head
   // group, with 32-bit byte offsets from one buffer resource
@@ -1051,9 +1077,10 @@ void fwd_impl(const seg_layout *L, const seg_sizes *sz, int hq, int hkv, float s
               float *lse, hipStream_t st) {
   const int G = sz->num_qtiles;
   ProfScope prof("attn_fwd", st);
-  k_attn_fwd<D, TO><<<xcd_grid(G, hq), 256, 0, st>>>(
+  const XcdRanges xr = xcd_ranges(L->xcd_rows);
+  k_attn_fwd<D, TO><<<xcd_grid(xr, hq), 256, 0, st>>>(
       q, k, v, L->seg_info, L->tile_seg, L->tok_meta, L->qt_ptr, L->qt_col, L->qt_cls,
-      G, hq, hkv, L->window, scale * LOG2E, sz->packed_tokens, static_cast<TO *>(o), lse);
+      xr, hq, hkv, L->window, scale * LOG2E, sz->packed_tokens, static_cast<TO *>(o), lse);
   SEG_LAUNCH_CHECK();
 }
 
@@ -1074,16 +1101,18 @@ void bwd_impl(const seg_layout *L, const seg_sizes *sz, int hq, int hkv, float s
   }
   {
     ProfScope prof("attn_bwd_dkdv", st);
-    k_attn_bwd_dkdv<D, TO><<<xcd_grid(G, hkv), 512, 0, st>>>(
+    const XcdRanges xc = xcd_ranges(L->xcd_cols);
+    k_attn_bwd_dkdv<D, TO><<<xcd_grid(xc, hkv), 512, 0, st>>>(
         q, k, v, dout, lse2, delta, L->seg_info, L->tile_seg, L->tok_meta, L->kt_ptr, L->kt_row,
-        L->kt_cls, G, hq, hkv, L->window, scale * LOG2E, scale, P, static_cast<TO *>(dk),
-        static_cast<TO *>(dv));
+        L->kt_cls, xc, hq, hkv, L->window, scale * LOG2E, scale, P,
+        static_cast<TO *>(dk), static_cast<TO *>(dv));
     SEG_LAUNCH_CHECK();
   }
   ProfScope prof("attn_bwd_dq", st);
-  k_attn_bwd_dq<D, TO><<<xcd_grid(G, hq), 256, 0, st>>>(
+  const XcdRanges xr = xcd_ranges(L->xcd_rows);
+  k_attn_bwd_dq<D, TO><<<xcd_grid(xr, hq), 256, 0, st>>>(
       q, k, v, dout, lse2, delta, L->seg_info, L->tile_seg, L->tok_meta, L->qt_ptr, L->qt_col,
-      L->qt_cls, G, hq, hkv, L->window, scale * LOG2E, scale, P, static_cast<TO *>(dq));
+      L->qt_cls, xr, hq, hkv, L->window, scale * LOG2E, scale, P, static_cast<TO *>(dq));
   SEG_LAUNCH_CHECK();
 }
 

@@ -53,7 +53,63 @@ struct Plan {
   std::vector<Piece> pieces;
   std::vector<LossPiece> lpieces;
   int32_t max_nt = 0;
+  // launch schedule of the attention kernels (see seg_layout)
+  std::vector<int32_t> row_work, col_work;  // [G] listed k-tiles / q-tiles of each tile
+  int32_t xcd_rows[9] = {}, xcd_cols[9] = {};
 };
+
+// Listed partners of every tile of one segment, from its token runs.  Turns
+// never decrease along a segment, so a q-tile's most permissive row is its
+// first one; a k-tile's most permissive key is the one that expires last
+// (text and prompt never do, a screenshot of turn s at turn s + Wv).  An
+// off-diagonal pair (q-tile i > k-tile j) holds a visible pair iff the first
+// row's turn of i is below the latest expiry in j, so k-tile j is listed by the
+// contiguous q-tiles j .. r_j - 1 (the diagonal always).
+void tile_work(const Piece *pc, int npc, int len, int tile, int Wv, int32_t *row_w,
+               int32_t *col_w) {
+  const int n = (len + tile - 1) / tile;
+  std::vector<int64_t> first_turn(n), last_exp(n, INT64_MIN);
+  int k = 0;
+  for (int t = 0; t < n; ++t) {
+    const int r0 = t * tile, r1 = std::min(len, r0 + tile);
+    while (k + 1 < npc && pc[k + 1].off <= r0) ++k;
+    first_turn[t] = pc[k].meta >> 2;
+    for (int i = k; i < npc && pc[i].off < r1; ++i) {
+      if (pc[i].len == 0 || pc[i].off + pc[i].len <= r0) continue;
+      const int kind = pc[i].meta & 3;
+      const int64_t e = kind == SEG_KIND_IMAGE ? (int64_t)(pc[i].meta >> 2) + Wv : INT64_MAX;
+      last_exp[t] = std::max(last_exp[t], e);
+    }
+  }
+  std::vector<int32_t> diff(n + 1, 0);
+  for (int j = 0; j < n; ++j) {
+    // first q-tile after j whose first row's turn has reached the expiry
+    const int r = (int)(std::lower_bound(first_turn.begin() + j + 1, first_turn.end(), last_exp[j]) -
+                        first_turn.begin());
+    col_w[j] = r - j;
+    diff[j + 1] += 1;
+    diff[r] -= 1;
+  }
+  int run = 0;
+  for (int i = 0; i < n; ++i) {
+    run += diff[i];
+    row_w[i] = 1 + run;
+  }
+}
+
+// Boundaries of eight consecutive tile ranges with about equal total work.
+void balance8(const std::vector<int32_t> &w, int32_t *b) {
+  const int G = (int)w.size();
+  std::vector<int64_t> pre(G + 1, 0);
+  for (int g = 0; g < G; ++g) pre[g + 1] = pre[g] + w[g];
+  b[0] = 0;
+  for (int x = 1; x < 8; ++x) {
+    const int64_t target = (pre[G] * x + 7) / 8;
+    b[x] = (int32_t)(std::lower_bound(pre.begin(), pre.end(), target) - pre.begin());
+    b[x] = std::max(b[x], b[x - 1]);
+  }
+  b[8] = G;
+}
 
 // Byte offsets of the build workspace regions.
 struct BuildWs {
@@ -255,6 +311,18 @@ Plan make_plan(const seg_problem *p) {
   }
   sz.num_qtiles = (int32_t)qbase;
   sz.tile_nnz_max = tri;
+  // launch schedule: per-tile work and eight balanced tile ranges per pass
+  {
+    const int Wv = anchored ? SEG_WINDOW_ANCHORED : p->window;
+    const int G = (int)qbase;
+    pl.row_work.assign(G, 0);
+    pl.col_work.assign(G, 0);
+    for (const DevSeg &d : pl.dsegs)
+      tile_work(pl.pieces.data() + d.piece_base, d.piece_count, d.len, tile, Wv,
+                pl.row_work.data() + d.qbase, pl.col_work.data() + d.qbase);
+    balance8(pl.row_work, pl.xcd_rows);
+    balance8(pl.col_work, pl.xcd_cols);
+  }
   sz.loss_rows = (int32_t)rows;
   sz.workspace_bytes = build_ws_layout(sz, pl.pieces.size(), pl.lpieces.size()).total;
   return pl;
@@ -504,6 +572,8 @@ extern "C" seg_status seg_build_layout(const seg_problem *p, const seg_sizes *sz
     const int Wv = p->mode == SEG_MODE_ANCHORED ? SEG_WINDOW_ANCHORED : p->window;
     out->window = Wv;
     out->tile = p->tile;
+    std::memcpy(out->xcd_rows, pl.xcd_rows, sizeof(pl.xcd_rows));
+    std::memcpy(out->xcd_cols, pl.xcd_cols, sizeof(pl.xcd_cols));
     const int S = sz->num_segments, G = sz->num_qtiles, R = sz->loss_rows;
     const int P = (int)sz->packed_tokens;
     if (S > 0) {

@@ -119,6 +119,8 @@ class Layout:
                 "seg_pairs": s.num_segments, "tile_nnz": 1}
         out = {f: getattr(self, f)[:lens[f]].cpu().numpy() for f in self.FIELDS}
         out["seg_info"] = out["seg_info"].reshape(-1, 8)
+        out["xcd_rows"] = np.array(self.c.xcd_rows[:], np.int64)
+        out["xcd_cols"] = np.array(self.c.xcd_cols[:], np.int64)
         return out
 
 

@@ -158,6 +158,18 @@ def test_build_and_compute_reject_bad_args_before_any_launch():
                         None, None, None, 1 << 40, None)
     assert st == _lib.SEG_ERR_UNSUPPORTED
     lay.tile = 128
+    # a layout whose launch schedule was not set by seg_build_layout
+    st = L.seg_attn_bwd(ctypes.byref(lay), ctypes.byref(sz), 0, 4, 1, 64, 0.1, None, None, None,
+                        None, None, None, None, None, None, None, 0, None)
+    assert st == _lib.SEG_ERR_ARG and b"schedule" in L.seg_last_error()
+    G = sz.num_qtiles
+    for x in range(9):
+        lay.xcd_rows[x] = lay.xcd_cols[x] = G * x // 8
+    lay.xcd_cols[3], lay.xcd_cols[4] = lay.xcd_cols[4], lay.xcd_cols[3]   # not monotonic
+    st = L.seg_attn_bwd(ctypes.byref(lay), ctypes.byref(sz), 0, 4, 1, 64, 0.1, None, None, None,
+                        None, None, None, None, None, None, None, 0, None)
+    assert st == _lib.SEG_ERR_ARG
+    lay.xcd_cols[3], lay.xcd_cols[4] = lay.xcd_cols[4], lay.xcd_cols[3]
     st = L.seg_attn_bwd(ctypes.byref(lay), ctypes.byref(sz), 0, 4, 1, 64, 0.1, None, None, None,
                         None, None, None, None, None, None, None, 0, None)
     assert st == _lib.SEG_ERR_WORKSPACE
@@ -188,6 +200,8 @@ def test_noalloc_backward_rejects_before_any_launch():
     sz = S.seg_layout_query(_prob())
     lay = _lib.SegLayout()
     lay.tile, lay.window = 128, 2
+    for x in range(9):
+        lay.xcd_rows[x] = lay.xcd_cols[x] = sz.num_qtiles * x // 8
     big = _lib.SegSizes.from_buffer_copy(sz)
     hq, hkv, d = 28, 4, 128
     big.packed_tokens = _lib.SEG_ATTN_BWD_SCRATCH_BYTES // (8 * hq) + 256

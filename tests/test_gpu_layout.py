@@ -22,12 +22,33 @@ def _gpu(sp, W, L, tile, cap=0, buf=0, mode="sliding"):
     return S.seg_build_layout(pr, device="cuda").host()
 
 
+def _balance8(work):
+    """Boundaries of eight consecutive ranges of about equal total work: the
+    first index whose prefix reaches ceil(total * x / 8)."""
+    pre = np.concatenate([[0], np.cumsum(work)]).astype(np.int64)
+    b = [0]
+    for x in range(1, 8):
+        b.append(max(int(np.searchsorted(pre, (pre[-1] * x + 7) // 8, "left")), b[-1]))
+    return b + [len(work)]
+
+
+def _check_schedule(got):
+    """The attention launch schedule, recomputed from the layout's own CSR
+    lengths (listed k-tiles per q-tile, listed q-tiles per k-tile): the
+    host's balanced tile ranges must be what the GPU's tile map gives."""
+    rows, cols = np.diff(got["qt_ptr"]), np.diff(got["kt_ptr"])
+    assert got["xcd_rows"].tolist() == _balance8(rows)
+    assert got["xcd_cols"].tolist() == _balance8(cols)
+
+
 def _check_all(got, ref):
     for f in ("tok_src", "tok_meta", "loss_pred_row", "loss_tgt_src", "loss_traj", "tile_seg",
               "qt_ptr", "qt_col", "qt_cls", "kt_ptr", "kt_row", "kt_cls", "seg_pairs"):
         assert np.array_equal(got[f].astype(np.int64), getattr(ref, f).astype(np.int64)), f
     assert np.array_equal(got["seg_info"].astype(np.int64), ref.seg_info), "seg_info"
     assert int(got["tile_nnz"][0]) == len(ref.qt_col)
+    if len(got["qt_ptr"]) > 1:
+        _check_schedule(got)
 
 
 @pytest.mark.parametrize("name", ["appA_example_a.json", "appA_example_b.json"])
@@ -104,6 +125,7 @@ def test_configs_large_sampled(cfg):
     for f in ("tok_src", "tok_meta", "loss_pred_row", "loss_tgt_src", "loss_traj"):
         assert np.array_equal(got[f].astype(np.int64), getattr(ref, f).astype(np.int64)), f
     assert np.array_equal(got["seg_info"].astype(np.int64), ref.seg_info)
+    _check_schedule(got)
     S_ = len(ref.segments)
     lens = [sg.length for sg in ref.segments]
     picks = sorted({0, S_ // 2, S_ - 1, int(np.argmax(lens))})
