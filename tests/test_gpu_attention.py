@@ -47,6 +47,9 @@ CASES = {
     # no prompt: rows whose first listed 64-key unit is an expired screenshot
     # (fully masked for them) and whose first visible key comes later
     "med_no_prompt": MED.with_(prompt_len=0, seed=19, steps=(5, 7)),
+    # fewer tiles than the chip's eight dies: most launch-schedule ranges are
+    # empty (one trajectory of two turns, a single 2-tile segment)
+    "few_tiles": MED.with_(num_traj=1, steps=(2, 2), seed=20),
     "tiny": WL.TINY,
 }
 RAMPED = {"med_ramped_keys"}
