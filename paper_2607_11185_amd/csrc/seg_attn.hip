@@ -629,10 +629,14 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
   const __amdgpu_buffer_rsrc_t rO = make_rsrc(dout + hbase, qbytes);
   const long pbase = (long)hk * grp * P + tr.start;
   const unsigned pbytes = (unsigned)(((long)(grp - 1) * P + tr.len) * 4);
-  const __amdgpu_buffer_rsrc_t rS = make_rsrc(wave == 0 ? (const void *)(lse2 + pbase)
-                                              : wave == 1 ? (const void *)(delta + pbase)
-                                                          : (const void *)(tok_meta + tr.start),
-                                              wave < 2 ? pbytes : (unsigned)tr.len * 4);
+  // the wave index as a scalar: the resource is then built in scalar
+  // registers (a resource held in vector registers needs a waterfall loop
+  // around every load)
+  const int swave = __builtin_amdgcn_readfirstlane(wave);
+  const __amdgpu_buffer_rsrc_t rS = make_rsrc(swave == 0 ? (const void *)(lse2 + pbase)
+                                              : swave == 1 ? (const void *)(delta + pbase)
+                                                           : (const void *)(tok_meta + tr.start),
+                                              swave < 2 ? pbytes : (unsigned)tr.len * 4);
   u16x8 stq[PW], sto[PW];
   int stv = 0, st_vrows = 0;
   auto load = [&](int r0, int vrows, int hi) __attribute__((always_inline)) {
@@ -647,9 +651,9 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
     // were never computed): rows past the unit's valid rows are replaced by
     // zeros when stored, so no non-finite value can reach dS = P (dP - Delta)
     // through a masked P = 0.
-    if (wave < 3)
+    if (swave < 3)
       stv = __builtin_amdgcn_raw_buffer_load_b32(rS, lane * 4,
-                                                 (wave < 2 ? hi * (int)P * 4 : 0) + r0 * 4, 0);
+                                                 (swave < 2 ? hi * (int)P * 4 : 0) + r0 * 4, 0);
     st_vrows = vrows;
   };
   auto store = [&](int b) __attribute__((always_inline)) {
