@@ -3,7 +3,9 @@ against the float64 oracle.
 
 Full parity on workloads the oracle finishes in seconds (several tiles per
 segment, ragged tails, GQA ratios, head_dim 64 and 128, fp32 inputs,
-buffer padding); sampled rows plus exact identities at the 7B-class size;
+buffer padding) and on ten seeded random shapes (span lengths, empty
+prompts, window, segment length, head shape, buffers, anchored mode);
+sampled rows plus exact identities at the 7B-class size;
 bitwise run-to-run determinism; and the segment == step-wise invariant of
 the action rows (Sec. 3.3)."""
 import math
@@ -117,7 +119,44 @@ def _ref_layout(run):
 
 @pytest.mark.parametrize("name", list(CASES))
 def test_fwd_bwd_full_parity(name):
-    cfg = CASES[name]
+    _full_parity(name, CASES[name])
+
+
+def _random_config(i):
+    """Seeded random workload of a few thousand packed rows: trajectory count,
+    turn counts, prompt (possibly empty), span lengths, window and segment
+    length, head shape (GQA ratios 1-7, d 64 or 128), buffer packing and the
+    anchored mode all drawn from one generator per case."""
+    rng = np.random.default_rng(1000 + i)
+    hq, hkv, d = [(2, 1, 64), (4, 2, 128), (8, 8, 64), (6, 3, 128), (7, 1, 128),
+                  (14, 2, 64)][rng.integers(6)]
+    lo = int(rng.integers(1, 6))
+    t_lo = int(rng.integers(1, 60))
+    cfg = MED.with_(name=f"random{i}", num_traj=int(rng.integers(1, 4)),
+                    steps=(lo, lo + int(rng.integers(0, 4))),
+                    prompt_len=int(rng.choice([0, int(rng.integers(1, 200))])),
+                    img_len=int(rng.integers(1, 260)),
+                    text_len=(t_lo, t_lo + int(rng.integers(0, 120))),
+                    action_len=int(rng.integers(0, t_lo + 1)),
+                    window=int(rng.integers(1, 6)), seg_steps=int(rng.integers(1, 6)),
+                    hq=hq, hkv=hkv, head_dim=d, seed=2000 + i,
+                    mode="anchored" if rng.random() < 0.25 else "sliding")
+    if cfg.mode == "sliding" and rng.random() < 0.4:
+        # buffer packing: room for the longest segment plus a random slack
+        ref = OL.build(WL.Inputs(cfg).spans, cfg.window, cfg.seg_steps, 128, with_tiles=False)
+        longest = max(sg.length for sg in ref.segments)
+        cfg = cfg.with_(buffer_tokens=longest + int(rng.integers(0, 700)))
+    return cfg
+
+
+@pytest.mark.parametrize("i", range(10))
+def test_random_shapes_full_parity(i):
+    cfg = _random_config(i)
+    say(f"random case {i}: {cfg}")
+    _full_parity(cfg.name, cfg)
+
+
+def _full_parity(name, cfg):
     say(f"case {name}")
     import torch
     run = GpuRun(cfg).packed_inputs()
