@@ -1,7 +1,9 @@
 """GPU fused log-prob + clipped-ratio loss with its KL penalty
 (seg_logprob_loss through the C ABI) against the float64 oracle (Eq. loss):
-full parity on the tiny and small heads (also with the KL penalty on), the
-7B-class head at full vocabulary and hidden size on a reduced row count, and
+full parity on the tiny and small heads (also with the KL penalty on), on
+eight seeded random problems (rows, hidden, vocabulary, clip range, dual
+clip, KL, input dtype), the 7B-class head at full vocabulary and hidden size
+on a reduced row count, and
 the full 7B-class row count on sampled rows plus the identity
 sum_v dW[v] = 0 (each dz row sums to zero)."""
 import numpy as np
@@ -73,6 +75,40 @@ def _full_case(cfg, dual=0.0, want_grad=True, kl=None):
 def test_full_parity(cfg, dual):
     say(f"logprob {cfg.name} dual={dual}")
     run, ref, out, old = _full_case(cfg, dual)
+    _check_full(run, ref, out, old, cfg, dual, both_branches=True)
+
+
+def _random_case(i):
+    """Seeded random loss problem: row count (through turn and action
+    counts), hidden size, vocabulary, clip range (possibly asymmetric), dual
+    clip, KL penalty and logit dtype drawn from one generator per case."""
+    rng = np.random.default_rng(3000 + i)
+    hidden = 8 * int(rng.integers(1, 97))
+    cfg = WL.TINY.with_(name=f"lp_random{i}", num_traj=int(rng.integers(1, 4)),
+                        steps=(1, int(rng.integers(1, 9))), text_len=(40, 40),
+                        action_len=int(rng.integers(1, 33)), hidden=hidden,
+                        vocab=int(rng.integers(1, 6000)),
+                        eps_low=float(rng.uniform(0.05, 0.3)), eps_high=float(rng.uniform(0.05, 0.3)),
+                        old_noise_std=float(rng.uniform(0.05, 0.4)),
+                        dtype="bf16" if rng.random() < 0.7 else "f32", seed=4000 + i)
+    dual = float(rng.uniform(1.5, 3.5)) if rng.random() < 0.4 else 0.0
+    kl = float(rng.uniform(1e-4, 0.1)) if rng.random() < 0.5 else None
+    return cfg, dual, kl
+
+
+@pytest.mark.parametrize("i", range(8))
+def test_random_shapes_parity(i):
+    cfg, dual, kl = _random_case(i)
+    say(f"logprob random case {i}: hidden={cfg.hidden} vocab={cfg.vocab} dtype={cfg.dtype} "
+        f"eps=({cfg.eps_low:.3f},{cfg.eps_high:.3f}) dual={dual} kl={kl}")
+    run, ref, out, old = _full_case(cfg, dual, kl=kl)
+    _check_full(run, ref, out, old, cfg, dual, both_branches=False)
+    if kl is not None:
+        R = run.lay.sizes.loss_rows
+        assert rel(out["loss_tok"][:R].cpu().numpy(), ref["loss_tok"]) < TOL
+
+
+def _check_full(run, ref, out, old, cfg, dual, both_branches):
     R = run.lay.sizes.loss_rows
     logp = out["logp"][:R].cpu().numpy()
     assert np.abs(logp - ref["logp"]).max() < 2e-2 * max(1.0, np.abs(ref["logp"]).max())
@@ -99,7 +135,8 @@ def test_full_parity(cfg, dual):
     flips = cl != ref["clipped"]
     say(f"  clip flags differing from the oracle: {int(flips.sum())} of {R}")
     assert near(lr_ref, err + 1e-5)[flips].all()
-    assert ref["clipped"].any() and (~ref["clipped"]).any()
+    if both_branches:
+        assert ref["clipped"].any() and (~ref["clipped"]).any()
     assert abs(float(out["loss_sum"][0]) - ref["loss_sum"]) < TOL * max(1e-3, abs(ref["loss_sum"]))
     e_dh = rel(out["dh"][:R].float().cpu().numpy(), ref["dh"])
     e_dw = rel(out["dw"].cpu().numpy(), ref["dw"])
