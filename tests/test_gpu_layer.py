@@ -5,7 +5,9 @@ Full parity of the outputs, the saved activations, dx and every weight
 gradient on workloads the oracle finishes in seconds: several segments of
 several 128-row tiles with ragged tails, hidden and MLP widths that are not
 multiples of the GEMM tile, head_dim 64 and 128, buffer padding, row chunking
-smaller than the batch.  Plus: chunking leaves the row-wise results bitwise
+smaller than the batch; six seeded random problems (widths, head shape,
+window, segment length, buffers, chunking, mode).  Plus: chunking leaves the
+row-wise results bitwise
 unchanged, padding rows get no gradient, and an empty batch gives zero
 weight gradients.  At the 7B-class layer width (hidden 3584, MLP 18944,
 28q/4kv): sampled output rows against the oracle's row-sampled forward, and
@@ -106,6 +108,34 @@ def test_layer_wide_gemm_parity():
     lr = _full_parity("wide", cfg, H, I, 0)
     assert _big_tiles(lr.P, H) >= 192 and _big_tiles(lr.P, I) >= 192
     assert _big_tiles(lr.P, cfg.hq * cfg.head_dim) >= 192
+
+
+def _random_layer_case(i):
+    """Seeded random layer problem: widths (multiples of 8 only), head shape,
+    segment window and length, buffers, row chunking and mode drawn from one
+    generator per case."""
+    rng = np.random.default_rng(5000 + i)
+    hq, hkv, d = [(2, 1, 64), (4, 2, 128), (6, 6, 64), (7, 1, 128), (8, 2, 64)][rng.integers(5)]
+    cfg = MED.with_(num_traj=int(rng.integers(1, 3)), steps=(2, 2 + int(rng.integers(0, 3))),
+                    prompt_len=int(rng.integers(0, 120)), img_len=int(rng.integers(1, 200)),
+                    text_len=(20, 20 + int(rng.integers(0, 100))), action_len=4,
+                    window=int(rng.integers(1, 4)), seg_steps=int(rng.integers(1, 4)),
+                    hq=hq, hkv=hkv, head_dim=d, seed=6000 + i,
+                    mode="anchored" if rng.random() < 0.2 else "sliding")
+    if cfg.mode == "sliding" and rng.random() < 0.4:
+        ref = OL.build(WL.Inputs(cfg).spans, cfg.window, cfg.seg_steps, 128, with_tiles=False)
+        cfg = cfg.with_(buffer_tokens=max(sg.length for sg in ref.segments) + int(rng.integers(0, 500)))
+    H = 8 * int(rng.integers(1, 81))
+    I = 8 * int(rng.integers(1, 151))
+    chunk = int(rng.choice([0, int(rng.integers(1, 900))]))
+    return cfg, H, I, chunk
+
+
+@pytest.mark.parametrize("i", range(6))
+def test_layer_random_shapes_parity(i):
+    cfg, H, I, chunk = _random_layer_case(i)
+    say(f"layer random case {i}: {cfg}")
+    _full_parity(f"random{i}", cfg, H, I, chunk)
 
 
 def _full_parity(name, cfg, H, I, chunk):
