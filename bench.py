@@ -655,7 +655,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--config", default="7b", help="workload name (7b, 7b_anchored, small, long, tiny)")
+    ap.add_argument("--config", default="7b", help="workload name (7b, 7b_anchored, 7b_tp4_rank, small, long, tiny)")
     ap.add_argument("--no-stepwise", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--sweep", action="store_true",

@@ -87,7 +87,12 @@ LONG = Config("long", 16, (10, 50), 512, 4096, (100, 600), 32, 5, 8, 28, 4, 128,
 # threshold delta = 5, clip 0.2 / 0.28 with ratio cap c = 3.
 SEVEN_B_ANCHORED = SEVEN_B.with_(name="7b_anchored", mode="anchored", window=5, seg_steps=5,
                                  eps_high=0.28, dual_clip=3.0)
-CONFIGS = {c.name: c for c in (TINY, SMALL, SEVEN_B, STEPWISE_7B, LONG, SEVEN_B_ANCHORED)}
+# One rank's share of the 7B-class batch under the paper's tensor parallelism
+# (TP = 4, heads and vocabulary split): 7 query heads of one kv head and a
+# quarter of the vocabulary (the collectives themselves are not modelled).
+SEVEN_B_TP4_RANK = SEVEN_B.with_(name="7b_tp4_rank", hq=7, hkv=1, vocab=151936 // 4)
+CONFIGS = {c.name: c for c in (TINY, SMALL, SEVEN_B, STEPWISE_7B, LONG, SEVEN_B_ANCHORED,
+                               SEVEN_B_TP4_RANK)}
 
 
 @dataclasses.dataclass
