@@ -145,9 +145,15 @@ typedef struct {
   int32_t *qt_ptr;        /* [G+1] CSR over q-tiles: non-skipped k-tiles, ascending */
   int32_t *qt_col;        /* [Z] global tile index of the k-tile */
   uint8_t *qt_cls;        /* [Z] SEG_TILE_PARTIAL or SEG_TILE_FULL */
+  int32_t *qt_ord;        /* [Z] the same entries per q-tile in the order the forward and dQ
+                             kernels walk them: FULL k-tiles first, then PARTIAL ones (each
+                             ascending); the global k-tile index, bit 31 set for PARTIAL */
   int32_t *kt_ptr;        /* [G+1] transposed CSR over k-tiles: non-skipped q-tiles, ascending */
   int32_t *kt_row;        /* [Z] */
   uint8_t *kt_cls;        /* [Z] */
+  int32_t *kt_ord;        /* [Z] the same entries per k-tile in the order the dK/dV kernel walks
+                             them: FULL q-tiles first, then PARTIAL ones (each descending); the
+                             global q-tile index, bit 31 set for PARTIAL */
   int64_t *seg_pairs;     /* [S] exact visible (query, key) pairs of each segment */
   int64_t *tile_nnz;      /* [1] non-skipped tiles */
   int32_t window;         /* set by seg_build_layout: the visibility window the

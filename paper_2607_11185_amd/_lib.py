@@ -58,7 +58,8 @@ class SegSizes(ctypes.Structure):
 class SegLayout(ctypes.Structure):
     _fields_ = [("seg_info", VP), ("tok_src", VP), ("tok_meta", VP), ("loss_pred_row", VP),
                 ("loss_tgt_src", VP), ("loss_traj", VP), ("tile_seg", VP), ("qt_ptr", VP),
-                ("qt_col", VP), ("qt_cls", VP), ("kt_ptr", VP), ("kt_row", VP), ("kt_cls", VP),
+                ("qt_col", VP), ("qt_cls", VP), ("qt_ord", VP), ("kt_ptr", VP), ("kt_row", VP),
+                ("kt_cls", VP), ("kt_ord", VP),
                 ("seg_pairs", VP), ("tile_nnz", VP),
                 ("window", ctypes.c_int32), ("tile", ctypes.c_int32),
                 ("xcd_rows", ctypes.c_int32 * 9), ("xcd_cols", ctypes.c_int32 * 9)]

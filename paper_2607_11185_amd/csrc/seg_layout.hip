@@ -496,7 +496,8 @@ __global__ void __launch_bounds__(64) k_fill_rows(const DevSeg *__restrict__ seg
                                                   const uint8_t *__restrict__ cls,
                                                   const int32_t *__restrict__ ptr,
                                                   int32_t *__restrict__ col,
-                                                  uint8_t *__restrict__ ccls) {
+                                                  uint8_t *__restrict__ ccls,
+                                                  int32_t *__restrict__ ord) {
   const int g = blockIdx.x, lane = threadIdx.x;
   const DevSeg d = segs[tile_seg[g]];
   const int i = g - d.qbase;
@@ -513,6 +514,23 @@ __global__ void __launch_bounds__(64) k_fill_rows(const DevSeg *__restrict__ seg
     }
     out += __popcll(m);
   }
+  // The walking order of the q-tile-stationary kernels: the same entries,
+  // FULL tiles first and PARTIAL ones after (each ascending), with bit 31
+  // marking PARTIAL.
+  out = ptr[g];
+  for (int pass = 0; pass < 2; ++pass) {
+    const uint8_t want = pass == 0 ? SEG_TILE_FULL : SEG_TILE_PARTIAL;
+    for (int j0 = 0; j0 <= i; j0 += 64) {
+      const int j = j0 + lane;
+      const uint8_t c = j <= i ? row[j] : 0;
+      const unsigned long long m = __ballot(c == want);
+      if (c == want) {
+        const int r = __popcll(m & ((1ull << lane) - 1));
+        ord[out + r] = (int32_t)((unsigned)(d.qbase + j) | (pass ? 0x80000000u : 0u));
+      }
+      out += __popcll(m);
+    }
+  }
 }
 
 // Transposed CSR columns: one wave per k-tile, q-tiles ascending.
@@ -521,11 +539,13 @@ __global__ void __launch_bounds__(64) k_fill_cols(const DevSeg *__restrict__ seg
                                                   const uint8_t *__restrict__ cls,
                                                   const int32_t *__restrict__ ptr,
                                                   int32_t *__restrict__ rowi,
-                                                  uint8_t *__restrict__ ccls) {
+                                                  uint8_t *__restrict__ ccls,
+                                                  int32_t *__restrict__ ord) {
   const int g = blockIdx.x, lane = threadIdx.x;
   const DevSeg d = segs[tile_seg[g]];
   const int j = g - d.qbase;
-  int out = ptr[g];
+  const int e0 = ptr[g];
+  int out = e0, nfull = 0;
   for (int i0 = j; i0 < d.nt; i0 += 64) {
     const int i = i0 + lane;
     const uint8_t c = i < d.nt ? cls[d.tri_base + (int64_t)i * (i + 1) / 2 + j] : 0;
@@ -536,6 +556,23 @@ __global__ void __launch_bounds__(64) k_fill_cols(const DevSeg *__restrict__ seg
       ccls[out + r] = c;
     }
     out += __popcll(m);
+    nfull += __popcll(__ballot(c == SEG_TILE_FULL));
+  }
+  // The walking order of the k-tile-stationary kernel: FULL q-tiles first,
+  // then PARTIAL ones, each descending, with bit 31 marking PARTIAL.
+  int rf = 0, rp = 0;  // ascending ranks so far within each class
+  for (int i0 = j; i0 < d.nt; i0 += 64) {
+    const int i = i0 + lane;
+    const uint8_t c = i < d.nt ? cls[d.tri_base + (int64_t)i * (i + 1) / 2 + j] : 0;
+    const unsigned long long mf = __ballot(c == SEG_TILE_FULL);
+    const unsigned long long mp = __ballot(c == SEG_TILE_PARTIAL);
+    const unsigned long long below = (1ull << lane) - 1;
+    if (c == SEG_TILE_FULL) ord[e0 + nfull - 1 - (rf + __popcll(mf & below))] = d.qbase + i;
+    if (c == SEG_TILE_PARTIAL)
+      ord[out - 1 - (rp + __popcll(mp & below))] =
+          (int32_t)((unsigned)(d.qbase + i) | 0x80000000u);
+    rf += __popcll(mf);
+    rp += __popcll(mp);
   }
 }
 
@@ -578,7 +615,8 @@ extern "C" seg_status seg_build_layout(const seg_problem *p, const seg_sizes *sz
     const int P = (int)sz->packed_tokens;
     if (S > 0) {
       SEG_CHECK(ws && out->seg_info && out->tok_src && out->tok_meta && out->tile_seg &&
-                    out->qt_ptr && out->qt_col && out->qt_cls && out->kt_ptr && out->kt_row &&
+                    out->qt_ptr && out->qt_col && out->qt_cls && out->qt_ord && out->kt_ptr &&
+                    out->kt_row && out->kt_ord &&
                     out->kt_cls && out->seg_pairs && out->tile_nnz,
                 SEG_ERR_ARG, "a layout array is NULL");
       SEG_CHECK(R == 0 || (out->loss_pred_row && out->loss_tgt_src && out->loss_traj),
@@ -640,10 +678,10 @@ extern "C" seg_status seg_build_layout(const seg_problem *p, const seg_sizes *sz
     k_scan<<<1, 1024, 0, stream>>>(d_kcnt, G, out->kt_ptr, nullptr);
     SEG_LAUNCH_CHECK();
     k_fill_rows<<<G, 64, 0, stream>>>(d_segs, out->tile_seg, d_cls, out->qt_ptr, out->qt_col,
-                                      out->qt_cls);
+                                      out->qt_cls, out->qt_ord);
     SEG_LAUNCH_CHECK();
     k_fill_cols<<<G, 64, 0, stream>>>(d_segs, out->tile_seg, d_cls, out->kt_ptr, out->kt_row,
-                                      out->kt_cls);
+                                      out->kt_cls, out->kt_ord);
     SEG_LAUNCH_CHECK();
   });
 }

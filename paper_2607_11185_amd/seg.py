@@ -75,8 +75,8 @@ class Layout:
     """Device arrays of one layout (torch tensors) and the C struct over them."""
 
     FIELDS = ["seg_info", "tok_src", "tok_meta", "loss_pred_row", "loss_tgt_src", "loss_traj",
-              "tile_seg", "qt_ptr", "qt_col", "qt_cls", "kt_ptr", "kt_row", "kt_cls",
-              "seg_pairs", "tile_nnz"]
+              "tile_seg", "qt_ptr", "qt_col", "qt_cls", "qt_ord", "kt_ptr", "kt_row", "kt_cls",
+              "kt_ord", "seg_pairs", "tile_nnz"]
 
     def __init__(self, sizes: SegSizes, device):
         import torch
@@ -99,9 +99,11 @@ class Layout:
         self.qt_ptr = e(G + 1, i32)
         self.qt_col = e(Z, i32)
         self.qt_cls = e(Z, u8)
+        self.qt_ord = e(Z, i32)
         self.kt_ptr = e(G + 1, i32)
         self.kt_row = e(Z, i32)
         self.kt_cls = e(Z, u8)
+        self.kt_ord = e(Z, i32)
         self.seg_pairs = e(S, i64)
         self.tile_nnz = e(1, i64)
         self.ws = e(sizes.workspace_bytes, u8)
@@ -115,8 +117,8 @@ class Layout:
                 "tok_meta": s.packed_tokens, "loss_pred_row": s.loss_rows,
                 "loss_tgt_src": s.loss_rows, "loss_traj": s.loss_rows,
                 "tile_seg": s.num_qtiles, "qt_ptr": s.num_qtiles + 1, "qt_col": nnz,
-                "qt_cls": nnz, "kt_ptr": s.num_qtiles + 1, "kt_row": nnz, "kt_cls": nnz,
-                "seg_pairs": s.num_segments, "tile_nnz": 1}
+                "qt_cls": nnz, "qt_ord": nnz, "kt_ptr": s.num_qtiles + 1, "kt_row": nnz,
+                "kt_cls": nnz, "kt_ord": nnz, "seg_pairs": s.num_segments, "tile_nnz": 1}
         out = {f: getattr(self, f)[:lens[f]].cpu().numpy() for f in self.FIELDS}
         out["seg_info"] = out["seg_info"].reshape(-1, 8)
         out["xcd_rows"] = np.array(self.c.xcd_rows[:], np.int64)

@@ -1,6 +1,7 @@
 """GPU layout (seg_build_layout through the C ABI) bit-exact against the oracle:
-tokens, loss rows, segment records, tile map (CSR and transposed CSR) and the
-exact visible-pair counts."""
+tokens, loss rows, segment records, tile map (CSR and transposed CSR, and the
+attention kernels' FULL-first walking orders of both) and the exact
+visible-pair counts."""
 import json
 import os
 
@@ -41,12 +42,43 @@ def _check_schedule(got):
     assert got["xcd_cols"].tolist() == _balance8(cols)
 
 
+def _want_order(cols, cls):
+    """One q-tile's walking order of the q-tile-stationary kernels: its listed
+    k-tiles with every FULL one first and the PARTIAL ones after, each in
+    ascending order, bit 31 marking PARTIAL (as int32)."""
+    cols = np.asarray(cols, np.int64)
+    cls = np.asarray(cls)
+    full, part = cols[cls == OL.CLS_FULL], cols[cls == OL.CLS_PARTIAL]
+    assert len(full) + len(part) == len(cols)
+    return np.concatenate([full, part | (1 << 31)]).astype(np.uint32).view(np.int32)
+
+
+def _check_order(got, g, e0, e1):
+    want = _want_order(got["qt_col"][e0:e1], got["qt_cls"][e0:e1])
+    assert np.array_equal(got["qt_ord"][e0:e1], want), ("qt_ord", g)
+
+
+def _check_col_order(got, g, e0, e1):
+    """One k-tile's walking order of the dK/dV kernel: FULL q-tiles first,
+    then PARTIAL ones, each descending, bit 31 marking PARTIAL."""
+    rows = np.asarray(got["kt_row"][e0:e1], np.int64)
+    cls = np.asarray(got["kt_cls"][e0:e1])
+    full, part = rows[cls == OL.CLS_FULL], rows[cls == OL.CLS_PARTIAL]
+    assert len(full) + len(part) == len(rows)
+    want = np.concatenate([full[::-1], part[::-1] | (1 << 31)]).astype(np.uint32).view(np.int32)
+    assert np.array_equal(got["kt_ord"][e0:e1], want), ("kt_ord", g)
+
+
 def _check_all(got, ref):
     for f in ("tok_src", "tok_meta", "loss_pred_row", "loss_tgt_src", "loss_traj", "tile_seg",
               "qt_ptr", "qt_col", "qt_cls", "kt_ptr", "kt_row", "kt_cls", "seg_pairs"):
         assert np.array_equal(got[f].astype(np.int64), getattr(ref, f).astype(np.int64)), f
     assert np.array_equal(got["seg_info"].astype(np.int64), ref.seg_info), "seg_info"
     assert int(got["tile_nnz"][0]) == len(ref.qt_col)
+    ptr, kptr = got["qt_ptr"], got["kt_ptr"]
+    for g in range(len(ptr) - 1):
+        _check_order(got, g, ptr[g], ptr[g + 1])
+        _check_col_order(got, g, kptr[g], kptr[g + 1])
     if len(got["qt_ptr"]) > 1:
         _check_schedule(got)
 
@@ -143,6 +175,7 @@ def test_configs_large_sampled(cfg):
             want = np.nonzero(cls[i])[0]
             assert np.array_equal(cols, want), (si, i)
             assert np.array_equal(got["qt_cls"][e0:e1], cls[i][want]), (si, i)
+            _check_order(got, g, e0, e1)
         for j in range(nt):
             g = base + j
             e0, e1 = got["kt_ptr"][g], got["kt_ptr"][g + 1]
@@ -150,6 +183,7 @@ def test_configs_large_sampled(cfg):
             want = np.nonzero(cls[:, j])[0]
             assert np.array_equal(rows, want), (si, j)
             assert np.array_equal(got["kt_cls"][e0:e1], cls[want, j]), (si, j)
+            _check_col_order(got, g, e0, e1)
     # with multi-turn segments, expired screenshots make skipped tiles; a
     # step-wise sample already holds only its last W screenshots
     total_lower = sum((n := -(-l // 128)) * (n + 1) // 2 for l in lens)
