@@ -293,22 +293,29 @@ __device__ __forceinline__ float sum8(const bf16x8 &v, float acc) {
 // XCDs (block b runs on XCD b % 8), each with its own L2.  XCD x takes the
 // contiguous tile range [r.b[x], r.b[x+1]) chosen by the layout so that the
 // ranges hold about equal work (the kernel ends with the slowest XCD), and
-// runs the nh heads of one tile back to back: heads of a tile read the same
-// key/value tiles, and neighbouring tiles of a segment read mostly the same
-// ones, so they meet in one L2.  `reverse` walks the range from its end (the
+// runs it kv head by kv head, with the grp query heads of one tile back to
+// back: those heads read the same key/value tiles, and neighbouring tiles of
+// a segment read mostly the same ones, so the blocks resident on one XCD
+// share one kv head's tiles in its L2 (the whole range of one kv head before
+// the next measured 1.5-2% faster for the forward and dQ than all nh heads
+// of a tile back to back).  `reverse` walks the range from its end (the
 // longest rows of each segment first).  The grid is 8 * max range * nh
 // blocks; blocks past their XCD's range exit at once.
 struct XcdRanges {
   int32_t b[9];
 };
 
-__device__ __forceinline__ bool xcd_block(const XcdRanges &r, int nh, bool reverse, int &tile,
-                                          int &head) {
+__device__ __forceinline__ bool xcd_block(const XcdRanges &r, int nh, int grp, bool reverse,
+                                          int &tile, int &head) {
   const int bx = blockIdx.x, x = bx & 7, i = bx >> 3;
   const int lo = r.b[x], C = r.b[x + 1] - lo;
-  const int t = i / nh;
-  if (t >= C) return false;
-  head = i - t * nh;
+  const int per = C * grp;  // blocks of one kv head's query heads over the range
+  if (per == 0) return false;
+  const int hk = i / per;
+  if (hk >= nh / grp) return false;
+  const int rem = i - hk * per;
+  const int t = rem / grp;
+  head = hk * grp + (rem - t * grp);
   tile = lo + (reverse ? C - 1 - t : t);
   return true;
 }
@@ -412,7 +419,7 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd(
   __shared__ __attribute__((aligned(16))) int sM0[64], sM1[64];
 
   int g, h;
-  if (!xcd_block(xr, hq, true, g, h)) return;
+  if (!xcd_block(xr, hq, hq / hkv, true, g, h)) return;
   const int hk = h / (hq / hkv);
   const TileRows tr = tile_rows(seg_info, tile_seg, g);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -894,7 +901,7 @@ __global__ void __launch_bounds__(256, 2) k_attn_bwd_dq(
   __shared__ __attribute__((aligned(16))) int sM0[64], sM1[64];
 
   int g, h;
-  if (!xcd_block(xr, hq, true, g, h)) return;
+  if (!xcd_block(xr, hq, hq / hkv, true, g, h)) return;
   const int hk = h / (hq / hkv);
   const TileRows tr = tile_rows(seg_info, tile_seg, g);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
