@@ -16,6 +16,7 @@
 #include <climits>
 #include <cmath>
 #include <mutex>
+#include <type_traits>
 
 #include "common.h"
 
@@ -120,17 +121,15 @@ __global__ void __launch_bounds__(256) k_delta(const TI *__restrict__ o, const T
 //
 // Tiles of 64 rows x d (row-major, bf16) are multi-buffered in LDS: the
 // loads of the next unit are in flight while the current one is computed.
-// The forward and dQ kernels fill with direct 16-byte buffer->LDS loads; the
-// dK/dV kernel stages the next unit in registers (see the note on wait counts
-// below).  All tile loads go through buffer resources that start at the
-// segment's first row, so a lane's offset inside a tile is fixed for the
-// kernel and a unit adds one scalar; rows past the segment read as zeros.
-// Rows are stored with a
-// 16-byte-chunk swizzle that keeps both 16-byte row reads (MFMA operands
-// contracting over d; 16 lanes per LDS cycle) and 4x16 transpose reads
-// (ds_read_b64_tr_b16: operands contracting over the rows; 32 lanes per
-// cycle) free of bank conflicts on 64 four-byte banks, so no transposed copy
-// of any tensor is needed.  Every lane's swizzled offsets are computed once;
+// Every kernel fills them with direct 16-byte buffer->LDS loads (see the
+// note on wait counts below).  All tile loads go through buffer resources
+// that start at the segment's first row, so a lane's offset inside a tile is
+// fixed for the kernel and a unit adds one scalar; rows past the segment read
+// as zeros.  Rows are stored with a 16-byte-chunk swizzle that keeps both
+// 16-byte row reads (MFMA operands contracting over d; 16 lanes per LDS
+// cycle) and 4x16 transpose reads (ds_read_b64_tr_b16: operands contracting
+// over the rows; 32 lanes per cycle) free of bank conflicts on 64 four-byte
+// banks, so no transposed copy of any tensor is needed.  Every lane's swizzled offsets are computed once;
 // inside the loops a read is a register offset plus an immediate.
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
@@ -196,31 +195,6 @@ __device__ __forceinline__ bf16x8 frag_tr(const char *tile, int R, int offa, int
   return r;
 }
 
-// Lane coordinates of a register-staged 64-row tile fill by NW waves (PW
-// 16-byte chunks per lane, each wave instruction covering 1 KB of the tile,
-// lane-contiguous in LDS); the swizzle is applied by choosing which global
-// chunk each lane loads.  `store` writes the staged registers to LDS.
-template <int D, int NW>
-struct StagePlan {
-  static constexpr int CPR = D / 8, PW = 64 * CPR / (64 * NW);
-  static_assert(PW >= 1, "tile too small for the wave count");
-  int row[PW], chunk[PW];  // tile row and element offset of the lane's 16 bytes
-  __device__ __forceinline__ void init(int wave, int lane) {
-#pragma unroll
-    for (int i = 0; i < PW; ++i) {
-      const int s = (wave * PW + i) * 64 + lane;
-      row[i] = s / CPR;
-      chunk[i] = ((s % CPR) ^ swz<D>(row[i])) * 8;
-    }
-  }
-  __device__ __forceinline__ void store(unsigned short *tile, const u16x8 (&st)[PW], int wave,
-                                        int lane) const {
-#pragma unroll
-    for (int i = 0; i < PW; ++i)
-      *reinterpret_cast<u16x8 *>(tile + ((wave * PW + i) * 64 + lane) * 8) = st[i];
-  }
-};
-
 // Raw buffer resource over [base, base + bytes): loads past the end return
 // zeros, so a tile fill needs no clamping of its rows.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *base, unsigned bytes) {
@@ -269,11 +243,11 @@ __device__ __forceinline__ void buf64_dw(void *dst, __amdgpu_buffer_rsrc_t rs, i
 // buffers are distinct __restrict__ parameters: a direct load's LDS write is
 // counted with the global loads, and without the no-alias facts the compiler
 // would wait for the loads in flight before the first LDS read of the
-// compute.  Every LDS access of a step goes through those parameters.  While
-// a direct load is in flight the compiler also gives up counted LDS waits
-// (every wait becomes lgkmcnt(0)), which serialises read-ahead; the dK/dV
-// kernel, whose loads must stay in flight across a whole step, therefore
-// stages its next unit in registers instead.
+// compute.  Every LDS access of a step goes through those parameters (an
+// access without them, such as one indexed by a run-time buffer number, waits
+// for every direct load in flight).  While a direct load is in flight the
+// compiler also gives up counted LDS waits (every wait becomes lgkmcnt(0)),
+// which serialises read-ahead.
 
 __device__ __forceinline__ void wait_all_and_sync() {
   __builtin_amdgcn_s_waitcnt(0);
@@ -576,8 +550,8 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd(
 //   dS side: dP = dO V^T, P <- LDS, dS = P (dP - Delta), dK += dS^T Q
 // The dS side works one unit behind the P side, so the P of a unit crosses
 // the barrier that ends a step; Q/dO tiles therefore live in three buffers
-// (the P side's unit, the dS side's unit, and the next unit being staged in
-// registers).  Units are 64-row halves of the listed q-tiles, for every query
+// (the P side's unit, the dS side's unit, and the next unit being loaded;
+// the step is unrolled three ways so that each is a compile-time buffer).  Units are 64-row halves of the listed q-tiles, for every query
 // head of the group, in the order of `kt_ord` (FULL q-tiles first, then the
 // PARTIAL ones, each from the segment's last q-tile down).  No atomics.
 template <int D, class TO>
@@ -591,10 +565,15 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
     int hq, int hkv, int W,
     float scale_log2, float scale, long P, TO *__restrict__ dk, TO *__restrict__ dv) {
   constexpr int KK = D / 16, T64 = 64 * D, DB = D / 32, NB = 3;
-  __shared__ __attribute__((aligned(16))) unsigned short sQ[NB][T64], sD[NB][T64];
+  // three Q/dO buffers (and their per-row values) as distinct objects, so
+  // that the direct loads into one provably write other LDS than the reads
+  // of the other two
+  __shared__ __attribute__((aligned(16))) unsigned short sQ0[T64], sQ1[T64], sQ2[T64];
+  __shared__ __attribute__((aligned(16))) unsigned short sD0[T64], sD1[T64], sD2[T64];
   __shared__ __attribute__((aligned(16))) unsigned short sP[2][64 * TQ];
-  __shared__ __attribute__((aligned(16))) float sL[NB][64], sE[NB][64];
-  __shared__ __attribute__((aligned(16))) int sM[NB][64];
+  __shared__ __attribute__((aligned(16))) float sL0[64], sL1[64], sL2[64];
+  __shared__ __attribute__((aligned(16))) float sE0[64], sE1[64], sE2[64];
+  __shared__ __attribute__((aligned(16))) int sM0[64], sM1[64], sM2[64];
 
   int g, hk;
   {
@@ -637,64 +616,50 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
   const long q_stride = (long)hq * D;
   const int e0 = kt_ptr[g], e1 = kt_ptr[g + 1];
 
-  // register-staged fill of one unit by all 8 waves: Q and dO rows, and one
-  // per-row value by waves 0-2 (log2-sum-exp, Delta, turn).  Buffer
-  // resources start at the segment's first row of the group's first head;
-  // a unit adds a scalar byte offset, and rows past the end read as zeros.
-  StagePlan<D, 8> sp;
-  sp.init(wave, lane);
-  constexpr int PW = StagePlan<D, 8>::PW;
+  // Fill of one unit by all 8 waves with direct buffer->LDS loads: Q and dO
+  // rows, and one per-row value by waves 0-2 (log2-sum-exp, Delta, turn).
+  // The Q/dO resources start at the segment's first row of the group's first
+  // head and a unit adds a scalar byte offset; the per-row resources cover
+  // one head's rows of the segment, so rows past the segment (the next
+  // segment's, or buffer padding whose log-sum-exp and Delta were never
+  // computed) read as zeros and no non-finite value can reach dS = P (dP -
+  // Delta) through a masked P = 0.
   const int qrow_bytes = (int)(q_stride * 2);
-  int voff[PW];
-#pragma unroll
-  for (int i = 0; i < PW; ++i) voff[i] = sp.row[i] * qrow_bytes + sp.chunk[i] * 2;
+  BufFill<D, 8> fq;
+  fq.init(wave, lane, qrow_bytes);
   const long hbase = (long)hk * grp * D + (long)tr.start * q_stride;
   const unsigned qbytes = (unsigned)(tr.len * (long)qrow_bytes);
   const __amdgpu_buffer_rsrc_t rQ = make_rsrc(q + hbase, qbytes);
   const __amdgpu_buffer_rsrc_t rO = make_rsrc(dout + hbase, qbytes);
-  const long pbase = (long)hk * grp * P + tr.start;
-  const unsigned pbytes = (unsigned)(((long)(grp - 1) * P + tr.len) * 4);
-  // the wave index as a scalar: the resource is then built in scalar
+  // the wave index as a scalar: the resources are then built in scalar
   // registers (a resource held in vector registers needs a waterfall loop
   // around every load)
   const int swave = __builtin_amdgcn_readfirstlane(wave);
-  const __amdgpu_buffer_rsrc_t rS = make_rsrc(swave == 0 ? (const void *)(lse2 + pbase)
-                                              : swave == 1 ? (const void *)(delta + pbase)
-                                                           : (const void *)(tok_meta + tr.start),
-                                              swave < 2 ? pbytes : (unsigned)tr.len * 4);
-  u16x8 stq[PW], sto[PW];
-  int stv = 0, st_vrows = 0;
-  auto load = [&](int r0, int vrows, int hi) __attribute__((always_inline)) {
+  const unsigned rbytes = (unsigned)tr.len * 4;
+  auto issue = [&](int r0, int hi, unsigned short *__restrict__ nQ, unsigned short *__restrict__ nD,
+                   float *__restrict__ nL, float *__restrict__ nE, int *__restrict__ nM)
+                   __attribute__((always_inline)) {
     const int so = r0 * qrow_bytes + hi * D * 2;
-#pragma unroll
-    for (int i = 0; i < PW; ++i) {
-      stq[i] = __builtin_bit_cast(u16x8, __builtin_amdgcn_raw_buffer_load_b128(rQ, voff[i], so, 0));
-      sto[i] = __builtin_bit_cast(u16x8, __builtin_amdgcn_raw_buffer_load_b128(rO, voff[i], so, 0));
+    fq.issue(nQ, rQ, so, wave);
+    fq.issue(nD, rO, so, wave);
+    if (swave < 3) {
+      const long hrow = (long)(hk * grp + hi) * P + tr.start;
+      const __amdgpu_buffer_rsrc_t rS =
+          make_rsrc(swave == 0 ? (const void *)(lse2 + hrow)
+                    : swave == 1 ? (const void *)(delta + hrow)
+                                 : (const void *)(tok_meta + tr.start),
+                    rbytes);
+      buf64_dw(swave == 0 ? (void *)nL : swave == 1 ? (void *)nE : (void *)nM, rS, lane, r0 * 4);
     }
-    // The per-row resource of a head spans the following rows of the packed
-    // batch (other segments, or buffer padding whose log-sum-exp and Delta
-    // were never computed): rows past the unit's valid rows are replaced by
-    // zeros when stored, so no non-finite value can reach dS = P (dP - Delta)
-    // through a masked P = 0.
-    if (swave < 3)
-      stv = __builtin_amdgcn_raw_buffer_load_b32(rS, lane * 4,
-                                                 (swave < 2 ? hi * (int)P * 4 : 0) + r0 * 4, 0);
-    st_vrows = vrows;
-  };
-  auto store = [&](int b) __attribute__((always_inline)) {
-    sp.store(sQ[b], stq, wave, lane);
-    sp.store(sD[b], sto, wave, lane);
-    const int val = lane < st_vrows ? stv : 0;
-    if (wave == 0) sL[b][lane] = __builtin_bit_cast(float, val);
-    else if (wave == 1) sE[b][lane] = __builtin_bit_cast(float, val);
-    else if (wave == 2) sM[b][lane] = val;
   };
 
   // P side: one unit (rows r0 .. r0 + vrows - 1, PARTIAL or ragged if masked)
-  auto p_side = [&](const int r0, const int vrows, const bool masked, const int b, const int pb)
-                    __attribute__((always_inline)) {
-    const char *cQ = reinterpret_cast<const char *>(sQ[b]);
-    const char *cD = reinterpret_cast<const char *>(sD[b]);
+  auto p_side = [&](const int r0, const int vrows, const bool masked,
+                    const unsigned short *__restrict__ bQ, const unsigned short *__restrict__ bD,
+                    const float *__restrict__ bL, const int *__restrict__ bM,
+                    unsigned short *__restrict__ bP) __attribute__((always_inline)) {
+    const char *cQ = reinterpret_cast<const char *>(bQ);
+    const char *cD = reinterpret_cast<const char *>(bD);
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
       bf16x8 aq[KK];
@@ -705,7 +670,7 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
       for (int kk = 0; kk < KK; ++kk) s = mfma32(aq[kk], xf[kk], s);
 #pragma unroll
       for (int rg = 0; rg < 4; ++rg) {
-        const f32x4 L4 = *reinterpret_cast<const f32x4 *>(&sL[b][qb * 32 + 8 * rg + 4 * hh]);
+        const f32x4 L4 = *reinterpret_cast<const f32x4 *>(&bL[qb * 32 + 8 * rg + 4 * hh]);
 #pragma unroll
         for (int j = 0; j < 4; ++j) s[rg * 4 + j] = fmaf(s[rg * 4 + j], scale_log2, -L4[j]);
       }
@@ -713,7 +678,7 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
 #pragma unroll
         for (int rg = 0; rg < 4; ++rg) {
           const int base = qb * 32 + 8 * rg + 4 * hh;
-          const i32x4 M4 = *reinterpret_cast<const i32x4 *>(&sM[b][base]);
+          const i32x4 M4 = *reinterpret_cast<const i32x4 *>(&bM[base]);
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             const int ql = base + j;
@@ -728,7 +693,7 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
       pa[0] = pack8(s, 0);
       pa[1] = pack8(s, 8);
       // P in the accumulator's lane order, read back by the dS wave of the same keys
-      bf16x8 *pdst = reinterpret_cast<bf16x8 *>(sP[pb]) + ((qb * 4 + kg) * 2) * 64 + lane;
+      bf16x8 *pdst = reinterpret_cast<bf16x8 *>(bP) + ((qb * 4 + kg) * 2) * 64 + lane;
       pdst[0] = pa[0];
       pdst[64] = pa[1];
 #pragma unroll
@@ -743,9 +708,11 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
     }
   };
   // dS side: one unit, whose P was written in the previous step
-  auto ds_side = [&](const int b, const int pb) __attribute__((always_inline)) {
-    const char *cQ = reinterpret_cast<const char *>(sQ[b]);
-    const char *cD = reinterpret_cast<const char *>(sD[b]);
+  auto ds_side = [&](const unsigned short *__restrict__ bQ, const unsigned short *__restrict__ bD,
+                     const float *__restrict__ bE, const unsigned short *__restrict__ bP)
+                     __attribute__((always_inline)) {
+    const char *cQ = reinterpret_cast<const char *>(bQ);
+    const char *cD = reinterpret_cast<const char *>(bD);
     f32x16 dpb[2];
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
@@ -759,11 +726,11 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
 #pragma unroll
     for (int qb = 0; qb < 2; ++qb) {
       f32x16 dp = dpb[qb];
-      const bf16x8 *psrc = reinterpret_cast<const bf16x8 *>(sP[pb]) + ((qb * 4 + kg) * 2) * 64 + lane;
+      const bf16x8 *psrc = reinterpret_cast<const bf16x8 *>(bP) + ((qb * 4 + kg) * 2) * 64 + lane;
       const bf16x8 p0 = psrc[0], p1 = psrc[64];
 #pragma unroll
       for (int rg = 0; rg < 4; ++rg) {
-        const f32x4 D4 = *reinterpret_cast<const f32x4 *>(&sE[b][qb * 32 + 8 * rg + 4 * hh]);
+        const f32x4 D4 = *reinterpret_cast<const f32x4 *>(&bE[qb * 32 + 8 * rg + 4 * hh]);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int r = rg * 4 + j;
@@ -787,16 +754,44 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
   };
 
   if (e0 < e1) {
-    // Unit state as scalars: CSR entry, half, query head, first row.
+    // Unit state as scalars: walking-order entry, half, query head, first row.
     int ce = e0, chalf = 0, chi = 0;
     int cr0 = (((int)((unsigned)kt_ord[ce] & 0x7fffffffu)) - tr.qbase) * TQ;
     int cpart = (int)((unsigned)kt_ord[ce] >> 31);
-    load(cr0, min(64, tr.len - cr0), 0);
-    store(0);
-    __syncthreads();
+    issue(cr0, 0, sQ0, sD0, sL0, sE0, sM0);
+    wait_all_and_sync();
     bool have_cur = true;  // the P side has a unit this step
-    int b = 0, pb = 0;     // buffers of the P side's unit (the dS side uses the previous ones)
-    for (int n = 0;; ++n) {
+    int pb = 0;            // P buffer of the P side's unit (the dS side uses the other)
+    bool first = true;
+    // The work of one step, with every LDS buffer it touches as a distinct
+    // __restrict__ parameter: the direct loads into the next unit's buffers
+    // (n*) are then known not to write what the P side (c*), the dS side
+    // (p*) and the P exchange (wP, rP) access, so no LDS access waits for
+    // them.
+    auto body = [&](const bool more, const int nr0, const int nhi, unsigned short *__restrict__ nQ,
+                    unsigned short *__restrict__ nD, float *__restrict__ nL,
+                    float *__restrict__ nE, int *__restrict__ nM,
+                    const unsigned short *__restrict__ cQ, const unsigned short *__restrict__ cD,
+                    const float *__restrict__ cL, const int *__restrict__ cM,
+                    const unsigned short *__restrict__ pQ, const unsigned short *__restrict__ pD,
+                    const float *__restrict__ pE, unsigned short *__restrict__ wP,
+                    const unsigned short *__restrict__ rP) __attribute__((always_inline)) {
+      if (more) issue(nr0, nhi, nQ, nD, nL, nE, nM);
+      if (side == 0) {
+        if (have_cur) {
+          const int vrows = min(64, tr.len - cr0);
+          p_side(cr0, vrows, (cpart | (vrows < 64)) != 0, cQ, cD, cL, cM, wP);
+        }
+      } else if (!first) {
+        ds_side(pQ, pD, pE, rP);
+      }
+    };
+    // One step on Q/dO buffer B (the P side's unit; the dS side's is the
+    // previous buffer, the next unit's loads go to the following one), with
+    // the buffers as compile-time indices: the direct loads in flight then
+    // provably write other LDS than the step reads.
+    auto step = [&](auto bc) __attribute__((always_inline)) -> bool {
+      constexpr int B = decltype(bc)::value, NBUF = (B + 1) % NB, PBUF = (B + NB - 1) % NB;
       // next unit: other half of this tile, else next head, else next entry
       int ne = ce, nhalf = 0, nhi = chi, nr0 = 0, npart = cpart;
       bool more = false;
@@ -819,34 +814,34 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
           nhi = 0;
         }
       }
-      const int nb = b == NB - 1 ? 0 : b + 1;
-      if (more) load(nr0, min(64, tr.len - nr0), nhi);
-      if (side == 0) {
-        if (have_cur) {
-          const int vrows = min(64, tr.len - cr0);
-          p_side(cr0, vrows, (cpart | (vrows < 64)) != 0, b, pb);
-        }
-      } else if (n > 0) {
-        ds_side(b == 0 ? NB - 1 : b - 1, pb ^ 1);
-      }
-      if (more) store(nb);
+      unsigned short *const Q[NB] = {sQ0, sQ1, sQ2}, *const Dd[NB] = {sD0, sD1, sD2};
+      float *const Lr[NB] = {sL0, sL1, sL2}, *const Er[NB] = {sE0, sE1, sE2};
+      int *const Mr[NB] = {sM0, sM1, sM2};
+      body(more, nr0, nhi, Q[NBUF], Dd[NBUF], Lr[NBUF], Er[NBUF], Mr[NBUF], Q[B], Dd[B], Lr[B],
+           Mr[B], Q[PBUF], Dd[PBUF], Er[PBUF], sP[pb], sP[pb ^ 1]);
       __syncthreads();
-      if (!have_cur) break;
+      if (!have_cur) return false;
       have_cur = more;
       ce = ne;
       chalf = nhalf;
       chi = nhi;
       cr0 = nr0;
       cpart = npart;
-      b = nb;
       pb ^= 1;
+      first = false;
+      return true;
+    };
+    for (;;) {
+      if (!step(std::integral_constant<int, 0>{})) break;
+      if (!step(std::integral_constant<int, 1>{})) break;
+      if (!step(std::integral_constant<int, 2>{})) break;
     }
   }
 
   // stage through LDS (RP key rows per pass) for coalesced stores;
   // accumulator D[i = key][j = d]
   wait_all_and_sync();
-  TO *st = reinterpret_cast<TO *>(&sQ[0][0]);
+  TO *st = reinterpret_cast<TO *>(sQ0);
   constexpr int CH = 16 / sizeof(TO);   // elements per 16-byte chunk
   constexpr int RP = 128 / sizeof(TO);  // key rows per pass (16 KB)
   const float mul = side == 0 ? 1.f : scale;
