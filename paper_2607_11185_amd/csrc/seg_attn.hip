@@ -81,7 +81,9 @@ __global__ void k_f32_to_bf16(const float *__restrict__ x, unsigned short *__res
 }
 
 // Delta[h][row] = sum_d dO[row][h][d] * O[row][h][d]  (D/8 lanes per (row, head)),
-// and the row's log-sum-exp in log2 units for the backward kernels.
+// stored negated (the backward kernels start their dP accumulators from
+// -Delta, so dP - Delta costs no instruction), and the row's log-sum-exp in
+// log2 units for the backward kernels.
 template <class TI, int D>
 __global__ void __launch_bounds__(256) k_delta(const TI *__restrict__ o, const TI *__restrict__ dout,
                                                const float *__restrict__ lse, int hq, long P,
@@ -112,7 +114,7 @@ __global__ void __launch_bounds__(256) k_delta(const TI *__restrict__ o, const T
   if (ok && part == 0) {
     const long row = pair / hq;
     const int h = (int)(pair % hq);
-    delta[(long)h * P + row] = acc;
+    delta[(long)h * P + row] = -acc;
     lse2[(long)h * P + row] = lse[(long)h * P + row] * LOG2E;
   }
 }
@@ -551,9 +553,10 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd(
 // The dS side works one unit behind the P side, so the P of a unit crosses
 // the barrier that ends a step; Q/dO tiles therefore live in three buffers
 // (the P side's unit, the dS side's unit, and the next unit being loaded;
-// the step is unrolled three ways so that each is a compile-time buffer).  Units are 64-row halves of the listed q-tiles, for every query
-// head of the group, in the order of `kt_ord` (FULL q-tiles first, then the
-// PARTIAL ones, each from the segment's last q-tile down).  No atomics.
+// the step is unrolled three ways so that each is a compile-time buffer).
+// Units are 64-row halves of the listed q-tiles, for every query head of the
+// group, in the order of `kt_ord` (FULL q-tiles first, then the PARTIAL
+// ones, each from the segment's last q-tile down).  No atomics.
 template <int D, class TO>
 __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
     const unsigned short *__restrict__ q, const unsigned short *__restrict__ k,
@@ -719,7 +722,13 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
       bf16x8 ad[KK];
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) ad[kk] = frag_row<D>(cD, qb * 32, lo.row[kk]);
-      dpb[qb] = f32x16{};
+      // dP - Delta: the chain starts from the rows' -Delta
+#pragma unroll
+      for (int rg = 0; rg < 4; ++rg) {
+        const f32x4 N4 = *reinterpret_cast<const f32x4 *>(&bE[qb * 32 + 8 * rg + 4 * hh]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) dpb[qb][rg * 4 + j] = N4[j];
+      }
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) dpb[qb] = mfma32(ad[kk], xf[kk], dpb[qb]);
     }
@@ -729,15 +738,7 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
       const bf16x8 *psrc = reinterpret_cast<const bf16x8 *>(bP) + ((qb * 4 + kg) * 2) * 64 + lane;
       const bf16x8 p0 = psrc[0], p1 = psrc[64];
 #pragma unroll
-      for (int rg = 0; rg < 4; ++rg) {
-        const f32x4 D4 = *reinterpret_cast<const f32x4 *>(&bE[qb * 32 + 8 * rg + 4 * hh]);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int r = rg * 4 + j;
-          const float pr = (float)(r < 8 ? p0[r] : p1[r - 8]);
-          dp[r] = pr * (dp[r] - D4[j]);
-        }
-      }
+      for (int r = 0; r < 16; ++r) dp[r] *= (float)(r < 8 ? p0[r] : p1[r - 8]);
       bf16x8 dsa[2];
       dsa[0] = pack8(dp, 0);
       dsa[1] = pack8(dp, 8);
@@ -907,7 +908,7 @@ __global__ void __launch_bounds__(256, 2) k_attn_bwd_dq(
   const long qrow_abs = tr.start + qr;
   const int qstep = tok_meta[qrow_abs] >> 2;
   const float l2 = lse2[(long)h * P + qrow_abs];
-  const float dlt = delta[(long)h * P + qrow_abs];
+  const float ndlt = delta[(long)h * P + qrow_abs];  // -Delta of the lane's query
 
   bf16x8 qf[KK], df[KK];
   {
@@ -953,7 +954,10 @@ __global__ void __launch_bounds__(256, 2) k_attn_bwd_dq(
         ak[kk] = frag_row<D>(sK, kb * 32, lo.row[kk]);
         av[kk] = frag_row<D>(sV, kb * 32, lo.row[kk]);
       }
-      f32x16 s = f32x16{}, dp = f32x16{};
+      // dP^T - Delta: the chain starts from -Delta (one value per lane's query)
+      f32x16 s = f32x16{}, dp;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) dp[r] = ndlt;
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) {
         s = mfma32(ak[kk], qf[kk], s);
@@ -973,13 +977,13 @@ __global__ void __launch_bounds__(256, 2) k_attn_bwd_dq(
             const bool vis = qvalid & (kl < u.vrows) & (u.r0 + kl <= qr) &
                              (qstep < key_expiry(M4[j], W));
             const float x = vis ? fmaf(s[r], scale_log2, -l2) : -INFINITY;
-            s[r] = __builtin_amdgcn_exp2f(x) * (dp[r] - dlt);
+            s[r] = __builtin_amdgcn_exp2f(x) * dp[r];
           }
         }
       } else {
 #pragma unroll
         for (int r = 0; r < 16; ++r)
-          s[r] = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -l2)) * (dp[r] - dlt);
+          s[r] = __builtin_amdgcn_exp2f(fmaf(s[r], scale_log2, -l2)) * dp[r];
       }
 #pragma unroll
       for (int c2 = 0; c2 < 2; ++c2) {
