@@ -634,17 +634,17 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
   const unsigned qbytes = (unsigned)(tr.len * (long)qrow_bytes);
   const __amdgpu_buffer_rsrc_t rQ = make_rsrc(q + hbase, qbytes);
   const __amdgpu_buffer_rsrc_t rO = make_rsrc(dout + hbase, qbytes);
-  // the wave index as a scalar: the resources are then built in scalar
-  // registers (a resource held in vector registers needs a waterfall loop
-  // around every load)
+  // the wave index as a scalar: the resources and the direct loads' LDS
+  // addresses are then built in scalar registers (a resource held in vector
+  // registers needs a waterfall loop around every load)
   const int swave = __builtin_amdgcn_readfirstlane(wave);
   const unsigned rbytes = (unsigned)tr.len * 4;
   auto issue = [&](int r0, int hi, unsigned short *__restrict__ nQ, unsigned short *__restrict__ nD,
                    float *__restrict__ nL, float *__restrict__ nE, int *__restrict__ nM)
                    __attribute__((always_inline)) {
     const int so = r0 * qrow_bytes + hi * D * 2;
-    fq.issue(nQ, rQ, so, wave);
-    fq.issue(nD, rO, so, wave);
+    fq.issue(nQ, rQ, so, swave);
+    fq.issue(nD, rO, so, swave);
     if (swave < 3) {
       const long hrow = (long)(hk * grp + hi) * P + tr.start;
       const __amdgpu_buffer_rsrc_t rS =
@@ -937,11 +937,14 @@ __global__ void __launch_bounds__(256, 2) k_attn_bwd_dq(
       make_rsrc(v + (long)hk * D + (long)tr.start * kv_stride, (unsigned)tr.len * row_bytes);
   const __amdgpu_buffer_rsrc_t rM = make_rsrc(tok_meta + tr.start, (unsigned)tr.len * 4);
 
+  // the wave index as a scalar: the direct loads' LDS addresses are then
+  // formed in scalar registers (no readfirstlane per load)
+  const int swave = __builtin_amdgcn_readfirstlane(wave);
   auto issue = [&](const Unit &u, unsigned short *__restrict__ nK, unsigned short *__restrict__ nV,
                    int *__restrict__ nM) __attribute__((always_inline)) {
-    fp.issue(nK, rK, u.r0 * row_bytes, wave);
-    fp.issue(nV, rV, u.r0 * row_bytes, wave);
-    if (wave == 0) buf64_dw(nM, rM, lane, u.r0 * 4);
+    fp.issue(nK, rK, u.r0 * row_bytes, swave);
+    fp.issue(nV, rV, u.r0 * row_bytes, swave);
+    if (swave == 0) buf64_dw(nM, rM, lane, u.r0 * 4);
   };
   auto compute = [&](const Unit &u, const char *__restrict__ sK, const char *__restrict__ sV,
                      const int *__restrict__ sM) __attribute__((always_inline)) {
