@@ -357,8 +357,8 @@ seg_status seg_layer_bwd(const seg_layout *L, const seg_sizes *sz, const seg_lay
  * Kernel timing.  While enabled, every kernel the library launches is
  * bracketed by HIP events recorded on its launch stream.  seg_profile_read sums
  * the device time of all recorded launches of one kernel (names: "layout",
- * "attn_prep", "attn_fwd", "attn_delta", "attn_bwd_dkdv", "attn_bwd_dq",
- * "logits", "row_loss", "dz", "lp_prep", "dh", "dw", and for the layer
+ * "attn_prep", "attn_fwd", "attn_delta" (fp32 inputs only: with bf16 inputs
+ * the dQ kernel forms Delta itself), "attn_bwd_dkdv", "attn_bwd_dq", "logits", "row_loss", "dz", "lp_prep", "dh", "dw", and for the layer
  * "ly_norm", "ly_rope", "ly_proj", "ly_mlp", "ly_wgrad", "ly_misc"), waiting for them to
  * finish; seg_profile_reset forgets the records.  Timing adds two event
  * records per launch and is off by default.  These three calls are the one

@@ -882,12 +882,17 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
 
 // dQ: one block = one q-tile x one query head, 4 waves of 32 query rows;
 // units are 64-key halves of the listed k-tiles.  Recomputes S^T and dP^T per
-// unit; dQ^T += K^T dS^T with K^T by transpose reads.
-template <int D, class TO>
+// unit; dQ^T += K^T dS^T with K^T by transpose reads.  With FUSE (bf16
+// inputs) the kernel also forms each of its rows' -Delta = -(dO . O) and
+// log2-sum-exp from O and the natural-log LSE, uses them, and writes them for
+// the dK/dV kernel that runs after it (no separate pre-pass); without FUSE it
+// reads what the pre-pass wrote.
+template <int D, class TO, bool FUSE>
 __global__ void __launch_bounds__(256, 2) k_attn_bwd_dq(
     const unsigned short *__restrict__ q, const unsigned short *__restrict__ k,
     const unsigned short *__restrict__ v, const unsigned short *__restrict__ dout,
-    const float *__restrict__ lse2, const float *__restrict__ delta,
+    const unsigned short *__restrict__ o, const float *__restrict__ lse,
+    float *__restrict__ lse2, float *__restrict__ delta,
     const int32_t *__restrict__ seg_info, const int32_t *__restrict__ tile_seg,
     const int32_t *__restrict__ tok_meta, const int32_t *__restrict__ qt_ptr,
     const int32_t *__restrict__ qt_ord, const XcdRanges xr, int hq, int hkv, int W,
@@ -907,8 +912,6 @@ __global__ void __launch_bounds__(256, 2) k_attn_bwd_dq(
   const int qr = tr.row0 + (qvalid ? qloc : 0);
   const long qrow_abs = tr.start + qr;
   const int qstep = tok_meta[qrow_abs] >> 2;
-  const float l2 = lse2[(long)h * P + qrow_abs];
-  const float ndlt = delta[(long)h * P + qrow_abs];  // -Delta of the lane's query
 
   bf16x8 qf[KK], df[KK];
   {
@@ -919,6 +922,32 @@ __global__ void __launch_bounds__(256, 2) k_attn_bwd_dq(
       qf[kk] = lds8(qp + kk * 16 + hh * 8);
       df[kk] = lds8(dp + kk * 16 + hh * 8);
     }
+  }
+  float l2, ndlt;  // log2-sum-exp and -Delta of the lane's query
+  const long rv = (long)h * P + qrow_abs;
+  if constexpr (FUSE) {
+    // the lane holds half of the row's d (the other half in lane + 32):
+    // bf16 products are exact in fp32, summed in a fixed order
+    const unsigned short *op = o + (qrow_abs * hq + h) * D;
+    float acc = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      const bf16x8 of = lds8(op + kk * 16 + hh * 8);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        acc = __builtin_amdgcn_fdot2_f32_bf16(bf16x2{df[kk][2 * i], df[kk][2 * i + 1]},
+                                              bf16x2{of[2 * i], of[2 * i + 1]}, acc, false);
+    }
+    acc += __shfl_xor(acc, 32, 64);
+    ndlt = -acc;
+    l2 = lse[rv] * LOG2E;
+    if (qvalid && hh == 0) {
+      delta[rv] = ndlt;
+      lse2[rv] = l2;
+    }
+  } else {
+    l2 = lse2[rv];
+    ndlt = delta[rv];
   }
   f32x16 dqacc[DB];
 #pragma unroll
@@ -1111,11 +1140,24 @@ void bwd_impl(const seg_layout *L, const seg_sizes *sz, int hq, int hkv, float s
               hipStream_t st) {
   const int G = sz->num_qtiles;
   const long P = sz->packed_tokens;
-  {
+  // bf16 inputs: the dQ kernel forms -Delta and the log2-sum-exp of its rows
+  // and runs first; fp32 inputs: the pre-pass forms them from the unrounded
+  // O and dO
+  constexpr bool FUSE = sizeof(TI) == 2;
+  if constexpr (!FUSE) {
     const long threads = P * hq * (D / 8);
     ProfScope prof("attn_delta", st);
     k_delta<TI, D><<<(int)((threads + 255) / 256), 256, 0, st>>>(o_raw, dout_raw, lse, hq, P, delta,
                                                                  lse2);
+    SEG_LAUNCH_CHECK();
+  }
+  {
+    ProfScope prof("attn_bwd_dq", st);
+    const XcdRanges xr = xcd_ranges(L->xcd_rows);
+    k_attn_bwd_dq<D, TO, FUSE><<<xcd_grid(xr, hq), 256, 0, st>>>(
+        q, k, v, dout, reinterpret_cast<const unsigned short *>(o_raw), lse, lse2, delta,
+        L->seg_info, L->tile_seg, L->tok_meta, L->qt_ptr, L->qt_ord, xr, hq, hkv, L->window,
+        scale * LOG2E, scale, P, static_cast<TO *>(dq));
     SEG_LAUNCH_CHECK();
   }
   {
@@ -1127,12 +1169,6 @@ void bwd_impl(const seg_layout *L, const seg_sizes *sz, int hq, int hkv, float s
         static_cast<TO *>(dk), static_cast<TO *>(dv));
     SEG_LAUNCH_CHECK();
   }
-  ProfScope prof("attn_bwd_dq", st);
-  const XcdRanges xr = xcd_ranges(L->xcd_rows);
-  k_attn_bwd_dq<D, TO><<<xcd_grid(xr, hq), 256, 0, st>>>(
-      q, k, v, dout, lse2, delta, L->seg_info, L->tile_seg, L->tok_meta, L->qt_ptr, L->qt_ord,
-      xr, hq, hkv, L->window, scale * LOG2E, scale, P, static_cast<TO *>(dq));
-  SEG_LAUNCH_CHECK();
 }
 
 }  // namespace
