@@ -119,6 +119,41 @@ __global__ void __launch_bounds__(256) k_delta(const TI *__restrict__ o, const T
   }
 }
 
+// Largest squared key norm of each (segment, kv head), a bound on the
+// forward's scores: |q . k| <= |q| |k|.  One block per (k-tile, kv head), two
+// lanes per row; squared norms are >= 0, so their float bits order as
+// unsigned integers and the maximum is an integer atomic (any order gives
+// the same result).  The targets start at 0.
+template <int D>
+__global__ void __launch_bounds__(256) k_key_norm(const unsigned short *__restrict__ k,
+                                                  const int32_t *__restrict__ seg_info,
+                                                  const int32_t *__restrict__ tile_seg, int hkv,
+                                                  unsigned *__restrict__ kn2) {
+  constexpr int LPR = 256 / TQ, PER = D / LPR;
+  const int g = blockIdx.x, hk = blockIdx.y;
+  const TileRows tr = tile_rows(seg_info, tile_seg, g);
+  const int r = threadIdx.x / LPR, part = threadIdx.x % LPR;
+  float n2 = 0.f;
+  if (r < tr.nrows) {
+    const unsigned short *src = k + ((long)(tr.start + tr.row0 + r) * hkv + hk) * D + part * PER;
+#pragma unroll
+    for (int i = 0; i < PER; i += 8) {
+      const bf16x8 x = lds8(src + i);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) n2 = fmaf((float)x[j], (float)x[j], n2);
+    }
+  }
+  n2 += __shfl_xor(n2, 1, 64);
+#pragma unroll
+  for (int off = 2; off < 64; off <<= 1) n2 = fmaxf(n2, __shfl_xor(n2, off, 64));
+  __shared__ float wmax[4];
+  if ((threadIdx.x & 63) == 0) wmax[threadIdx.x >> 6] = n2;
+  __syncthreads();
+  if (threadIdx.x == 0)
+    atomicMax(kn2 + (long)tile_seg[g] * hkv + hk,
+              __float_as_uint(fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]))));
+}
+
 // ------------------------------------------------------------- pipelined kernels
 //
 // Tiles of 64 rows x d (row-major, bf16) are multi-buffered in LDS: the
@@ -138,6 +173,7 @@ typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
 // 16-byte chunk swizzle of row `row`: a bijection on row % 16 (a 16-lane row
 // read of one logical chunk hits 16 distinct chunks), and rows 4m..4m+3 differ
@@ -387,9 +423,9 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd(
     const unsigned short *__restrict__ q, const unsigned short *__restrict__ k,
     const unsigned short *__restrict__ v, const int32_t *__restrict__ seg_info,
     const int32_t *__restrict__ tile_seg, const int32_t *__restrict__ tok_meta,
-    const int32_t *__restrict__ qt_ptr, const int32_t *__restrict__ qt_ord, const XcdRanges xr,
-    int hq, int hkv, int W, float scale_log2, long P, TO *__restrict__ o,
-    float *__restrict__ lse) {
+    const int32_t *__restrict__ qt_ptr, const int32_t *__restrict__ qt_ord,
+    const float *__restrict__ kn2, const XcdRanges xr, int hq, int hkv, int W, float scale_log2,
+    long P, TO *__restrict__ o, float *__restrict__ lse) {
   constexpr int KK = D / 16, DB = D / 32, T64 = 64 * D;
   __shared__ __attribute__((aligned(16))) unsigned short sK0[T64], sK1[T64], sV0[T64], sV1[T64];
   __shared__ __attribute__((aligned(16))) int sM0[64], sM1[64];
@@ -411,10 +447,26 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd(
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) qf[kk] = lds8(qrow + kk * 16 + hh * 8);
   }
+  // Fixed offset: when |q| max|k| * scale * log2(e) <= 64 for every row of
+  // the wave (max over the segment's keys), every score in log2 units lies
+  // in [-64, 64], so P = exp2(S) needs no running max (P and its sums stay
+  // within fp32 and bf16 range, and relative precision does not depend on
+  // the offset).  Other waves keep the lazily rescaled running max.
+  bool zoff;
+  {
+    float qn2 = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) qn2 = fmaf((float)qf[kk][j], (float)qf[kk][j], qn2);
+    qn2 += __shfl_xor(qn2, 32, 64);
+    const float kmax2 = kn2[(long)tile_seg[g] * hkv + hk];
+    zoff = __all(!qvalid || qn2 * kmax2 * (scale_log2 * scale_log2) <= 4096.f);
+  }
   f32x16 oacc[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db) oacc[db] = f32x16{};
-  float m_run = -INFINITY, l_run = 0.f;
+  float m_run = zoff ? 0.f : -INFINITY, l_run = 0.f;
 
   LaneOffsets<D> lo;
   lo.init(lane, 0);
@@ -465,24 +517,26 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd(
           }
         }
     }
-    float mloc = -INFINITY;
+    if (!zoff) {
+      float mloc = -INFINITY;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, sacc[kb][r]);
-    mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64)) * scale_log2;
-    // Lazy rescaling: the running max (log2 units) only moves when a row's
-    // tile max exceeds it by more than 8, so unnormalised P stays below 2^8.
-    const bool grow = mloc > m_run + 8.f;
-    if (__any(grow)) {
-      // lanes that keep their max keep alpha = 1: with an unset (-inf) max,
-      // exp2(m_run - m_new) would be exp2(NaN)
-      const float m_new = grow ? mloc : m_run;
-      const float alpha = grow ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.f;
-      l_run *= alpha;
+        for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, sacc[kb][r]);
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64)) * scale_log2;
+      // Lazy rescaling: the running max (log2 units) only moves when a row's
+      // tile max exceeds it by more than 8, so unnormalised P stays below 2^8.
+      const bool grow = mloc > m_run + 8.f;
+      if (__any(grow)) {
+        // lanes that keep their max keep alpha = 1: with an unset (-inf)
+        // max, exp2(m_run - m_new) would be exp2(NaN)
+        const float m_new = grow ? mloc : m_run;
+        const float alpha = grow ? __builtin_amdgcn_exp2f(m_run - m_new) : 1.f;
+        l_run *= alpha;
 #pragma unroll
-      for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
-      m_run = m_new;
+        for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
+        m_run = m_new;
+      }
     }
     const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
     bf16x8 pf[2][2];
@@ -1061,7 +1115,7 @@ __global__ void __launch_bounds__(256, 2) k_attn_bwd_dq(
 // ------------------------------------------------------------- host side
 
 struct AttnWs {
-  size_t delta, lse2, qb, kb, vb, dob, total;
+  size_t kn2, delta, lse2, qb, kb, vb, dob, total;
 };
 
 AttnWs attn_ws(const seg_sizes &sz, seg_dtype dt, int hq, int hkv, int d, int bwd) {
@@ -1073,6 +1127,7 @@ AttnWs attn_ws(const seg_sizes &sz, seg_dtype dt, int hq, int hkv, int d, int bw
     return o;
   };
   const size_t P = (size_t)std::max<int64_t>(1, sz.packed_tokens);
+  w.kn2 = take((size_t)std::max(1, sz.num_segments) * hkv * sizeof(float));
   if (bwd) {
     w.delta = take(P * hq * sizeof(float));
     w.lse2 = take(P * hq * sizeof(float));
@@ -1122,13 +1177,17 @@ void to_bf16(const void *x, unsigned short *y, long n, hipStream_t st) {
 template <int D, class TO>
 void fwd_impl(const seg_layout *L, const seg_sizes *sz, int hq, int hkv, float scale,
               const unsigned short *q, const unsigned short *k, const unsigned short *v, void *o,
-              float *lse, hipStream_t st) {
+              float *lse, unsigned *kn2, hipStream_t st) {
   const int G = sz->num_qtiles;
   ProfScope prof("attn_fwd", st);
+  fill32(kn2, (long)sz->num_segments * hkv, 0u, st);
+  k_key_norm<D><<<dim3(G, hkv), 256, 0, st>>>(k, L->seg_info, L->tile_seg, hkv, kn2);
+  SEG_LAUNCH_CHECK();
   const XcdRanges xr = xcd_ranges(L->xcd_rows);
   k_attn_fwd<D, TO><<<xcd_grid(xr, hq), 256, 0, st>>>(
-      q, k, v, L->seg_info, L->tile_seg, L->tok_meta, L->qt_ptr, L->qt_ord, xr, hq, hkv,
-      L->window, scale * LOG2E, sz->packed_tokens, static_cast<TO *>(o), lse);
+      q, k, v, L->seg_info, L->tile_seg, L->tok_meta, L->qt_ptr, L->qt_ord,
+      reinterpret_cast<const float *>(kn2), xr, hq, hkv, L->window, scale * LOG2E,
+      sz->packed_tokens, static_cast<TO *>(o), lse);
   SEG_LAUNCH_CHECK();
 }
 
@@ -1196,6 +1255,7 @@ extern "C" seg_status seg_attn_fwd(const seg_layout *L, const seg_sizes *sz, seg
     SEG_CHECK(std::isfinite(softmax_scale), SEG_ERR_ARG, "softmax_scale is not finite");
     char *base = static_cast<char *>(ws);
     const long P = sz->packed_tokens;
+    unsigned *kn2 = reinterpret_cast<unsigned *>(base + w.kn2);
     const unsigned short *qb, *kb, *vb;
     if (dt == SEG_F32) {
       unsigned short *q2 = reinterpret_cast<unsigned short *>(base + w.qb);
@@ -1213,11 +1273,11 @@ extern "C" seg_status seg_attn_fwd(const seg_layout *L, const seg_sizes *sz, seg
       vb = static_cast<const unsigned short *>(v);
     }
     if (d == 128) {
-      if (dt == SEG_F32) fwd_impl<128, float>(L, sz, hq, hkv, softmax_scale, qb, kb, vb, o, lse, stream);
-      else fwd_impl<128, unsigned short>(L, sz, hq, hkv, softmax_scale, qb, kb, vb, o, lse, stream);
+      if (dt == SEG_F32) fwd_impl<128, float>(L, sz, hq, hkv, softmax_scale, qb, kb, vb, o, lse, kn2, stream);
+      else fwd_impl<128, unsigned short>(L, sz, hq, hkv, softmax_scale, qb, kb, vb, o, lse, kn2, stream);
     } else {
-      if (dt == SEG_F32) fwd_impl<64, float>(L, sz, hq, hkv, softmax_scale, qb, kb, vb, o, lse, stream);
-      else fwd_impl<64, unsigned short>(L, sz, hq, hkv, softmax_scale, qb, kb, vb, o, lse, stream);
+      if (dt == SEG_F32) fwd_impl<64, float>(L, sz, hq, hkv, softmax_scale, qb, kb, vb, o, lse, kn2, stream);
+      else fwd_impl<64, unsigned short>(L, sz, hq, hkv, softmax_scale, qb, kb, vb, o, lse, kn2, stream);
     }
   });
 }

@@ -46,6 +46,7 @@ CASES = {
     # forward's running max moves by more than 8 log2 units after it is
     # finite, so the online-softmax rescale runs (asserted from the inputs)
     "med_ramped_keys": MED.with_(seed=16),
+    "med_mixed_offset": MED.with_(seed=21, hq=8, hkv=2),
     # no prompt: rows whose first listed 64-key unit is an expired screenshot
     # (fully masked for them) and whose first visible key comes later
     "med_no_prompt": MED.with_(prompt_len=0, seed=19, steps=(5, 7)),
@@ -55,6 +56,10 @@ CASES = {
     "tiny": WL.TINY,
 }
 RAMPED = {"med_ramped_keys"}
+# queries of every third 32-row group scaled by 8: in one launch some waves
+# have every score bounded by |q| max|k| within 64 log2 units (fixed offset,
+# no running max) and others do not (running max)
+MIXED = {"med_mixed_offset"}
 
 
 def _key_factors(ref, P):
@@ -64,6 +69,30 @@ def _key_factors(ref, P):
     for sg in ref.segments:
         f[sg.start:sg.start + sg.length] = 4.0 ** np.minimum(2, np.arange(sg.length) // 128)
     return f
+
+
+def _query_factors(ref, P):
+    """Per packed row: 8 for every third group of 32 rows of a segment
+    (a power of two, so scaling bf16 queries is exact), else 1."""
+    f = np.ones(P)
+    for sg in ref.segments:
+        f[sg.start:sg.start + sg.length] = np.where(np.arange(sg.length) // 32 % 3 == 0, 8.0, 1.0)
+    return f
+
+
+def _offset_waves(q, k, scale, grp):
+    """(waves with every row's bound |q| max|k| * scale * log2 e <= 64, waves
+    without), a wave being 32 consecutive rows of the segment for one query
+    head and max|k| running over the segment's keys of its kv head."""
+    kmax = np.sqrt((k.astype(np.float64) ** 2).sum(-1).max(0))  # [hkv]
+    qn = np.sqrt((q.astype(np.float64) ** 2).sum(-1))           # [len, hq]
+    bound = qn * kmax[np.arange(q.shape[1]) // grp][None, :] * scale * np.log2(np.e)
+    fixed = other = 0
+    for w0 in range(0, q.shape[0], 32):
+        ok = (bound[w0:w0 + 32] <= 64).all(0)
+        fixed += int(ok.sum())
+        other += int((~ok).sum())
+    return fixed, other
 
 
 def _unit_scores(q, k, mask, scale, h, grp):
@@ -165,6 +194,10 @@ def _full_parity(name, cfg):
     fac = _key_factors(ref, run.P) if name in RAMPED else None
     if fac is not None:
         run.k = run.k * torch.from_numpy(fac).to(run.dev, torch.bfloat16)[:, None, None]
+    qfac = _query_factors(ref, run.P) if name in MIXED else None
+    if qfac is not None:
+        run.q = run.q * torch.from_numpy(qfac).to(run.dev, torch.bfloat16)[:, None, None]
+    waves = [0, 0]
     run.fwd()
     run.bwd()
     torch.cuda.synchronize()
@@ -180,6 +213,11 @@ def _full_parity(name, cfg):
             events += _rescale_events(q, k, mask, run.scale, cfg.hq, cfg.hkv)
         if name == "med_no_prompt":
             masked_first += _masked_first_units(mask)
+        if qfac is not None:
+            q = q * qfac[sg.start:sg.start + sg.length, None, None]
+            fx, ot = _offset_waves(q, k, run.scale, cfg.hq // cfg.hkv)
+            waves[0] += fx
+            waves[1] += ot
         o_r, lse_r = OA.forward(q, k, v, mask, run.scale)
         dq_r, dk_r, dv_r = OA.backward(q, k, v, mask, run.scale, dout)
         rows = slice(sg.start, sg.start + sg.length)
@@ -214,6 +252,9 @@ def _full_parity(name, cfg):
     if name == "med_no_prompt":
         say(f"  rows whose first listed unit is fully masked: {masked_first}")
         assert masked_first > 0
+    if qfac is not None:
+        say(f"  waves with bounded scores {waves[0]}, without {waves[1]}")
+        assert waves[0] > 0 and waves[1] > 0
 
 
 def test_padding_rows_hold_nan():
