@@ -182,7 +182,9 @@ seg_status seg_layout_query(const seg_problem *p, seg_sizes *out);
 seg_status seg_build_layout(const seg_problem *p, const seg_sizes *sz, seg_layout *out,
                             void *ws, size_t ws_bytes, hipStream_t stream);
 
-/* Workspace of seg_attn_fwd (bwd = 0) or seg_attn_bwd (bwd = 1). */
+/* Workspace of seg_attn_fwd (bwd = 0: the largest key norm of each segment
+ * and kv head, plus bf16 copies of fp32 inputs) or seg_attn_bwd (bwd = 1:
+ * per-row -Delta and log2-sum-exp, plus bf16 copies of fp32 inputs). */
 size_t seg_attn_workspace_bytes(const seg_sizes *sz, seg_dtype dt, int32_t hq, int32_t hkv,
                                 int32_t d, int32_t bwd);
 

@@ -1127,7 +1127,7 @@ AttnWs attn_ws(const seg_sizes &sz, seg_dtype dt, int hq, int hkv, int d, int bw
     return o;
   };
   const size_t P = (size_t)std::max<int64_t>(1, sz.packed_tokens);
-  w.kn2 = take((size_t)std::max(1, sz.num_segments) * hkv * sizeof(float));
+  if (!bwd) w.kn2 = take((size_t)std::max(1, sz.num_segments) * hkv * sizeof(float));
   if (bwd) {
     w.delta = take(P * hq * sizeof(float));
     w.lse2 = take(P * hq * sizeof(float));
