@@ -49,6 +49,18 @@ __device__ __forceinline__ int key_expiry(int meta, int W) {
   return ((meta & 3) == SEG_KIND_IMAGE) ? (meta >> 2) + W : INT_MAX;
 }
 
+// The window test of a key's turn/kind word (turn << 2 | kind) in one
+// unsigned compare: with the kind bits xored with IMAGE and rotated to the
+// top, an image key reads as its turn tau and any other kind as >= 2^30.  A
+// query of turn t sees an image key iff t < tau + W, i.e. iff the rotated
+// word is >= max(t - W + 1, 0).
+__device__ __forceinline__ unsigned window_word(int meta) {
+  return __builtin_rotateright32((unsigned)meta ^ SEG_KIND_IMAGE, 2);
+}
+__device__ __forceinline__ unsigned window_floor(int qstep, int W) {
+  return (unsigned)max(qstep - W + 1, 0);
+}
+
 __device__ __forceinline__ bf16x8 lds8(const unsigned short *p) {
   return *reinterpret_cast<const bf16x8 *>(p);
 }
@@ -499,7 +511,10 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd(
 #pragma unroll
       for (int kk = 0; kk < KK; ++kk) sacc[kb] = mfma32(ak[kk], qf[kk], sacc[kb]);
     }
-    // raw scores; masked entries -inf (scale > 0 keeps the order)
+    // raw scores; masked entries -inf (scale > 0 keeps the order).  The
+    // forward keeps the direct per-element test: with the cheaper form of
+    // the backward kernels the compiler schedules the unmasked path of this
+    // kernel less well (1% slower overall in measurement).
     if (__builtin_expect(u.partial, 0)) {
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
@@ -654,7 +669,10 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
   const int kloc = kg * 32 + col;
   const bool kvalid = kloc < tr.nrows;
   const int kr = tr.row0 + (kvalid ? kloc : 0);
+  // a query row sees the lane's key only if its turn/kind word is below
+  // kexp4 = 4 x (the key's expiry turn), INT_MAX for keys that never expire
   const int kexp = key_expiry(tok_meta[tr.start + kr], W);
+  const int kexp4 = kexp >= (1 << 29) ? INT_MAX : kexp << 2;
 
   // K fragments (P side) or V fragments (dS side) of the wave's 32 keys
   bf16x8 xf[KK];
@@ -732,14 +750,18 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
         for (int j = 0; j < 4; ++j) s[rg * 4 + j] = fmaf(s[rg * 4 + j], scale_log2, -L4[j]);
       }
       if (masked) {  // uniform branch: only the exponents change
+        // the lane's query rows qc + 4 hh in [qlo, qhi) are inside the unit
+        // and not before its key
+        const int qhi = vrows - 4 * hh;
+        const int qlo = kvalid ? kr - r0 - 4 * hh : qhi;
 #pragma unroll
         for (int rg = 0; rg < 4; ++rg) {
-          const int base = qb * 32 + 8 * rg + 4 * hh;
-          const i32x4 M4 = *reinterpret_cast<const i32x4 *>(&bM[base]);
+          const int qc0 = qb * 32 + 8 * rg;
+          const i32x4 M4 = *reinterpret_cast<const i32x4 *>(&bM[qc0 + 4 * hh]);
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            const int ql = base + j;
-            const bool vis = kvalid & (ql < vrows) & (kr <= r0 + ql) & ((M4[j] >> 2) < kexp);
+            const int qc = qc0 + j;
+            const bool vis = (qc >= qlo) & (qc < qhi) & (M4[j] < kexp4);
             s[rg * 4 + j] = vis ? s[rg * 4 + j] : -INFINITY;
           }
         }
@@ -1053,15 +1075,18 @@ __global__ void __launch_bounds__(256, 2) k_attn_bwd_dq(
       // One uniform branch; inside, the predicate is bitwise (no branch per
       // element).
       if (__builtin_expect(u.partial, 0)) {
+        // the lane's keys kc + 4 hh < lim are inside the unit and not after
+        // its query
+        const int lim = (qvalid ? min(u.vrows, qr - u.r0 + 1) : 0) - 4 * hh;
+        const unsigned wfloor = window_floor(qstep, W);
 #pragma unroll
         for (int rg = 0; rg < 4; ++rg) {
-          const int kb0 = kb * 32 + 8 * rg + 4 * hh;
-          const i32x4 M4 = *reinterpret_cast<const i32x4 *>(sM + kb0);
+          const int kc0 = kb * 32 + 8 * rg;
+          const i32x4 M4 = *reinterpret_cast<const i32x4 *>(sM + kc0 + 4 * hh);
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            const int r = rg * 4 + j, kl = kb0 + j;
-            const bool vis = qvalid & (kl < u.vrows) & (u.r0 + kl <= qr) &
-                             (qstep < key_expiry(M4[j], W));
+            const int r = rg * 4 + j;
+            const bool vis = (kc0 + j < lim) & (window_word(M4[j]) >= wfloor);
             const float x = vis ? fmaf(s[r], scale_log2, -l2) : -INFINITY;
             s[r] = __builtin_amdgcn_exp2f(x) * dp[r];
           }
