@@ -46,7 +46,7 @@ KERNEL_FLOP_PER_PAIR_D = {"attn_fwd": 4, "attn_bwd_dkdv": 6, "attn_bwd_dq": 2}
 # kernel source they were taken on and are reported only while it is unchanged.
 MEASURED_TRAFFIC = {
     "source": "paper_2607_11185_amd/csrc/seg_attn.hip",
-    "source_sha256": "0296b94406c5d13bc2e671b642fbbdb0a7de3cf48c49d6c8bf1a8ec7489a46ab",
+    "source_sha256": "06cbe1cde187cb637af5a784bbccb108f3ff330f9ac7fad772bbd28fe9a496bf",
     "config": "7b",
     "bytes_per_launch": {"attn_bwd_dkdv": 307.75e9, "attn_fwd": 65.81e9,
                          "attn_bwd_dq": 98.02e9},
