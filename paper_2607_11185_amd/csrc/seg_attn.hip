@@ -233,10 +233,14 @@ __device__ __forceinline__ bf16x8 frag_row(const char *tile, int R, int off) {
 // Operand fragment contracting over tile rows: lane l receives column
 // n(l) of rows R + kperm(8h + j), j = 0..7 (h = l/32), the MFMA k-order of
 // accumulator-held operands.
+// `bias` is a constant already added to offa and offb (see the dK/dV kernel).
 template <int D>
-__device__ __forceinline__ bf16x8 frag_tr(const char *tile, int R, int offa, int offb) {
-  const v4i16 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)(tile + R * D * 2 + offa));
-  const v4i16 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)(tile + R * D * 2 + offb));
+__device__ __forceinline__ bf16x8 frag_tr(const char *tile, int R, int offa, int offb,
+                                          int bias = 0) {
+  const v4i16 a =
+      __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)(tile + (R * D * 2 - bias + offa)));
+  const v4i16 b =
+      __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16 *)(tile + (R * D * 2 - bias + offb)));
   const bf16x4 a4 = __builtin_bit_cast(bf16x4, a), b4 = __builtin_bit_cast(bf16x4, b);
   bf16x8 r;
   r[0] = a4[0]; r[1] = a4[1]; r[2] = a4[2]; r[3] = a4[3];
@@ -639,8 +643,10 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
   // three Q/dO buffers (and their per-row values) as distinct objects, so
   // that the direct loads into one provably write other LDS than the reads
   // of the other two
-  __shared__ __attribute__((aligned(16))) unsigned short sQ0[T64], sQ1[T64], sQ2[T64];
-  __shared__ __attribute__((aligned(16))) unsigned short sD0[T64], sD1[T64], sD2[T64];
+  // Q/dO tiles first (LDS is laid out by decreasing alignment), buffers 0
+  // and 1 in the low 64 KB and buffer 2 above it
+  __shared__ __attribute__((aligned(1024))) unsigned short sQ0[T64], sQ1[T64], sD0[T64], sD1[T64];
+  __shared__ __attribute__((aligned(512))) unsigned short sQ2[T64], sD2[T64];
   __shared__ __attribute__((aligned(16))) unsigned short sP[2][64 * TQ];
   __shared__ __attribute__((aligned(16))) float sL0[64], sL1[64], sL2[64];
   __shared__ __attribute__((aligned(16))) float sE0[64], sE1[64], sE2[64];
@@ -687,6 +693,20 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
 
   LaneOffsets<D> lo;
   lo.init(lane, 0);
+  // Transposed-read offsets with 64 KB added, hidden from the compiler: for
+  // d = 128 a tile of buffer 2 lies above the 64 KB that an LDS
+  // instruction's offset field reaches, and with these its reads carry the
+  // tile's address in that field instead of adding it to the lane offset per
+  // read.
+  constexpr int HIBUF = 2, HIBIAS = 65536;
+  constexpr bool HIGH2 = 4 * T64 * 2 >= HIBIAS;  // buffers 0 and 1 fill the low 64 KB
+  int trah[DB], trbh[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    trah[db] = lo.tra[db] + HIBIAS;
+    trbh[db] = lo.trb[db] + HIBIAS;
+    asm volatile("" : "+v"(trah[db]), "+v"(trbh[db]));
+  }
   const long q_stride = (long)hq * D;
   const int e0 = kt_ptr[g], e1 = kt_ptr[g + 1];
 
@@ -728,7 +748,7 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
   };
 
   // P side: one unit (rows r0 .. r0 + vrows - 1, PARTIAL or ragged if masked)
-  auto p_side = [&](const int r0, const int vrows, const bool masked,
+  auto p_side = [&](auto hi_tag, const int r0, const int vrows, const bool masked,
                     const unsigned short *__restrict__ bQ, const unsigned short *__restrict__ bD,
                     const float *__restrict__ bL, const int *__restrict__ bM,
                     unsigned short *__restrict__ bP) __attribute__((always_inline)) {
@@ -779,14 +799,17 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
         bf16x8 bo[DB];
 #pragma unroll
         for (int db = 0; db < DB; ++db)
-          bo[db] = frag_tr<D>(cD, qb * 32 + c2 * 16, lo.tra[db], lo.trb[db]);
+          bo[db] = decltype(hi_tag)::value
+                       ? frag_tr<D>(cD, qb * 32 + c2 * 16, trah[db], trbh[db], HIBIAS)
+                       : frag_tr<D>(cD, qb * 32 + c2 * 16, lo.tra[db], lo.trb[db]);
 #pragma unroll
         for (int db = 0; db < DB; ++db) acc[db] = mfma32(pa[c2], bo[db], acc[db]);
       }
     }
   };
   // dS side: one unit, whose P was written in the previous step
-  auto ds_side = [&](const unsigned short *__restrict__ bQ, const unsigned short *__restrict__ bD,
+  auto ds_side = [&](auto hi_tag, const unsigned short *__restrict__ bQ,
+                     const unsigned short *__restrict__ bD,
                      const float *__restrict__ bE, const unsigned short *__restrict__ bP)
                      __attribute__((always_inline)) {
     const char *cQ = reinterpret_cast<const char *>(bQ);
@@ -822,7 +845,9 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
         bf16x8 bq[DB];
 #pragma unroll
         for (int db = 0; db < DB; ++db)
-          bq[db] = frag_tr<D>(cQ, qb * 32 + c2 * 16, lo.tra[db], lo.trb[db]);
+          bq[db] = decltype(hi_tag)::value
+                       ? frag_tr<D>(cQ, qb * 32 + c2 * 16, trah[db], trbh[db], HIBIAS)
+                       : frag_tr<D>(cQ, qb * 32 + c2 * 16, lo.tra[db], lo.trb[db]);
 #pragma unroll
         for (int db = 0; db < DB; ++db) acc[db] = mfma32(dsa[c2], bq[db], acc[db]);
       }
@@ -844,7 +869,8 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
     // (n*) are then known not to write what the P side (c*), the dS side
     // (p*) and the P exchange (wP, rP) access, so no LDS access waits for
     // them.
-    auto body = [&](const bool more, const int nr0, const int nhi, unsigned short *__restrict__ nQ,
+    auto body = [&](auto cur_hi, auto prev_hi, const bool more, const int nr0, const int nhi,
+                    unsigned short *__restrict__ nQ,
                     unsigned short *__restrict__ nD, float *__restrict__ nL,
                     float *__restrict__ nE, int *__restrict__ nM,
                     const unsigned short *__restrict__ cQ, const unsigned short *__restrict__ cD,
@@ -856,10 +882,10 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
       if (side == 0) {
         if (have_cur) {
           const int vrows = min(64, tr.len - cr0);
-          p_side(cr0, vrows, (cpart | (vrows < 64)) != 0, cQ, cD, cL, cM, wP);
+          p_side(cur_hi, cr0, vrows, (cpart | (vrows < 64)) != 0, cQ, cD, cL, cM, wP);
         }
       } else if (!first) {
-        ds_side(pQ, pD, pE, rP);
+        ds_side(prev_hi, pQ, pD, pE, rP);
       }
     };
     // One step on Q/dO buffer B (the P side's unit; the dS side's is the
@@ -893,7 +919,9 @@ __global__ void __launch_bounds__(512, 1) k_attn_bwd_dkdv(
       unsigned short *const Q[NB] = {sQ0, sQ1, sQ2}, *const Dd[NB] = {sD0, sD1, sD2};
       float *const Lr[NB] = {sL0, sL1, sL2}, *const Er[NB] = {sE0, sE1, sE2};
       int *const Mr[NB] = {sM0, sM1, sM2};
-      body(more, nr0, nhi, Q[NBUF], Dd[NBUF], Lr[NBUF], Er[NBUF], Mr[NBUF], Q[B], Dd[B], Lr[B],
+      body(std::integral_constant<bool, HIGH2 && B == HIBUF>{},
+           std::integral_constant<bool, HIGH2 && PBUF == HIBUF>{},
+           more, nr0, nhi, Q[NBUF], Dd[NBUF], Lr[NBUF], Er[NBUF], Mr[NBUF], Q[B], Dd[B], Lr[B],
            Mr[B], Q[PBUF], Dd[PBUF], Er[PBUF], sP[pb], sP[pb ^ 1]);
       __syncthreads();
       if (!have_cur) return false;
