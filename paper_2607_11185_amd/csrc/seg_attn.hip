@@ -569,7 +569,9 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd(
       rsum = sum8(pf[kb][0], rsum);
       rsum = sum8(pf[kb][1], rsum);
     }
-    rsum += __shfl_xor(rsum, 32, 64);
+    // l_run holds the sum over this lane's keys only: both half-waves of a
+    // row share its max and rescale factors, so their sums are combined once
+    // at the end
     l_run += rsum;
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -599,6 +601,7 @@ __global__ void __launch_bounds__(256, 2) k_attn_fwd(
   walk_units(make_unit(qt_ord, e0, 0, tr.qbase, tr.len), step, issue, next, sK0, sV0, sM0,
              sK1, sV1, sM1);
 
+  l_run += __shfl_xor(l_run, 32, 64);
   if (qvalid) {
     const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
     const long row = tr.start + qr;
